@@ -1,0 +1,14 @@
+"""CPU oracle for the verifier scoring pass (VideoSpeculateRAG, Section 3.1,
+Eq. 6-7).
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, by the smoke check and by the
+benchmark's CPU-baseline leg. The product path never imports, calls or links
+anything here, and nothing here imports the product package.
+"""
+from .decoder import (apply_rope, causal_attention, decoder_layer, embed_prefix,
+                      forward_hidden, rms_norm, rope_angles, score_bruteforce,
+                      score_shared_prefix, select, silu, token_log_probs)
+
+__all__ = ["apply_rope", "causal_attention", "decoder_layer", "embed_prefix",
+           "forward_hidden", "rms_norm", "rope_angles", "score_bruteforce",
+           "score_shared_prefix", "select", "silu", "token_log_probs"]
