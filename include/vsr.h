@@ -1,0 +1,147 @@
+/*
+ * vsr.h -- C ABI of the MI355X (gfx950) verifier scoring pass of
+ * VideoSpeculateRAG (arxiv 2601.01513).
+ *
+ * The paper's verification stage (Section 3.1, Eq. 6-7) scores every drafted
+ * answer a_i with the heavyweight verifier conditioned on the question and the
+ * video, score_i = Verifier(Q, V, a_i), and selects a* = argmax_i score_i.
+ * This library computes that pass for a decoder-only verifier:
+ *
+ *   vsr_prefill  runs the verifier once over the shared conditioning prefix
+ *                [visual-frame rows ; text ids (retrieved passages + question)]
+ *                and keeps every layer's rotated keys/values (the prefix cache);
+ *   vsr_score    teacher-forces M candidates against that cache and returns
+ *                lp[m][j] = log P(c_mj | prefix, c_m<j)   (j < n_m, else 0),
+ *                score[m] = sum_j lp[m][j]                 (Eq. 6),
+ *                argmax   = lowest m with the largest score (Eq. 7).
+ *
+ * Each candidate sees the prefix plus its own earlier tokens only (the drafts
+ * are scored independently, Eq. 6); candidate token j sits at position P + j.
+ *
+ * Conventions shared by every call:
+ *   - Device pointers are HIP device addresses on the device that was current
+ *     at vsr_create. Host pointers are plain host memory. Each argument below
+ *     says which it is.
+ *   - Floating-point tensors are in the context's dtype (VSR_F32: float,
+ *     VSR_BF16: bfloat16); ids are int32; outputs are float / int32.
+ *   - Matrices use the torch nn.Linear layout [out][in], rows contiguous.
+ *   - Calls are asynchronous and ordered on the stream given to vsr_create:
+ *     device outputs are valid once that stream has been synchronised.
+ *   - Every call returns VSR_OK (0) or a negative code; vsr_last_error gives
+ *     the message of the last failure. No call throws or aborts.
+ *   - The library allocates no device memory: everything it keeps (prefix
+ *     cache, activations, partial results) lives in the caller's workspace.
+ *   - A context is not thread-safe; use one context per stream.
+ */
+#ifndef VSR_H
+#define VSR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define VSR_OK 0
+#define VSR_EINVAL (-1)  /* null pointer, bad shape, unsupported config   */
+#define VSR_ESTATE (-2)  /* call out of order (e.g. score before prefill) */
+#define VSR_ERANGE (-3)  /* a size exceeds the maxima given at create     */
+#define VSR_ENOMEM (-4)  /* workspace smaller than vsr_workspace_size     */
+#define VSR_EHIP (-5)    /* a HIP runtime call failed (message has text)  */
+
+/* Arithmetic types of weights, visual rows and activations. */
+#define VSR_F32 0
+#define VSR_BF16 1
+
+/* Verifier architecture and the maxima the workspace is sized for.
+ * Decoder: pre-RMSNorm blocks with rotary grouped-query attention (query head
+ * h reads KV head h / (n_heads / n_kv_heads); rotate-half pairs (i, i+hd/2),
+ * inverse frequency rope_base^(-2i/hd)) and a SwiGLU FFN, final RMSNorm and an
+ * untied LM head; no biases.
+ * Supported: n_heads % n_kv_heads == 0; VSR_BF16 needs head_dim == 128 and
+ * d_model, d_ff multiples of 64; VSR_F32 needs head_dim even and <= 256. */
+typedef struct vsr_config {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff, vocab;
+  float rms_eps, rope_base;
+  int32_t dtype;        /* VSR_F32 or VSR_BF16 */
+  int32_t max_prefix;   /* largest P = n_visual + n_text passed to prefill */
+  int32_t max_cands;    /* largest M passed to score (<= VSR_MAX_CANDS)    */
+  int32_t max_cand_len; /* largest Cmax passed to score                    */
+} vsr_config;
+
+#define VSR_MAX_CANDS 256
+
+/* Borrowed device pointers to the verifier weights (no copy is made; they
+ * must outlive the context). The per-layer members are HOST arrays of
+ * n_layers device pointers; they are copied at vsr_load_weights.
+ *   embed, lm_head [vocab][d_model]; final_norm [d_model];
+ *   attn_norm, ffn_norm [d_model];
+ *   wqkv  [(n_heads + 2 n_kv_heads) head_dim][d_model]: q rows, then k rows,
+ *         then v rows, each head-major;
+ *   wo    [d_model][n_heads head_dim];
+ *   wgu   [2 d_ff][d_model]: gate rows, then up rows;
+ *   wdown [d_model][d_ff]. */
+typedef struct vsr_weights {
+  const void *embed, *lm_head, *final_norm;
+  const void *const *attn_norm;
+  const void *const *wqkv;
+  const void *const *wo;
+  const void *const *ffn_norm;
+  const void *const *wgu;
+  const void *const *wdown;
+} vsr_weights;
+
+typedef struct vsr_ctx vsr_ctx;
+
+/* Bytes of device workspace a context with this config needs (0 if the
+ * config is invalid). Pure host computation. */
+size_t vsr_workspace_size(const vsr_config *cfg);
+
+/* Creates a context. `workspace` is a device buffer of at least
+ * vsr_workspace_size(cfg) bytes, 256-byte aligned, owned by the caller and
+ * kept alive until vsr_destroy. `hip_stream` is a hipStream_t (NULL = the
+ * default stream). On success *out receives the context. Enqueues the rotary
+ * table construction on the stream. */
+int vsr_create(const vsr_config *cfg, void *workspace, size_t ws_bytes,
+               void *hip_stream, vsr_ctx **out);
+
+/* Binds the weights (borrowed device pointers, layout above). */
+int vsr_load_weights(vsr_ctx *ctx, const vsr_weights *w);
+
+/* Prefill over the conditioning prefix (Eq. 6 conditions on (Q, V)).
+ *   visual : device [n_visual][d_model] rows fed directly as layer-0 inputs
+ *            (may be NULL when n_visual == 0);
+ *   ids    : device [n_text] int32 text ids in [0, vocab) (may be NULL when
+ *            n_text == 0); out-of-range ids are read as id 0.
+ * P = n_visual + n_text must satisfy 1 <= P <= max_prefix. Replaces any
+ * earlier prefix. */
+int vsr_prefill(vsr_ctx *ctx, const void *visual, int32_t n_visual,
+                const int32_t *ids, int32_t n_text);
+
+/* Teacher-forced scoring of M candidates against the current prefix
+ * (Eq. 6-7). May be called any number of times after one prefill.
+ *   cand_ids : device [M][Cmax] int32, row m holds candidate m's tokens in
+ *              positions 0..cand_len[m]-1 (the rest is ignored);
+ *              out-of-range ids are read as id 0;
+ *   cand_len : HOST [M] int32, each in [0, Cmax];
+ *   logprobs : device [M][Cmax] float out; 0 past each candidate's length;
+ *   scores   : device [M] float out, sum of each candidate's log-probs;
+ *   argmax   : device [1] int32 out, lowest index among the largest scores.
+ * 1 <= M <= max_cands, 1 <= Cmax <= max_cand_len. */
+int vsr_score(vsr_ctx *ctx, const int32_t *cand_ids, const int32_t *cand_len,
+              int32_t M, int32_t Cmax, float *logprobs, float *scores,
+              int32_t *argmax);
+
+/* Message of the last failed call on this context ("" if none). With
+ * ctx == NULL: message of the last failed vsr_create on this thread. */
+const char *vsr_last_error(const vsr_ctx *ctx);
+
+/* Releases the context (not the workspace or the weights). NULL is a no-op. */
+void vsr_destroy(vsr_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VSR_H */

@@ -1,0 +1,178 @@
+"""ctypes binding of libvsr.so (C ABI: include/vsr.h).
+
+Argument marshalling only: every step of the scoring pass runs inside the HIP
+library. Torch tensors supply device memory and the stream. If the library is
+not built, loading fails loudly; there is no other path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libvsr.so")
+
+VSR_OK, VSR_EINVAL, VSR_ESTATE, VSR_ERANGE, VSR_ENOMEM, VSR_EHIP = 0, -1, -2, -3, -4, -5
+VSR_F32, VSR_BF16 = 0, 1
+VSR_MAX_CANDS = 256
+
+EXPORTS = ["vsr_workspace_size", "vsr_create", "vsr_load_weights", "vsr_prefill",
+           "vsr_score", "vsr_last_error", "vsr_destroy"]
+
+
+class VsrConfig(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("d_ff", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("rope_base", ctypes.c_float), ("dtype", ctypes.c_int32),
+                ("max_prefix", ctypes.c_int32), ("max_cands", ctypes.c_int32),
+                ("max_cand_len", ctypes.c_int32)]
+
+
+_PP = ctypes.POINTER(ctypes.c_void_p)
+
+
+class VsrWeights(ctypes.Structure):
+    _fields_ = [("embed", ctypes.c_void_p), ("lm_head", ctypes.c_void_p),
+                ("final_norm", ctypes.c_void_p), ("attn_norm", _PP), ("wqkv", _PP),
+                ("wo", _PP), ("ffn_norm", _PP), ("wgu", _PP), ("wdown", _PP)]
+
+
+class VsrError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"vsr error {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Loads libvsr.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{path} is missing: build it with `python -m paper_2601_01513_amd.build`")
+    lib = ctypes.CDLL(path)
+    lib.vsr_workspace_size.argtypes = [ctypes.POINTER(VsrConfig)]
+    lib.vsr_workspace_size.restype = ctypes.c_size_t
+    lib.vsr_create.argtypes = [ctypes.POINTER(VsrConfig), ctypes.c_void_p, ctypes.c_size_t,
+                               ctypes.c_void_p, ctypes.POINTER(ctypes.c_void_p)]
+    lib.vsr_create.restype = ctypes.c_int
+    lib.vsr_load_weights.argtypes = [ctypes.c_void_p, ctypes.POINTER(VsrWeights)]
+    lib.vsr_load_weights.restype = ctypes.c_int
+    lib.vsr_prefill.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                ctypes.c_void_p, ctypes.c_int32]
+    lib.vsr_prefill.restype = ctypes.c_int
+    lib.vsr_score.argtypes = [ctypes.c_void_p, ctypes.c_void_p,
+                              ctypes.POINTER(ctypes.c_int32), ctypes.c_int32, ctypes.c_int32,
+                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.vsr_score.restype = ctypes.c_int
+    lib.vsr_last_error.argtypes = [ctypes.c_void_p]
+    lib.vsr_last_error.restype = ctypes.c_char_p
+    lib.vsr_destroy.argtypes = [ctypes.c_void_p]
+    lib.vsr_destroy.restype = None
+    _lib = lib
+    return lib
+
+
+def make_config(cfg, max_prefix: Optional[int] = None, max_cands: Optional[int] = None,
+                max_cand_len: Optional[int] = None) -> VsrConfig:
+    """vsr_config from a workload.VerifierConfig (maxima default to its sizes)."""
+    return VsrConfig(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim,
+                     cfg.d_ff, cfg.vocab, cfg.rms_eps, cfg.rope_base, cfg.dtype,
+                     max_prefix or cfg.n_prefix, max_cands or cfg.n_cands,
+                     max_cand_len or cfg.cand_len)
+
+
+def workspace_size(c: VsrConfig) -> int:
+    return load_library().vsr_workspace_size(ctypes.byref(c))
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else t.data_ptr()
+
+
+class Verifier:
+    """One vsr context: workspace, borrowed weights and the current prefix."""
+
+    def __init__(self, cfg, weights: Dict, device="cuda", stream=None,
+                 max_prefix=None, max_cands=None, max_cand_len=None):
+        import torch
+        self._torch = torch
+        self.lib = load_library()
+        self.cfg = cfg
+        self.c = make_config(cfg, max_prefix, max_cands, max_cand_len)
+        size = self.lib.vsr_workspace_size(ctypes.byref(self.c))
+        if size == 0:
+            raise VsrError(VSR_EINVAL, "unsupported config")
+        self.device = torch.device(device)
+        self.workspace = torch.empty(size, dtype=torch.uint8, device=self.device)
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        h = ctypes.c_void_p()
+        rc = self.lib.vsr_create(ctypes.byref(self.c), self.workspace.data_ptr(), size,
+                                 self.stream.cuda_stream, ctypes.byref(h))
+        if rc != VSR_OK:
+            raise VsrError(rc, self.lib.vsr_last_error(None).decode())
+        self.h = h
+        self.load_weights(weights)
+
+    def _check(self, rc: int):
+        if rc != VSR_OK:
+            raise VsrError(rc, self.lib.vsr_last_error(self.h).decode())
+
+    def load_weights(self, w: Dict):
+        self.weights = w  # keep the borrowed tensors alive
+        L = len(w["layers"])
+        arrs = {}
+        for k in ("attn_norm", "wqkv", "wo", "ffn_norm", "wgu", "wdown"):
+            arrs[k] = (ctypes.c_void_p * max(L, 1))(*[_ptr(lw[k]) for lw in w["layers"]])
+        self._arrs = arrs
+        cw = VsrWeights(_ptr(w["embed"]), _ptr(w["lm_head"]), _ptr(w["final_norm"]),
+                        *[ctypes.cast(arrs[k], _PP) for k in
+                          ("attn_norm", "wqkv", "wo", "ffn_norm", "wgu", "wdown")])
+        self._check(self.lib.vsr_load_weights(self.h, ctypes.byref(cw)))
+
+    def prefill(self, visual, ids):
+        """visual: device [Pv][d] (config dtype) or None; ids: device int32 [Pt] or None."""
+        nv = 0 if visual is None else int(visual.shape[0])
+        nt = 0 if ids is None else int(ids.shape[0])
+        self._keep = (visual, ids)
+        self._check(self.lib.vsr_prefill(self.h, _ptr(visual), nv, _ptr(ids), nt))
+
+    def score(self, cand_ids, cand_len: Sequence[int], out=None):
+        """cand_ids: device int32 [M][Cmax]; cand_len: host ints [M].
+
+        Returns device tensors (logprobs [M][Cmax] f32, scores [M] f32,
+        argmax [1] int32), valid once the stream is synchronised.
+        """
+        torch = self._torch
+        M, cmax = int(cand_ids.shape[0]), int(cand_ids.shape[1])
+        lens = (ctypes.c_int32 * M)(*[int(x) for x in cand_len])
+        if out is None:
+            out = (torch.empty((M, cmax), dtype=torch.float32, device=self.device),
+                   torch.empty(M, dtype=torch.float32, device=self.device),
+                   torch.empty(1, dtype=torch.int32, device=self.device))
+        lp, sc, am = out
+        self._check(self.lib.vsr_score(self.h, _ptr(cand_ids), lens, M, cmax, _ptr(lp),
+                                       _ptr(sc), _ptr(am)))
+        return lp, sc, am
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.lib.vsr_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def verifier_from_workload(wl, device="cuda", **kw) -> Verifier:
+    return Verifier(wl.cfg, wl.weights, device=device, **kw)

@@ -1,0 +1,160 @@
+// Internal declarations shared by the HIP kernels and the host orchestrator of
+// the verifier scoring pass. Not part of the C ABI (include/vsr.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace vsr {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16 x) { return static_cast<float>(x); }
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return static_cast<bf16>(x); }
+
+// Largest number of candidates one score call may carry.
+constexpr int kMaxCands = 256;
+
+// Packed candidate rows: candidate m owns rows [cu[m], cu[m+1]).
+struct Branches {
+  int M;
+  int cmax;
+  int cu[kMaxCands + 1];
+};
+
+// ---------------------------------------------------------------- launchers
+// Every launcher enqueues on `s` and returns the hipError_t of the launch.
+
+// Rotary table: cs[p][i] = (cos, sin)(p * base^(-2i/hd)), i < hd/2, p < npos.
+hipError_t launch_rope_table(float2 *cs, int npos, int hd, float base, hipStream_t s);
+
+// Row tables of one score call: for packed row t of candidate m at offset j,
+// row_lo[t] = cu[m] (first row of its candidate), row_pos[t] = P + j,
+// lm_tgt[t] = cand_ids[m][j] (clamped into [0, vocab)).
+hipError_t launch_row_tables(const Branches &br, int P, const int32_t *cand_ids, int vocab,
+                             int32_t *row_lo, int32_t *row_pos, int32_t *lm_tgt,
+                             hipStream_t s);
+
+// x[p] = visual[p] for p < n_visual, else embed[ids[p - n_visual]] (fp32 out).
+template <typename T>
+hipError_t launch_embed_prefix(const T *visual, int n_visual, const int32_t *ids, int n_text,
+                               const T *embed, int vocab, int d, float *x, hipStream_t s);
+// x[t] = embed[ids[t]] for t < rows (ids already in [0, vocab)).
+template <typename T>
+hipError_t launch_embed_rows(const int32_t *ids, int rows, const T *embed, int d, float *x,
+                             hipStream_t s);
+
+// y[r] = T(x[r] / sqrt(mean(x[r]^2) + eps) * g) for rows r < rows.
+template <typename T>
+hipError_t launch_rmsnorm(const float *x, const T *g, int rows, int d, float eps, T *y,
+                          hipStream_t s);
+// LM-head inputs of a score call: y[t] = norm(h_last) if t is the first row
+// of its candidate, else norm(x[t - 1]).
+template <typename T>
+hipError_t launch_lm_inputs(const float *x, const float *h_last, const int32_t *row_lo,
+                            const T *g, int T_rows, int d, float eps, T *y, hipStream_t s);
+
+// Per-row merge of the LM-head partials: lse over the vocabulary chunks,
+// lp = target logit - lse, scattered to logprobs[m][j] (zeros elsewhere).
+hipError_t launch_lse_gather(const Branches &br, const float2 *part, int nchunks,
+                             const float *tgt_logit, float *logprobs, hipStream_t s);
+// scores[m] = sum_j logprobs[m][j] (fixed order), argmax = lowest best m.
+hipError_t launch_reduce_select(const Branches &br, const float *logprobs, float *scores,
+                                int32_t *argmax, hipStream_t s);
+
+// ----- layouts of the caches -----------------------------------------------
+// K cache  : [n_kv][npos][hd]  (rotated keys, position-major)
+// Vt cache : [n_kv][hd][npos]  (values, transposed: position-contiguous)
+
+// Destinations of the QKV projection epilogue.
+template <typename T>
+struct QKVOut {
+  T *q;            // [rows][n_heads][hd] rotated queries
+  T *k;            // K cache base (this layer)
+  T *vt;           // Vt cache base (this layer)
+  int kv_npos;     // position stride of the caches (their capacity)
+  const int32_t *row_pos;  // rotary position of each row (NULL: position = row)
+  const float2 *rope;      // rotary table [npos][hd/2]
+};
+
+// ------------------------------------------------------------ bf16 MFMA path
+// C = A[rows][K] . B[N][K]^T with fused epilogues.
+hipError_t gemm_qkv_rope(const bf16 *A, const bf16 *W, int rows, int K, int n_heads,
+                         int n_kv, const QKVOut<bf16> &out, hipStream_t s);
+// x[rows][N] += A . W^T (residual stream, fp32).
+hipError_t gemm_residual(const bf16 *A, const bf16 *W, int rows, int N, int K, float *x,
+                         hipStream_t s);
+// h[rows][F] = silu(A . Wg^T) * (A . Wu^T), W = [Wg; Wu] ([2F][K]).
+hipError_t gemm_swiglu(const bf16 *A, const bf16 *W, int rows, int F, int K, bf16 *h,
+                       hipStream_t s);
+// LM head: per (vocab chunk c, row t): part[c][t] = (max, sum exp(l - max)) over
+// the chunk's logits l = W[v] . A[t]; tgt_logit[t] = logit of lm_tgt[t].
+int lmhead_chunks(int vocab);
+hipError_t gemm_lmhead(const bf16 *A, const bf16 *W, int rows, int vocab, int K,
+                       const int32_t *lm_tgt, float2 *part, float *tgt_logit, hipStream_t s);
+
+// Attention of query rows against one key source. Query row r of KV head h is
+// (token r / G, head h*G + r % G). Keys of a token t are the positions
+// [lo(t), hi(t)] of the key source:
+//   mode 0 (prefill)  : lo = 0, hi = t (causal);
+//   mode 1 (cascade)  : prefix keys [0, P) all visible, then the branch keys
+//                       [row_lo[t], t] of the token's own candidate.
+struct AttnArgs {
+  const bf16 *q;        // [T][n_heads][hd]
+  const bf16 *k;        // prefix / own K cache of this layer
+  const bf16 *vt;       // prefix / own Vt cache
+  int kv_npos;          // position stride of k / vt
+  const bf16 *bk;       // mode 1: branch K  [n_kv][bk_npos][hd]
+  const bf16 *bvt;      // mode 1: branch Vt [n_kv][hd][bk_npos]
+  int bk_npos;
+  const int32_t *row_lo;  // mode 1
+  int T;                // query tokens
+  int P;                // mode 1: prefix length
+  int n_heads, n_kv;
+  int nchunks;          // mode 1: prefix split (partials when > 1)
+  int chunk;            // prefix keys per split
+  bf16 *out;            // [T][n_heads][hd] when nchunks == 1
+  float *part_acc;      // [nchunks][n_kv][T*G][hd]
+  float2 *part_ml;      // [nchunks][n_kv][T*G]
+};
+hipError_t attn_prefill(const AttnArgs &a, hipStream_t s);
+hipError_t attn_cascade(const AttnArgs &a, hipStream_t s);
+hipError_t attn_merge(const AttnArgs &a, hipStream_t s);
+
+// ------------------------------------------------------ simple (fp32) path
+// Plain kernels, one output element per thread; the path of VSR_F32 contexts.
+template <typename T>
+hipError_t simple_qkv_rope(const T *A, const T *W, int rows, int K, int n_heads, int n_kv,
+                           int hd, const QKVOut<T> &out, hipStream_t s);
+template <typename T>
+hipError_t simple_residual(const T *A, const T *W, int rows, int N, int K, float *x,
+                           hipStream_t s);
+template <typename T>
+hipError_t simple_swiglu(const T *A, const T *W, int rows, int F, int K, T *h, hipStream_t s);
+template <typename T>
+hipError_t simple_lmhead(const T *A, const T *W, int rows, int vocab, int K,
+                         const int32_t *lm_tgt, float2 *part, float *tgt_logit,
+                         hipStream_t s);
+// Attention with the same key rules as AttnArgs (mode 0: causal over the
+// prefix cache; mode 1: prefix + own candidate), one block per (token, head).
+struct SimpleAttnArgs {
+  const void *q, *k, *vt, *bk, *bvt;
+  int kv_npos, bk_npos;
+  const int32_t *row_lo;
+  int T, P, n_heads, n_kv, hd;
+  int mode;
+  void *out;
+};
+template <typename T>
+hipError_t simple_attn(const SimpleAttnArgs &a, hipStream_t s);
+
+}  // namespace vsr

@@ -1,0 +1,242 @@
+// Memory-bound helper kernels of the verifier scoring pass: rotary table,
+// per-row tables, embedding gathers, RMSNorm, LM-head inputs, the log-sum-exp
+// merge with the target gather, and the per-candidate sum and argmax
+// (Eq. 6-7). All of them read and write rows with consecutive lanes on
+// consecutive elements; reductions run in a fixed order (no atomics).
+#include "common.h"
+
+namespace vsr {
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Sum over a 256-thread block, same value returned to every thread.
+__device__ __forceinline__ float block_sum256(float v, float *red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  __syncthreads();
+  if (l == 0) red[w] = v;
+  __syncthreads();
+  return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// ------------------------------------------------------------- rotary table
+__global__ void k_rope_table(float2 *cs, int npos, int hd, double base) {
+  const int half = hd / 2;
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)npos * half) return;
+  const int p = (int)(idx / half), i = (int)(idx % half);
+  const double inv = pow(base, -2.0 * i / hd);
+  const double ang = (double)p * inv;
+  cs[idx] = make_float2((float)cos(ang), (float)sin(ang));
+}
+
+hipError_t launch_rope_table(float2 *cs, int npos, int hd, float base, hipStream_t s) {
+  const long n = (long)npos * (hd / 2);
+  k_rope_table<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(cs, npos, hd, (double)base);
+  return hipGetLastError();
+}
+
+// --------------------------------------------------------------- row tables
+__global__ void k_row_tables(Branches br, int P, const int32_t *cand_ids, int vocab,
+                             int32_t *row_lo, int32_t *row_pos, int32_t *lm_tgt) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= br.cu[br.M]) return;
+  int m = 0;
+  while (br.cu[m + 1] <= t) ++m;
+  const int j = t - br.cu[m];
+  int id = cand_ids[(long)m * br.cmax + j];
+  if (id < 0 || id >= vocab) id = 0;
+  row_lo[t] = br.cu[m];
+  row_pos[t] = P + j;
+  lm_tgt[t] = id;
+}
+
+hipError_t launch_row_tables(const Branches &br, int P, const int32_t *cand_ids, int vocab,
+                             int32_t *row_lo, int32_t *row_pos, int32_t *lm_tgt,
+                             hipStream_t s) {
+  const int T = br.cu[br.M];
+  if (T == 0) return hipSuccess;
+  k_row_tables<<<(T + 255) / 256, 256, 0, s>>>(br, P, cand_ids, vocab, row_lo, row_pos, lm_tgt);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- embedding
+template <typename T>
+__global__ void k_embed_prefix(const T *visual, int n_visual, const int32_t *ids,
+                               const T *embed, int vocab, int d, float *x) {
+  const int p = blockIdx.x;
+  const T *src;
+  if (p < n_visual) {
+    src = visual + (long)p * d;
+  } else {
+    int id = ids[p - n_visual];
+    if (id < 0 || id >= vocab) id = 0;
+    src = embed + (long)id * d;
+  }
+  float *dst = x + (long)p * d;
+  for (int c = threadIdx.x; c < d; c += blockDim.x) dst[c] = to_f32(src[c]);
+}
+
+template <typename T>
+hipError_t launch_embed_prefix(const T *visual, int n_visual, const int32_t *ids, int n_text,
+                               const T *embed, int vocab, int d, float *x, hipStream_t s) {
+  const int P = n_visual + n_text;
+  k_embed_prefix<T><<<P, 256, 0, s>>>(visual, n_visual, ids, embed, vocab, d, x);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ void k_embed_rows(const int32_t *ids, const T *embed, int d, float *x) {
+  const int t = blockIdx.x;
+  const T *src = embed + (long)ids[t] * d;
+  float *dst = x + (long)t * d;
+  for (int c = threadIdx.x; c < d; c += blockDim.x) dst[c] = to_f32(src[c]);
+}
+
+// Candidate rows use the row table's clamped ids (lm_tgt holds cand_ids[m][j]).
+template <typename T>
+hipError_t launch_embed_rows(const int32_t *ids, int rows, const T *embed, int d, float *x,
+                             hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  k_embed_rows<T><<<rows, 256, 0, s>>>(ids, embed, d, x);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ RMSNorm
+template <typename T>
+__device__ __forceinline__ void norm_row(const float *src, const T *g, int d, float eps,
+                                         T *dst, float *red) {
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < d; c += 256) {
+    const float v = src[c];
+    ss += v * v;
+  }
+  ss = block_sum256(ss, red);
+  const float r = rsqrtf(ss / (float)d + eps);
+  for (int c = threadIdx.x; c < d; c += 256) dst[c] = from_f32<T>(src[c] * r * to_f32(g[c]));
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_rmsnorm(const float *x, const T *g, int d, float eps,
+                                                 T *y) {
+  __shared__ float red[4];
+  const long r = blockIdx.x;
+  norm_row<T>(x + r * d, g, d, eps, y + r * d, red);
+}
+
+template <typename T>
+hipError_t launch_rmsnorm(const float *x, const T *g, int rows, int d, float eps, T *y,
+                          hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  k_rmsnorm<T><<<rows, 256, 0, s>>>(x, g, d, eps, y);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_lm_inputs(const float *x, const float *h_last,
+                                                   const int32_t *row_lo, const T *g, int d,
+                                                   float eps, T *y) {
+  __shared__ float red[4];
+  const int t = blockIdx.x;
+  const float *src = (row_lo[t] == t) ? h_last : x + (long)(t - 1) * d;
+  norm_row<T>(src, g, d, eps, y + (long)t * d, red);
+}
+
+template <typename T>
+hipError_t launch_lm_inputs(const float *x, const float *h_last, const int32_t *row_lo,
+                            const T *g, int T_rows, int d, float eps, T *y, hipStream_t s) {
+  if (T_rows == 0) return hipSuccess;
+  k_lm_inputs<T><<<T_rows, 256, 0, s>>>(x, h_last, row_lo, g, d, eps, y);
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------- LSE merge and gather
+// One wave per output slot (m, j); lanes stride over the vocabulary chunks.
+__global__ __launch_bounds__(256) void k_lse_gather(Branches br, const float2 *part,
+                                                    int nchunks, const float *tgt_logit,
+                                                    float *logprobs) {
+  const int slot = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (slot >= br.M * br.cmax) return;
+  const int m = slot / br.cmax, j = slot % br.cmax;
+  const int n = br.cu[m + 1] - br.cu[m];
+  if (j >= n) {
+    if (lane == 0) logprobs[slot] = 0.f;
+    return;
+  }
+  const int t = br.cu[m] + j;
+  const int T = br.cu[br.M];
+  float mx = -INFINITY;
+  for (int c = lane; c < nchunks; c += 64) mx = fmaxf(mx, part[(long)c * T + t].x);
+  mx = wave_max(mx);
+  float sum = 0.f;
+  for (int c = lane; c < nchunks; c += 64) {
+    const float2 p = part[(long)c * T + t];
+    sum += p.y * __expf(p.x - mx);
+  }
+  sum = wave_sum(sum);
+  if (lane == 0) logprobs[slot] = tgt_logit[t] - (mx + __logf(sum));
+}
+
+hipError_t launch_lse_gather(const Branches &br, const float2 *part, int nchunks,
+                             const float *tgt_logit, float *logprobs, hipStream_t s) {
+  const int slots = br.M * br.cmax;
+  k_lse_gather<<<(slots + 3) / 4, 256, 0, s>>>(br, part, nchunks, tgt_logit, logprobs);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------- per-candidate sum, argmax
+// One block; wave w sums candidates w, w+4, ... with a fixed lane order, then
+// thread 0 takes the first index of the largest score (Eq. 7).
+__global__ __launch_bounds__(256) void k_reduce_select(Branches br, const float *logprobs,
+                                                       float *scores, int32_t *argmax) {
+  __shared__ float sc[kMaxCands];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int m = w; m < br.M; m += 4) {
+    const int n = br.cu[m + 1] - br.cu[m];
+    float v = 0.f;
+    for (int j = lane; j < n; j += 64) v += logprobs[(long)m * br.cmax + j];
+    v = wave_sum(v);
+    if (lane == 0) {
+      sc[m] = v;
+      scores[m] = v;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int best = 0;
+    for (int m = 1; m < br.M; ++m)
+      if (sc[m] > sc[best]) best = m;
+    *argmax = best;
+  }
+}
+
+hipError_t launch_reduce_select(const Branches &br, const float *logprobs, float *scores,
+                                int32_t *argmax, hipStream_t s) {
+  k_reduce_select<<<1, 256, 0, s>>>(br, logprobs, scores, argmax);
+  return hipGetLastError();
+}
+
+#define VSR_INST(T)                                                                          \
+  template hipError_t launch_embed_prefix<T>(const T *, int, const int32_t *, int, const T *, \
+                                             int, int, float *, hipStream_t);               \
+  template hipError_t launch_embed_rows<T>(const int32_t *, int, const T *, int, float *,     \
+                                           hipStream_t);                                    \
+  template hipError_t launch_rmsnorm<T>(const float *, const T *, int, int, float, T *,      \
+                                        hipStream_t);                                       \
+  template hipError_t launch_lm_inputs<T>(const float *, const float *, const int32_t *,     \
+                                          const T *, int, int, float, T *, hipStream_t);
+VSR_INST(float)
+VSR_INST(bf16)
+#undef VSR_INST
+
+}  // namespace vsr

@@ -1,0 +1,464 @@
+// Host side of the C ABI (include/vsr.h): argument checks, workspace plan and
+// the launch sequence of the verifier scoring pass (Section 3.1, Eq. 6-7).
+//
+// Every argument check runs before any HIP call, so misuse is reported
+// without touching the device. The workspace plan is pure host arithmetic.
+#include "vsr.h"
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+using namespace vsr;
+
+namespace {
+
+thread_local std::string g_create_error;
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Prefix split of the candidate pass: enough blocks to cover the chip, chunks
+// of at least 256 keys, a multiple of the 64-key tile.
+struct Split {
+  int nchunks, chunk;
+};
+Split cascade_split(int T, int P, int n_heads, int n_kv) {
+  const int G = n_heads / n_kv;
+  const int qtiles = (T * G + 127) / 128 * n_kv;
+  int n = std::max(1, (512 + qtiles - 1) / qtiles);
+  n = std::min(n, std::max(1, P / 256));
+  n = std::min(n, 32);
+  int chunk = (int)align_up((size_t)((P + n - 1) / n), 64);
+  n = (P + chunk - 1) / chunk;
+  return {n, chunk};
+}
+
+struct Plan {
+  int kv_npos, bk_npos, max_t, rows_max, rope_npos, lm_chunks;
+  size_t x, xn, q, attn, h, kc, vtc, bk, bvt, part_acc, part_ml, lm_part, tgt, row_lo,
+      row_pos, lm_tgt, rope, h_last, total;
+};
+
+// Returns an empty message if cfg is supported.
+std::string check_config(const vsr_config *c) {
+  if (!c) return "config is NULL";
+  if (c->n_layers < 0 || c->d_model <= 0 || c->n_heads <= 0 || c->n_kv_heads <= 0 ||
+      c->head_dim <= 0 || c->d_ff <= 0 || c->vocab <= 0)
+    return "config sizes must be positive (n_layers >= 0)";
+  if (c->n_heads % c->n_kv_heads) return "n_heads must be a multiple of n_kv_heads";
+  if (!(c->rms_eps >= 0.f) || !(c->rope_base > 0.f)) return "rms_eps >= 0 and rope_base > 0 needed";
+  if (c->max_prefix < 1 || c->max_cands < 1 || c->max_cand_len < 1)
+    return "max_prefix, max_cands and max_cand_len must be >= 1";
+  if (c->max_cands > VSR_MAX_CANDS) return "max_cands exceeds VSR_MAX_CANDS";
+  if ((long long)c->max_cands * c->max_cand_len > (1 << 24)) return "max_cands * max_cand_len too large";
+  if (c->max_prefix > (1 << 24)) return "max_prefix too large";
+  if (c->dtype == VSR_BF16) {
+    if (c->head_dim != 128) return "bf16 contexts need head_dim == 128";
+    if (c->d_model % 64 || c->d_ff % 64) return "bf16 contexts need d_model and d_ff multiples of 64";
+  } else if (c->dtype == VSR_F32) {
+    if (c->head_dim % 2 || c->head_dim > 256) return "fp32 contexts need an even head_dim <= 256";
+  } else {
+    return "dtype must be VSR_F32 or VSR_BF16";
+  }
+  return "";
+}
+
+Plan make_plan(const vsr_config &c) {
+  Plan p{};
+  const size_t E = c.dtype == VSR_BF16 ? 2 : 4;
+  const int G = c.n_heads / c.n_kv_heads;
+  const size_t d = c.d_model, hd = c.head_dim;
+  p.kv_npos = (int)align_up(c.max_prefix, 64);
+  p.max_t = c.max_cands * c.max_cand_len;
+  p.bk_npos = (int)align_up(p.max_t, 64);
+  p.rows_max = std::max(c.max_prefix, p.max_t);
+  p.rope_npos = p.kv_npos + c.max_cand_len;
+  p.lm_chunks = c.dtype == VSR_BF16 ? lmhead_chunks(c.vocab) : 1;
+  // Largest partial-row count of the cascade split over every T <= max_t.
+  size_t part_rows = 0;
+  if (c.dtype == VSR_BF16) {
+    for (int T = 1; T <= p.max_t; ++T) {
+      const Split s = cascade_split(T, c.max_prefix, c.n_heads, c.n_kv_heads);
+      if (s.nchunks > 1) part_rows = std::max(part_rows, (size_t)s.nchunks * T * G);
+    }
+  }
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes, 256);
+    return o;
+  };
+  const size_t R = p.rows_max;
+  p.x = take(R * d * 4);
+  p.xn = take(R * d * E);
+  p.q = take(R * c.n_heads * hd * E);
+  p.attn = take(R * c.n_heads * hd * E);
+  p.h = take(R * (size_t)c.d_ff * E);
+  p.kc = take((size_t)c.n_layers * c.n_kv_heads * p.kv_npos * hd * E);
+  p.vtc = take((size_t)c.n_layers * c.n_kv_heads * p.kv_npos * hd * E);
+  p.bk = take((size_t)c.n_kv_heads * p.bk_npos * hd * E);
+  p.bvt = take((size_t)c.n_kv_heads * p.bk_npos * hd * E);
+  p.part_acc = take(part_rows * c.n_kv_heads * hd * 4);
+  p.part_ml = take(part_rows * c.n_kv_heads * 8);
+  p.lm_part = take((size_t)p.lm_chunks * p.max_t * 8);
+  p.tgt = take((size_t)p.max_t * 4);
+  p.row_lo = take((size_t)p.max_t * 4);
+  p.row_pos = take((size_t)p.max_t * 4);
+  p.lm_tgt = take((size_t)p.max_t * 4);
+  p.rope = take((size_t)p.rope_npos * (hd / 2) * 8);
+  p.h_last = take(d * 4);
+  p.total = off;
+  return p;
+}
+
+}  // namespace
+
+struct vsr_ctx {
+  vsr_config cfg;
+  Plan plan;
+  char *ws;
+  hipStream_t stream;
+  int device;
+  bool have_weights = false;
+  bool prefilled = false;
+  int P = 0;
+  const void *embed = nullptr, *lm_head = nullptr, *final_norm = nullptr;
+  std::vector<const void *> attn_norm, wqkv, wo, ffn_norm, wgu, wdown;
+  std::string err;
+
+  template <typename T>
+  T *at(size_t off) const {
+    return reinterpret_cast<T *>(ws + off);
+  }
+  int fail(int code, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    err = buf;
+    return code;
+  }
+};
+
+#define HIPCHECK(ctx, stage, expr)                                                        \
+  do {                                                                                    \
+    hipError_t e_ = (expr);                                                               \
+    if (e_ != hipSuccess)                                                                 \
+      return (ctx)->fail(VSR_EHIP, "HIP error in %s: %s", stage, hipGetErrorString(e_)); \
+  } while (0)
+
+extern "C" size_t vsr_workspace_size(const vsr_config *cfg) {
+  if (!check_config(cfg).empty()) return 0;
+  return make_plan(*cfg).total;
+}
+
+extern "C" int vsr_create(const vsr_config *cfg, void *workspace, size_t ws_bytes,
+                          void *hip_stream, vsr_ctx **out) {
+  g_create_error.clear();
+  if (!out) {
+    g_create_error = "out is NULL";
+    return VSR_EINVAL;
+  }
+  *out = nullptr;
+  const std::string msg = check_config(cfg);
+  if (!msg.empty()) {
+    g_create_error = msg;
+    return VSR_EINVAL;
+  }
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255)) {
+    g_create_error = "workspace must be a non-NULL, 256-byte aligned device pointer";
+    return VSR_EINVAL;
+  }
+  const Plan plan = make_plan(*cfg);
+  if (ws_bytes < plan.total) {
+    g_create_error = "workspace smaller than vsr_workspace_size";
+    return VSR_ENOMEM;
+  }
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    g_create_error = std::string("HIP error in hipGetDevice: ") + hipGetErrorString(e);
+    return VSR_EHIP;
+  }
+  vsr_ctx *c = new vsr_ctx();
+  c->cfg = *cfg;
+  c->plan = plan;
+  c->ws = static_cast<char *>(workspace);
+  c->stream = static_cast<hipStream_t>(hip_stream);
+  c->device = dev;
+  e = launch_rope_table(c->at<float2>(plan.rope), plan.rope_npos, cfg->head_dim, cfg->rope_base,
+                        c->stream);
+  if (e != hipSuccess) {
+    g_create_error = std::string("HIP error in rope table: ") + hipGetErrorString(e);
+    delete c;
+    return VSR_EHIP;
+  }
+  *out = c;
+  return VSR_OK;
+}
+
+extern "C" int vsr_load_weights(vsr_ctx *ctx, const vsr_weights *w) {
+  if (!ctx) return VSR_EINVAL;
+  if (!w || !w->embed || !w->lm_head || !w->final_norm)
+    return ctx->fail(VSR_EINVAL, "weights: embed, lm_head and final_norm must be non-NULL");
+  const int L = ctx->cfg.n_layers;
+  if (L > 0 && (!w->attn_norm || !w->wqkv || !w->wo || !w->ffn_norm || !w->wgu || !w->wdown))
+    return ctx->fail(VSR_EINVAL, "weights: per-layer pointer arrays must be non-NULL");
+  for (int l = 0; l < L; ++l)
+    if (!w->attn_norm[l] || !w->wqkv[l] || !w->wo[l] || !w->ffn_norm[l] || !w->wgu[l] ||
+        !w->wdown[l])
+      return ctx->fail(VSR_EINVAL, "weights: layer %d has a NULL tensor", l);
+  ctx->embed = w->embed;
+  ctx->lm_head = w->lm_head;
+  ctx->final_norm = w->final_norm;
+  ctx->attn_norm.assign(w->attn_norm, w->attn_norm + L);
+  ctx->wqkv.assign(w->wqkv, w->wqkv + L);
+  ctx->wo.assign(w->wo, w->wo + L);
+  ctx->ffn_norm.assign(w->ffn_norm, w->ffn_norm + L);
+  ctx->wgu.assign(w->wgu, w->wgu + L);
+  ctx->wdown.assign(w->wdown, w->wdown + L);
+  ctx->have_weights = true;
+  ctx->prefilled = false;
+  return VSR_OK;
+}
+
+namespace {
+
+// One decoder block over `rows` rows whose residual stream is x. `mode` 0 is
+// the prefix (causal, caches of layer l), 1 the candidates (cascade).
+template <typename T>
+int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
+  const vsr_config &cf = c->cfg;
+  const Plan &p = c->plan;
+  const int d = cf.d_model, Hq = cf.n_heads, Hkv = cf.n_kv_heads, hd = cf.head_dim, F = cf.d_ff;
+  const bool mfma = cf.dtype == VSR_BF16;
+  float *x = c->at<float>(p.x);
+  T *xn = c->at<T>(p.xn), *q = c->at<T>(p.q), *attn = c->at<T>(p.attn), *h = c->at<T>(p.h);
+  const size_t layer_cache = (size_t)Hkv * p.kv_npos * hd;
+  hipStream_t s = c->stream;
+  for (int l = 0; l < cf.n_layers; ++l) {
+    const T *wqkv = static_cast<const T *>(c->wqkv[l]);
+    const T *wo = static_cast<const T *>(c->wo[l]);
+    const T *wgu = static_cast<const T *>(c->wgu[l]);
+    const T *wdown = static_cast<const T *>(c->wdown[l]);
+    T *kc = c->at<T>(p.kc) + l * layer_cache;
+    T *vtc = c->at<T>(p.vtc) + l * layer_cache;
+    HIPCHECK(c, "attention norm",
+             launch_rmsnorm<T>(x, static_cast<const T *>(c->attn_norm[l]), rows, d, cf.rms_eps,
+                               xn, s));
+    QKVOut<T> qo;
+    qo.q = q;
+    qo.rope = c->at<float2>(p.rope);
+    if (mode == 0) {
+      qo.k = kc;
+      qo.vt = vtc;
+      qo.kv_npos = p.kv_npos;
+      qo.row_pos = nullptr;
+    } else {
+      qo.k = c->at<T>(p.bk);
+      qo.vt = c->at<T>(p.bvt);
+      qo.kv_npos = p.bk_npos;
+      qo.row_pos = c->at<int32_t>(p.row_pos);
+    }
+    if constexpr (sizeof(T) == 2) {
+      HIPCHECK(c, "qkv projection", gemm_qkv_rope(xn, wqkv, rows, d, Hq, Hkv, qo, s));
+    } else {
+      HIPCHECK(c, "qkv projection", simple_qkv_rope<T>(xn, wqkv, rows, d, Hq, Hkv, hd, qo, s));
+    }
+    if (mfma) {
+      AttnArgs a{};
+      a.q = reinterpret_cast<const bf16 *>(q);
+      a.k = reinterpret_cast<const bf16 *>(kc);
+      a.vt = reinterpret_cast<const bf16 *>(vtc);
+      a.kv_npos = p.kv_npos;
+      a.bk = c->at<bf16>(p.bk);
+      a.bvt = c->at<bf16>(p.bvt);
+      a.bk_npos = p.bk_npos;
+      a.row_lo = c->at<int32_t>(p.row_lo);
+      a.T = rows;
+      a.P = c->P;
+      a.n_heads = Hq;
+      a.n_kv = Hkv;
+      a.nchunks = split.nchunks;
+      a.chunk = split.chunk;
+      a.out = reinterpret_cast<bf16 *>(attn);
+      a.part_acc = c->at<float>(p.part_acc);
+      a.part_ml = c->at<float2>(p.part_ml);
+      if (mode == 0) {
+        HIPCHECK(c, "prefill attention", attn_prefill(a, s));
+      } else {
+        HIPCHECK(c, "cascade attention", attn_cascade(a, s));
+        HIPCHECK(c, "cascade merge", attn_merge(a, s));
+      }
+    } else {
+      SimpleAttnArgs a{};
+      a.q = q;
+      a.k = kc;
+      a.vt = vtc;
+      a.kv_npos = p.kv_npos;
+      a.bk = c->at<T>(p.bk);
+      a.bvt = c->at<T>(p.bvt);
+      a.bk_npos = p.bk_npos;
+      a.row_lo = c->at<int32_t>(p.row_lo);
+      a.T = rows;
+      a.P = c->P;
+      a.n_heads = Hq;
+      a.n_kv = Hkv;
+      a.hd = hd;
+      a.mode = mode;
+      a.out = attn;
+      HIPCHECK(c, "attention", simple_attn<T>(a, s));
+    }
+    if constexpr (sizeof(T) == 2) {
+      HIPCHECK(c, "output projection", gemm_residual(attn, wo, rows, d, Hq * hd, x, s));
+    } else {
+      HIPCHECK(c, "output projection", simple_residual<T>(attn, wo, rows, d, Hq * hd, x, s));
+    }
+    HIPCHECK(c, "ffn norm",
+             launch_rmsnorm<T>(x, static_cast<const T *>(c->ffn_norm[l]), rows, d, cf.rms_eps,
+                               xn, s));
+    if constexpr (sizeof(T) == 2) {
+      HIPCHECK(c, "gate/up projection", gemm_swiglu(xn, wgu, rows, F, d, h, s));
+      HIPCHECK(c, "down projection", gemm_residual(h, wdown, rows, d, F, x, s));
+    } else {
+      HIPCHECK(c, "gate/up projection", simple_swiglu<T>(xn, wgu, rows, F, d, h, s));
+      HIPCHECK(c, "down projection", simple_residual<T>(h, wdown, rows, d, F, x, s));
+    }
+  }
+  return VSR_OK;
+}
+
+template <typename T>
+int prefill_impl(vsr_ctx *c, const void *visual, int nv, const int32_t *ids, int nt) {
+  const vsr_config &cf = c->cfg;
+  const Plan &p = c->plan;
+  const int P = nv + nt;
+  float *x = c->at<float>(p.x);
+  HIPCHECK(c, "prefix embedding",
+           launch_embed_prefix<T>(static_cast<const T *>(visual), nv, ids, nt,
+                                  static_cast<const T *>(c->embed), cf.vocab, cf.d_model, x,
+                                  c->stream));
+  c->P = P;
+  const int rc = run_layers<T>(c, P, 0, Split{1, 0});
+  if (rc) return rc;
+  HIPCHECK(c, "last prefix row",
+           hipMemcpyAsync(c->at<float>(p.h_last), x + (size_t)(P - 1) * cf.d_model,
+                          (size_t)cf.d_model * 4, hipMemcpyDeviceToDevice, c->stream));
+  return VSR_OK;
+}
+
+template <typename T>
+int score_impl(vsr_ctx *c, const Branches &br, const int32_t *cand_ids, float *logprobs,
+               float *scores, int32_t *argmax) {
+  const vsr_config &cf = c->cfg;
+  const Plan &p = c->plan;
+  const int T_rows = br.cu[br.M];
+  hipStream_t s = c->stream;
+  int32_t *row_lo = c->at<int32_t>(p.row_lo), *row_pos = c->at<int32_t>(p.row_pos);
+  int32_t *lm_tgt = c->at<int32_t>(p.lm_tgt);
+  float2 *lm_part = c->at<float2>(p.lm_part);
+  float *tgt = c->at<float>(p.tgt);
+  int lm_chunks = 1;
+  if (T_rows > 0) {
+    HIPCHECK(c, "row tables",
+             launch_row_tables(br, c->P, cand_ids, cf.vocab, row_lo, row_pos, lm_tgt, s));
+    float *x = c->at<float>(p.x);
+    HIPCHECK(c, "candidate embedding",
+             launch_embed_rows<T>(lm_tgt, T_rows, static_cast<const T *>(c->embed), cf.d_model,
+                                  x, s));
+    const Split split = cf.dtype == VSR_BF16
+                            ? cascade_split(T_rows, c->P, cf.n_heads, cf.n_kv_heads)
+                            : Split{1, 0};
+    const int rc = run_layers<T>(c, T_rows, 1, split);
+    if (rc) return rc;
+    T *lm_in = c->at<T>(p.xn);
+    HIPCHECK(c, "lm inputs",
+             launch_lm_inputs<T>(x, c->at<float>(p.h_last), row_lo,
+                                 static_cast<const T *>(c->final_norm), T_rows, cf.d_model,
+                                 cf.rms_eps, lm_in, s));
+    if constexpr (sizeof(T) == 2) {
+      lm_chunks = lmhead_chunks(cf.vocab);
+      HIPCHECK(c, "lm head",
+               gemm_lmhead(lm_in, static_cast<const bf16 *>(c->lm_head), T_rows, cf.vocab,
+                           cf.d_model, lm_tgt, lm_part, tgt, s));
+    } else {
+      HIPCHECK(c, "lm head",
+               simple_lmhead<T>(lm_in, static_cast<const T *>(c->lm_head), T_rows, cf.vocab,
+                                cf.d_model, lm_tgt, lm_part, tgt, s));
+    }
+  }
+  HIPCHECK(c, "lse gather", launch_lse_gather(br, lm_part, lm_chunks, tgt, logprobs, s));
+  HIPCHECK(c, "reduce/select", launch_reduce_select(br, logprobs, scores, argmax, s));
+  return VSR_OK;
+}
+
+int set_device(vsr_ctx *c) {
+  int cur = -1;
+  if (hipGetDevice(&cur) == hipSuccess && cur == c->device) return VSR_OK;
+  HIPCHECK(c, "hipSetDevice", hipSetDevice(c->device));
+  return VSR_OK;
+}
+
+}  // namespace
+
+extern "C" int vsr_prefill(vsr_ctx *ctx, const void *visual, int32_t n_visual,
+                           const int32_t *ids, int32_t n_text) {
+  if (!ctx) return VSR_EINVAL;
+  if (!ctx->have_weights) return ctx->fail(VSR_ESTATE, "prefill before vsr_load_weights");
+  if (n_visual < 0 || n_text < 0) return ctx->fail(VSR_EINVAL, "negative prefix length");
+  const long long P = (long long)n_visual + n_text;
+  if (P < 1) return ctx->fail(VSR_EINVAL, "empty prefix (n_visual + n_text must be >= 1)");
+  if (P > ctx->cfg.max_prefix)
+    return ctx->fail(VSR_ERANGE, "prefix length %lld exceeds max_prefix %d", P,
+                     ctx->cfg.max_prefix);
+  if (n_visual > 0 && !visual) return ctx->fail(VSR_EINVAL, "visual is NULL");
+  if (n_text > 0 && !ids) return ctx->fail(VSR_EINVAL, "ids is NULL");
+  int rc = set_device(ctx);
+  if (rc) return rc;
+  ctx->prefilled = false;
+  rc = ctx->cfg.dtype == VSR_BF16 ? prefill_impl<bf16>(ctx, visual, n_visual, ids, n_text)
+                                  : prefill_impl<float>(ctx, visual, n_visual, ids, n_text);
+  if (rc == VSR_OK) ctx->prefilled = true;
+  return rc;
+}
+
+extern "C" int vsr_score(vsr_ctx *ctx, const int32_t *cand_ids, const int32_t *cand_len,
+                         int32_t M, int32_t Cmax, float *logprobs, float *scores,
+                         int32_t *argmax) {
+  if (!ctx) return VSR_EINVAL;
+  if (!ctx->prefilled) return ctx->fail(VSR_ESTATE, "score before a successful prefill");
+  if (M < 1 || Cmax < 1) return ctx->fail(VSR_EINVAL, "M and Cmax must be >= 1");
+  if (M > ctx->cfg.max_cands)
+    return ctx->fail(VSR_ERANGE, "M = %d exceeds max_cands %d", M, ctx->cfg.max_cands);
+  if (Cmax > ctx->cfg.max_cand_len)
+    return ctx->fail(VSR_ERANGE, "Cmax = %d exceeds max_cand_len %d", Cmax,
+                     ctx->cfg.max_cand_len);
+  if (!cand_ids || !cand_len || !logprobs || !scores || !argmax)
+    return ctx->fail(VSR_EINVAL, "score: NULL argument");
+  Branches br{};
+  br.M = M;
+  br.cmax = Cmax;
+  br.cu[0] = 0;
+  for (int m = 0; m < M; ++m) {
+    if (cand_len[m] < 0 || cand_len[m] > Cmax)
+      return ctx->fail(VSR_EINVAL, "cand_len[%d] = %d outside [0, Cmax]", m, cand_len[m]);
+    br.cu[m + 1] = br.cu[m] + cand_len[m];
+  }
+  const int rc = set_device(ctx);
+  if (rc) return rc;
+  return ctx->cfg.dtype == VSR_BF16
+             ? score_impl<bf16>(ctx, br, cand_ids, logprobs, scores, argmax)
+             : score_impl<float>(ctx, br, cand_ids, logprobs, scores, argmax);
+}
+
+extern "C" const char *vsr_last_error(const vsr_ctx *ctx) {
+  return ctx ? ctx->err.c_str() : g_create_error.c_str();
+}
+
+extern "C" void vsr_destroy(vsr_ctx *ctx) { delete ctx; }

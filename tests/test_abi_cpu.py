@@ -1,0 +1,82 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every entry point include/vsr.h declares, sizes workspaces and rejects bad
+arguments before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2601_01513_amd import binding as B
+from paper_2601_01513_amd import workload as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _lib():
+    if not os.path.exists(B.LIB_PATH):
+        pytest.skip("libvsr.so not built (python -m paper_2601_01513_amd.build)")
+    return B.load_library()
+
+
+def test_header_symbols_are_exported():
+    lib = _lib()
+    hdr = open(os.path.join(ROOT, "include", "vsr.h")).read()
+    declared = set(re.findall(r"\b(vsr_[a-z_]+)\s*\(", hdr))
+    assert declared == set(B.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+@pytest.mark.parametrize("cfg", W.CONFIGS, ids=lambda c: c.name)
+def test_workspace_size_of_each_workload(cfg):
+    _lib()
+    n = B.workspace_size(B.make_config(cfg))
+    assert n > 0 and n % 256 == 0
+    # The prefix caches alone: 2 L Hkv P hd elements.
+    e = 2 if cfg.dtype == W.BF16 else 4
+    assert n > 2 * cfg.n_layers * cfg.n_kv_heads * cfg.n_prefix * cfg.head_dim * e
+
+
+@pytest.mark.parametrize("field,value", [
+    ("n_heads", 5), ("head_dim", 64), ("d_model", 100), ("dtype", 7), ("max_cands", 0),
+    ("max_cands", B.VSR_MAX_CANDS + 1), ("vocab", 0), ("max_prefix", 0), ("d_ff", 96)])
+def test_invalid_configs_have_no_workspace(field, value):
+    _lib()
+    c = B.make_config(W.B1_5)
+    setattr(c, field, value)
+    assert B.workspace_size(c) == 0
+
+
+def test_create_rejects_bad_arguments():
+    lib = _lib()
+    c = B.make_config(W.TINY_F32)
+    need = lib.vsr_workspace_size(ctypes.byref(c))
+    h = ctypes.c_void_p()
+    assert lib.vsr_create(ctypes.byref(c), None, need, None, ctypes.byref(h)) == B.VSR_EINVAL
+    assert b"workspace" in lib.vsr_last_error(None)
+    assert lib.vsr_create(ctypes.byref(c), 0x1008, need, None, ctypes.byref(h)) == B.VSR_EINVAL
+    assert lib.vsr_create(ctypes.byref(c), 0x10000, need - 1, None, ctypes.byref(h)) == B.VSR_ENOMEM
+    assert lib.vsr_create(None, 0x10000, need, None, ctypes.byref(h)) == B.VSR_EINVAL
+    assert lib.vsr_create(ctypes.byref(c), 0x10000, need, None, None) == B.VSR_EINVAL
+    bad = B.make_config(W.TINY_F32)
+    bad.n_kv_heads = 3
+    assert lib.vsr_create(ctypes.byref(bad), 0x10000, need, None, ctypes.byref(h)) == B.VSR_EINVAL
+    assert b"n_kv_heads" in lib.vsr_last_error(None)
+
+
+def test_null_context_calls_fail_cleanly():
+    lib = _lib()
+    assert lib.vsr_load_weights(None, None) == B.VSR_EINVAL
+    assert lib.vsr_prefill(None, None, 0, None, 1) == B.VSR_EINVAL
+    lens = (ctypes.c_int32 * 1)(1)
+    assert lib.vsr_score(None, None, lens, 1, 1, None, None, None) == B.VSR_EINVAL
+    lib.vsr_destroy(None)
+
+
+def test_workspace_grows_with_the_maxima():
+    _lib()
+    a = B.workspace_size(B.make_config(W.B7))
+    b = B.workspace_size(B.make_config(W.B7, max_prefix=2 * W.B7.n_prefix))
+    c = B.workspace_size(B.make_config(W.B7, max_cands=2 * W.B7.n_cands))
+    assert b > a and c > a

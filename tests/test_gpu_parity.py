@@ -1,0 +1,176 @@
+"""GPU parity: the HIP scoring pass against the CPU oracle, element by element,
+on the same seeded inputs (calls go through the C ABI via the binding).
+
+Tolerances: per-token log-prob within 2e-2 absolute for bf16 workloads and
+1e-4 for fp32; sequence log-likelihood within 1e-2 relative; identical argmax
+whenever the oracle's top-2 margin exceeds 0.1 nats. Padded log-prob slots
+must be exactly 0.
+
+Sizes: small shapes that span several GEMM / attention tiles with ragged
+tails, the tiny fp32 and 1.5B-class workloads in full, and the 7B / long 7B /
+32B workloads at full width and full prefix / candidate sizes with two layers
+(same launches as the full-depth pass, the oracle finishing in seconds).
+"""
+import sys
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2601_01513_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _say(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def run_gpu(wl, cand_ids=None, cand_len=None, verifier=None):
+    torch = _torch()
+    from paper_2601_01513_amd.binding import Verifier
+    cfg = wl.cfg
+    v = verifier or Verifier(cfg, wl.weights, device="cuda")
+    ids = torch.tensor(wl.prefix_ids, dtype=torch.int32, device="cuda") if cfg.n_text else None
+    vis = wl.visual if cfg.n_visual else None
+    v.prefill(vis, ids)
+    cids = wl.cand_ids if cand_ids is None else cand_ids
+    lens = wl.cand_len if cand_len is None else cand_len
+    lp, sc, am = v.score(torch.tensor(cids, dtype=torch.int32, device="cuda"), lens)
+    torch.cuda.synchronize()
+    return lp.cpu().numpy(), sc.cpu().numpy(), int(am.cpu()[0]), v
+
+
+def run_oracle(wl, dtype=np.float64, cand_ids=None, cand_len=None):
+    hw = W.host_weights(wl.weights, lazy=True)
+    vis = W.to_host_f32(wl.visual)
+    cids = wl.cand_ids if cand_ids is None else cand_ids
+    lens = wl.cand_len if cand_len is None else cand_len
+    return oracle.score_shared_prefix(wl.cfg, hw, vis, wl.prefix_ids, cids, lens, dtype=dtype)
+
+
+def check(cfg, gpu, ora, lens):
+    lp_g, sc_g, am_g = gpu[:3]
+    lp_o, sc_o, am_o = ora
+    tol = 1e-4 if cfg.dtype == W.F32 else 2e-2
+    M, cmax = lp_o.shape
+    valid = np.arange(cmax)[None, :] < np.asarray(lens)[:, None]
+    assert np.all(np.isfinite(lp_g))
+    err = np.abs(lp_g - lp_o)[valid]
+    _say(f"  max |dlp| = {err.max() if err.size else 0:.3e} (tol {tol}), "
+         f"scores gpu {np.round(sc_g, 3)} oracle {np.round(sc_o, 3)}")
+    assert np.all(lp_g[~valid] == 0.0)
+    if err.size:
+        assert err.max() <= tol
+    nz = np.abs(sc_o) > 0
+    assert np.all(np.abs(sc_g - sc_o)[nz] <= 1e-2 * np.abs(sc_o)[nz])
+    assert np.all(sc_g[~nz] == 0.0)
+    np.testing.assert_allclose(sc_g, lp_g.sum(axis=1), rtol=1e-5, atol=1e-4)
+    top = np.sort(sc_o)[::-1]
+    if len(top) < 2 or top[0] - top[1] > 0.1:
+        assert am_g == am_o
+    else:
+        assert sc_o[am_g] >= top[0] - 0.1 - 1e-2 * abs(top[0])
+
+
+SMALL_BF16 = W.VerifierConfig(
+    name="small bf16 L2 d256 G2 F320 V1000", n_layers=2, d_model=256, n_heads=4,
+    n_kv_heads=2, head_dim=128, d_ff=320, vocab=1000, rope_base=1e6, dtype=W.BF16,
+    n_prefix=300, n_visual=100, n_cands=5, cand_len=40)
+GQA7_BF16 = W.VerifierConfig(
+    name="small bf16 L2 d896 G7 P700 M8x64", n_layers=2, d_model=896, n_heads=7,
+    n_kv_heads=1, head_dim=128, d_ff=1152, vocab=3001, rope_base=1e6, dtype=W.BF16,
+    n_prefix=700, n_visual=300, n_cands=8, cand_len=64, ragged=(1, 64))
+
+
+def _case(cfg, seed, lens=None):
+    _torch()
+    _say(f"case: {cfg.name} seed {seed}")
+    wl = W.make_workload(cfg, seed, device="cuda")
+    if lens is not None:
+        wl.cand_len = np.asarray(lens, dtype=np.int32)
+        for m in range(cfg.n_cands):
+            wl.cand_ids[m, lens[m]:] = 0
+    return wl
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_tiny_fp32_workload(seed):
+    wl = _case(W.TINY_F32, seed)
+    check(wl.cfg, run_gpu(wl), run_oracle(wl), wl.cand_len)
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_small_bf16_ragged_with_empty_candidate(seed):
+    wl = _case(SMALL_BF16, seed, lens=[40, 1, 0, 23, 37])
+    check(wl.cfg, run_gpu(wl), run_oracle(wl), wl.cand_len)
+
+
+def test_small_fp32_ragged_gqa():
+    cfg = SMALL_BF16.replace(name="small fp32 G2", dtype=W.F32, head_dim=64, d_model=256,
+                             n_heads=4, n_kv_heads=2)
+    wl = _case(cfg, 3, lens=[40, 0, 1, 17, 39])
+    check(cfg, run_gpu(wl), run_oracle(wl), wl.cand_len)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_gqa7_split_prefix_ragged(seed):
+    wl = _case(GQA7_BF16, seed)
+    check(wl.cfg, run_gpu(wl), run_oracle(wl), wl.cand_len)
+
+
+def test_text_only_and_visual_only_prefixes():
+    for nv in (0, SMALL_BF16.n_prefix):
+        cfg = SMALL_BF16.replace(n_visual=nv)
+        wl = _case(cfg, 4, lens=[5, 40, 3, 1, 9])
+        check(cfg, run_gpu(wl), run_oracle(wl), wl.cand_len)
+
+
+def test_rescore_and_replace_prefix():
+    """Several score calls per prefill; a second prefill replaces the prefix."""
+    wl = _case(SMALL_BF16, 5, lens=[40, 2, 7, 23, 37])
+    ora = run_oracle(wl)
+    g1 = run_gpu(wl)
+    v = g1[3]
+    torch = _torch()
+    lp, sc, am = v.score(torch.tensor(wl.cand_ids, dtype=torch.int32, device="cuda"), wl.cand_len)
+    torch.cuda.synchronize()
+    assert np.array_equal(lp.cpu().numpy(), g1[0]) and np.array_equal(sc.cpu().numpy(), g1[1])
+    check(wl.cfg, g1, ora, wl.cand_len)
+    wl2 = _case(SMALL_BF16.replace(n_prefix=130, n_visual=64), 6, lens=[1, 2, 3, 4, 40])
+    wl2.weights = wl.weights
+    check(wl2.cfg, run_gpu(wl2, verifier=v), run_oracle(wl2), wl2.cand_len)
+
+
+@pytest.mark.timeout(900)
+def test_full_1p5b_workload():
+    wl = _case(W.B1_5, 0)
+    t0 = time.time()
+    gpu = run_gpu(wl)
+    _say(f"  gpu done in {time.time() - t0:.1f}s, running oracle")
+    t0 = time.time()
+    ora = run_oracle(wl)
+    _say(f"  oracle done in {time.time() - t0:.1f}s")
+    check(wl.cfg, gpu, ora, wl.cand_len)
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("cfg", [W.B7, W.B7_LONG, W.B32], ids=["7B", "7B-long", "32B"])
+def test_full_width_two_layers(cfg):
+    cfg2 = cfg.replace(name=cfg.name + " (2 layers)", n_layers=2)
+    wl = _case(cfg2, 0)
+    t0 = time.time()
+    gpu = run_gpu(wl)
+    _say(f"  gpu done in {time.time() - t0:.1f}s, running oracle (fp32)")
+    t0 = time.time()
+    ora = run_oracle(wl, dtype=np.float32)
+    _say(f"  oracle done in {time.time() - t0:.1f}s")
+    check(cfg2, gpu, ora, wl.cand_len)
