@@ -1,0 +1,204 @@
+"""Benchmark of the verifier scoring pass on one GPU.
+
+A step is one verify pass: vsr_prefill over the shared prefix followed by
+vsr_score of all candidates (the prefix KV is rebuilt every step). Inputs are
+seeded synthetic tensors resident in HBM before the timed region.
+
+Prints one JSON line: candidate tokens scored per second over the timed steps,
+the roofline position of the dominant kernel (from per-launch HIP-event
+timings inside the library, on its stream, over the same timed region) and
+the CPU oracle timed on a bounded sample on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from paper_2601_01513_amd import workload as W  # noqa: E402
+
+METRIC = ("candidate tokens scored/sec and ms per verify pass "
+          "(7B-class, 4k prefix, 8×64)")
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+# Kernels as the profiler sees them, and the stages each one serves.
+KERNELS = {
+    "k_gemm_swiglu": ["prefill.gate_up_swiglu", "score.gate_up_swiglu"],
+    "k_gemm_residual": ["prefill.o_proj", "prefill.down_proj", "score.o_proj", "score.down_proj"],
+    "k_gemm_qkv": ["prefill.qkv_rope", "score.qkv_rope"],
+    "k_attn<0> (prefill)": ["prefill.attention"],
+    "k_attn<1> (cascade)": ["score.attention"],
+    "k_attn_merge": ["score.attn_merge"],
+    "k_gemm_lmhead": ["score.lm_head_lse"],
+    "k_rmsnorm": ["prefill.rmsnorm", "score.rmsnorm"],
+}
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def stage_flops(cfg, P, lens):
+    """Algorithmic FLOPs of one verify pass per stage (multiply-add = 2)."""
+    d, hq, hd, F, V = cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ff, cfg.vocab
+    L = cfg.n_layers
+    T = int(sum(lens))
+    f = {}
+    for ph, rows in (("prefill", P), ("score", T)):
+        f[f"{ph}.qkv_rope"] = 2.0 * rows * cfg.qkv_rows * d * L
+        f[f"{ph}.o_proj"] = 2.0 * rows * d * hq * hd * L
+        f[f"{ph}.gate_up_swiglu"] = 2.0 * rows * 2 * F * d * L
+        f[f"{ph}.down_proj"] = 2.0 * rows * d * F * L
+    # QK^T and PV over the visible keys of every query (causal / cascade).
+    f["prefill.attention"] = 4.0 * hd * hq * (P * (P + 1) / 2) * L
+    f["score.attention"] = 4.0 * hd * hq * sum(n * P + n * (n + 1) / 2 for n in lens) * L
+    f["score.lm_head_lse"] = 2.0 * T * V * d
+    return f
+
+
+def cpu_baseline(wl, log_fn):
+    """The oracle (float64, shared-prefix mode) on the same workload with 1 and
+    2 of its layers; the per-layer cost is extrapolated to the full depth."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()
+                       if i.get("user_api") == "blas"] or [os.cpu_count() or 1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    cfg = wl.cfg
+    hw = {"embed": W.to_host_f32(wl.weights["embed"]),
+          "lm_head": W.to_host_f32(wl.weights["lm_head"]),
+          "final_norm": W.to_host_f32(wl.weights["final_norm"])}
+    vis = W.to_host_f32(wl.visual)
+    times = {}
+    for nl in (1, 2):
+        w = dict(hw, layers=W.HostLayers(wl.weights["layers"][:nl]))
+        c = cfg.replace(n_layers=nl)
+        t0 = time.perf_counter()
+        oracle.score_shared_prefix(c, w, vis, wl.prefix_ids, wl.cand_ids, wl.cand_len,
+                                   dtype=np.float64)
+        times[nl] = time.perf_counter() - t0
+        log_fn(f"cpu oracle: {nl} layer(s) in {times[nl]:.1f}s")
+    per_layer = max(times[2] - times[1], 1e-9)
+    base = max(times[1] - per_layer, 0.0)
+    full = base + per_layer * cfg.n_layers
+    tokens = int(sum(wl.cand_len))
+    return {"value": tokens / full, "unit": "candidate tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": (f"float64 oracle, shared-prefix mode, on this workload with 1 and 2 of "
+                       f"its {cfg.n_layers} layers ({times[1]:.1f}s, {times[2]:.1f}s); "
+                       f"per-layer time extrapolated to {cfg.n_layers} layers = "
+                       f"{full:.1f}s per verify pass")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=2,
+                    help="index into the workload list (default: the 7B-class 4k prefix 8x64)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--stages", action="store_true", help="print per-stage times to stderr")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the scoring pass is "
+              "not sharded across GPUs", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2601_01513_amd.binding import Verifier
+
+    cfg = W.CONFIGS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"workload: {cfg.name}; generating inputs on the GPU")
+    wl = W.make_workload(cfg, args.seed, device=dev)
+    ids = torch.tensor(wl.prefix_ids, dtype=torch.int32, device=dev) if cfg.n_text else None
+    vis = wl.visual if cfg.n_visual else None
+    cids = torch.tensor(wl.cand_ids, dtype=torch.int32, device=dev)
+    lens = [int(x) for x in wl.cand_len]
+    v = Verifier(cfg, wl.weights, device=dev)
+    M, cmax = cids.shape
+    out = (torch.empty((M, cmax), dtype=torch.float32, device=dev),
+           torch.empty(M, dtype=torch.float32, device=dev),
+           torch.empty(1, dtype=torch.int32, device=dev))
+
+    def step():
+        v.prefill(vis, ids)
+        v.score(cids, lens, out=out)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps); timing {args.steps} steps")
+
+    v.profile(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    stages = v.profile_read()
+    v.profile(False)
+
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    tokens = sum(lens)
+    value = tokens / (ms_step / 1e3)
+    flops = stage_flops(cfg, cfg.n_prefix, lens)
+
+    per_step = {k: ms / args.steps for k, (ms, n) in stages.items()}
+    if args.stages:
+        for k, ms in sorted(per_step.items(), key=lambda kv: -kv[1]):
+            tf = flops.get(k, 0.0) / (ms * 1e-3) / 1e12 if ms > 0 else 0.0
+            log(f"  {k:28s} {ms:8.3f} ms/step  {stages[k][1] // args.steps:4d} launches"
+                + (f"  {tf:7.1f} TFLOP/s" if k in flops else ""))
+
+    # Dominant kernel: largest summed time over the timed region.
+    ktime = {k: sum(stages.get(s, (0.0, 0))[0] for s in ss) for k, ss in KERNELS.items()}
+    kname = max(ktime, key=ktime.get)
+    kst = KERNELS[kname]
+    launches = sum(stages.get(s, (0.0, 0))[1] for s in kst)
+    kflops = sum(flops.get(s, 0.0) for s in kst) * args.steps
+    avg_ms = ktime[kname] / max(launches, 1)
+    achieved = kflops / launches / (avg_ms * 1e-3) / 1e12
+    roofline = {"kernel": kname, "bound": "mfma", "achieved": round(achieved, 1),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "launches": launches, "avg_launch_ms": round(avg_ms, 4),
+                "flop_per_launch": kflops / launches}
+
+    pre = sum(ms for k, ms in per_step.items() if k.startswith("prefill."))
+    sco = sum(ms for k, ms in per_step.items() if k.startswith("score."))
+    result = {
+        "metric": METRIC, "value": round(value, 1), "unit": "candidate tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if cfg.dtype == W.BF16 else "f32",
+        "data": "synthetic (seeded, random-init weights)",
+        "config": {"workload": cfg.name, "layers": cfg.n_layers, "d_model": cfg.d_model,
+                   "heads": f"{cfg.n_heads}/{cfg.n_kv_heads}", "d_ff": cfg.d_ff,
+                   "vocab": cfg.vocab, "prefix": cfg.n_prefix, "visual_rows": cfg.n_visual,
+                   "candidates": M, "cand_len": cmax, "tokens_scored": tokens},
+        "breakdown": {"prefill_kernel_ms": round(pre, 3), "score_kernel_ms": round(sco, 3),
+                      "score_only_tok_s": round(tokens / (sco / 1e3), 1) if sco else None},
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, log)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -141,6 +141,25 @@ const char *vsr_last_error(const vsr_ctx *ctx);
 /* Releases the context (not the workspace or the weights). NULL is a no-op. */
 void vsr_destroy(vsr_ctx *ctx);
 
+/* ---- measurement (not part of the method) ----------------------------------
+ * Per-stage kernel timing for benchmarks: while enabled, every stage launch of
+ * vsr_prefill / vsr_score is bracketed by HIP events on the context's stream.
+ * Stage s of the prefix pass is s, of the candidate pass VSR_STAGE_KINDS + s;
+ * kinds: 0 embedding, 1 RMSNorm, 2 QKV projection + rotary + cache write,
+ * 3 attention, 4 attention merge, 5 output projection, 6 gate/up + SwiGLU,
+ * 7 down projection, 8 LM-head inputs, 9 LM head + chunk LSE,
+ * 10 LSE merge + target gather, 11 sum + argmax, 12 row tables, 13 copy. */
+#define VSR_STAGE_KINDS 14
+#define VSR_STAGES (2 * VSR_STAGE_KINDS)
+
+/* Turns stage timing on (1) or off (0); clears what was recorded. */
+int vsr_profile_enable(vsr_ctx *ctx, int enable);
+
+/* Waits for the recorded launches, then writes, for every stage, the summed
+ * kernel time in milliseconds (ms, HOST [VSR_STAGES]) and the number of
+ * launches (launches, HOST [VSR_STAGES]) since the last read, and clears them. */
+int vsr_profile_read(vsr_ctx *ctx, double *ms, int32_t *launches);
+
 #ifdef __cplusplus
 }
 #endif

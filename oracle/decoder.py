@@ -204,14 +204,16 @@ def score_bruteforce(cfg, weights: Dict, visual, prefix_ids, cand_ids, cand_len,
 
 
 def score_shared_prefix(cfg, weights: Dict, visual, prefix_ids, cand_ids, cand_len,
-                        dtype=np.float64, cands: Optional[List[int]] = None):
+                        dtype=np.float64, cands: Optional[List[int]] = None,
+                        progress=None):
     """Shared-prefix mode: the prefix is run once, each layer's rotated prefix
     keys/values are reused by every candidate. Exactly the definition above
     re-associated (a candidate token's visible keys are the prefix keys plus
     its own earlier tokens, as in one full causal sequence).
 
     `cands` restricts the work to some candidates (the others get lp = 0 and
-    score = nan). Returns (lp, score, argmax or -1 if restricted).
+    score = nan); `progress(layer)` is called after each layer.
+    Returns (lp, score, argmax or -1 if restricted).
     """
     P = cfg.n_visual + len(prefix_ids)
     M, cmax = np.asarray(cand_ids).shape
@@ -220,7 +222,7 @@ def score_shared_prefix(cfg, weights: Dict, visual, prefix_ids, cand_ids, cand_l
     x_pre = embed_prefix(weights, visual, prefix_ids, dtype)
     pos_pre = np.arange(P)
     xs = {m: e[np.asarray(cand_ids[m, :int(cand_len[m])])] for m in todo}
-    for lw in weights["layers"]:
+    for li, lw in enumerate(weights["layers"]):
         x_next, kp, vp = decoder_layer(x_pre, lw, pos_pre, cfg, dtype)
         for m in todo:
             n = xs[m].shape[0]
@@ -228,6 +230,8 @@ def score_shared_prefix(cfg, weights: Dict, visual, prefix_ids, cand_ids, cand_l
                 xs[m], _, _ = decoder_layer(xs[m], lw, P + np.arange(n), cfg, dtype,
                                             kp, vp, pos_pre)
         x_pre = x_next
+        if progress is not None:
+            progress(li)
     lp = np.zeros((M, cmax), dtype=dtype)
     scores = np.full(M, np.nan, dtype=dtype)
     for m in todo:

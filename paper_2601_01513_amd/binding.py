@@ -18,7 +18,15 @@ VSR_F32, VSR_BF16 = 0, 1
 VSR_MAX_CANDS = 256
 
 EXPORTS = ["vsr_workspace_size", "vsr_create", "vsr_load_weights", "vsr_prefill",
-           "vsr_score", "vsr_last_error", "vsr_destroy"]
+           "vsr_score", "vsr_last_error", "vsr_destroy", "vsr_profile_enable",
+           "vsr_profile_read"]
+
+VSR_STAGE_KINDS = 14
+VSR_STAGES = 2 * VSR_STAGE_KINDS
+STAGE_KINDS = ["embed", "rmsnorm", "qkv_rope", "attention", "attn_merge", "o_proj",
+               "gate_up_swiglu", "down_proj", "lm_inputs", "lm_head_lse", "lse_gather",
+               "sum_argmax", "row_tables", "copy"]
+STAGE_NAMES = [f"prefill.{k}" for k in STAGE_KINDS] + [f"score.{k}" for k in STAGE_KINDS]
 
 
 class VsrConfig(ctypes.Structure):
@@ -76,6 +84,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vsr_last_error.restype = ctypes.c_char_p
     lib.vsr_destroy.argtypes = [ctypes.c_void_p]
     lib.vsr_destroy.restype = None
+    lib.vsr_profile_enable.argtypes = [ctypes.c_void_p, ctypes.c_int]
+    lib.vsr_profile_enable.restype = ctypes.c_int
+    lib.vsr_profile_read.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_double),
+                                     ctypes.POINTER(ctypes.c_int32)]
+    lib.vsr_profile_read.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -161,6 +174,17 @@ class Verifier:
         self._check(self.lib.vsr_score(self.h, _ptr(cand_ids), lens, M, cmax, _ptr(lp),
                                        _ptr(sc), _ptr(am)))
         return lp, sc, am
+
+    def profile(self, enable: bool):
+        """Turns per-stage kernel timing on or off (clears recorded launches)."""
+        self._check(self.lib.vsr_profile_enable(self.h, 1 if enable else 0))
+
+    def profile_read(self) -> Dict[str, tuple]:
+        """{stage name: (summed ms, launches)} since the last read."""
+        ms = (ctypes.c_double * VSR_STAGES)()
+        n = (ctypes.c_int32 * VSR_STAGES)()
+        self._check(self.lib.vsr_profile_read(self.h, ms, n))
+        return {STAGE_NAMES[i]: (ms[i], n[i]) for i in range(VSR_STAGES) if n[i]}
 
     def close(self):
         if getattr(self, "h", None):

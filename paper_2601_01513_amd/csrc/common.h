@@ -9,17 +9,28 @@
 namespace vsr {
 
 typedef __bf16 bf16;
+typedef _Float16 f16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float to_f32(float x) { return x; }
 __device__ __forceinline__ float to_f32(bf16 x) { return static_cast<float>(x); }
+__device__ __forceinline__ float to_f32(f16 x) { return static_cast<float>(x); }
 template <typename T> __device__ __forceinline__ T from_f32(float x);
 template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return static_cast<bf16>(x); }
+template <> __device__ __forceinline__ f16 from_f32<f16>(float x) { return static_cast<f16>(x); }
+
+// Arithmetic types of the two paths. A VSR_BF16 context keeps its weights in
+// bf16 and its activations (GEMM / attention operands) in fp16: every bf16
+// weight converts exactly to fp16 (8 significant bits fit in 11), and the
+// fp16 operands carry 3 more mantissa bits than bf16 at the same MFMA rate.
+// A VSR_F32 context is fp32 throughout.
 
 // Largest number of candidates one score call may carry.
 constexpr int kMaxCands = 256;
@@ -53,15 +64,15 @@ template <typename T>
 hipError_t launch_embed_rows(const int32_t *ids, int rows, const T *embed, int d, float *x,
                              hipStream_t s);
 
-// y[r] = T(x[r] / sqrt(mean(x[r]^2) + eps) * g) for rows r < rows.
-template <typename T>
-hipError_t launch_rmsnorm(const float *x, const T *g, int rows, int d, float eps, T *y,
+// y[r] = TA(x[r] / sqrt(mean(x[r]^2) + eps) * g) for rows r < rows.
+template <typename TW, typename TA>
+hipError_t launch_rmsnorm(const float *x, const TW *g, int rows, int d, float eps, TA *y,
                           hipStream_t s);
 // LM-head inputs of a score call: y[t] = norm(h_last) if t is the first row
 // of its candidate, else norm(x[t - 1]).
-template <typename T>
+template <typename TW, typename TA>
 hipError_t launch_lm_inputs(const float *x, const float *h_last, const int32_t *row_lo,
-                            const T *g, int T_rows, int d, float eps, T *y, hipStream_t s);
+                            const TW *g, int T_rows, int d, float eps, TA *y, hipStream_t s);
 
 // Per-row merge of the LM-head partials: lse over the vocabulary chunks,
 // lp = target logit - lse, scattered to logprobs[m][j] (zeros elsewhere).
@@ -86,20 +97,21 @@ struct QKVOut {
   const float2 *rope;      // rotary table [npos][hd/2]
 };
 
-// ------------------------------------------------------------ bf16 MFMA path
-// C = A[rows][K] . B[N][K]^T with fused epilogues.
-hipError_t gemm_qkv_rope(const bf16 *A, const bf16 *W, int rows, int K, int n_heads,
-                         int n_kv, const QKVOut<bf16> &out, hipStream_t s);
+// ------------------------------------------------------------ MFMA path
+// C = A[rows][K] . W[N][K]^T with fused epilogues; A fp16 activations, W bf16
+// weights (converted to fp16 on their way into LDS), fp32 accumulation.
+hipError_t gemm_qkv_rope(const f16 *A, const bf16 *W, int rows, int K, int n_heads,
+                         int n_kv, const QKVOut<f16> &out, hipStream_t s);
 // x[rows][N] += A . W^T (residual stream, fp32).
-hipError_t gemm_residual(const bf16 *A, const bf16 *W, int rows, int N, int K, float *x,
+hipError_t gemm_residual(const f16 *A, const bf16 *W, int rows, int N, int K, float *x,
                          hipStream_t s);
 // h[rows][F] = silu(A . Wg^T) * (A . Wu^T), W = [Wg; Wu] ([2F][K]).
-hipError_t gemm_swiglu(const bf16 *A, const bf16 *W, int rows, int F, int K, bf16 *h,
+hipError_t gemm_swiglu(const f16 *A, const bf16 *W, int rows, int F, int K, f16 *h,
                        hipStream_t s);
 // LM head: per (vocab chunk c, row t): part[c][t] = (max, sum exp(l - max)) over
 // the chunk's logits l = W[v] . A[t]; tgt_logit[t] = logit of lm_tgt[t].
 int lmhead_chunks(int vocab);
-hipError_t gemm_lmhead(const bf16 *A, const bf16 *W, int rows, int vocab, int K,
+hipError_t gemm_lmhead(const f16 *A, const bf16 *W, int rows, int vocab, int K,
                        const int32_t *lm_tgt, float2 *part, float *tgt_logit, hipStream_t s);
 
 // Attention of query rows against one key source. Query row r of KV head h is
@@ -109,12 +121,12 @@ hipError_t gemm_lmhead(const bf16 *A, const bf16 *W, int rows, int vocab, int K,
 //   mode 1 (cascade)  : prefix keys [0, P) all visible, then the branch keys
 //                       [row_lo[t], t] of the token's own candidate.
 struct AttnArgs {
-  const bf16 *q;        // [T][n_heads][hd]
-  const bf16 *k;        // prefix / own K cache of this layer
-  const bf16 *vt;       // prefix / own Vt cache
+  const f16 *q;         // [T][n_heads][hd]
+  const f16 *k;         // prefix / own K cache of this layer
+  const f16 *vt;        // prefix / own Vt cache
   int kv_npos;          // position stride of k / vt
-  const bf16 *bk;       // mode 1: branch K  [n_kv][bk_npos][hd]
-  const bf16 *bvt;      // mode 1: branch Vt [n_kv][hd][bk_npos]
+  const f16 *bk;        // mode 1: branch K  [n_kv][bk_npos][hd]
+  const f16 *bvt;       // mode 1: branch Vt [n_kv][hd][bk_npos]
   int bk_npos;
   const int32_t *row_lo;  // mode 1
   int T;                // query tokens
@@ -122,7 +134,7 @@ struct AttnArgs {
   int n_heads, n_kv;
   int nchunks;          // mode 1: prefix split (partials when > 1)
   int chunk;            // prefix keys per split
-  bf16 *out;            // [T][n_heads][hd] when nchunks == 1
+  f16 *out;             // [T][n_heads][hd] when nchunks == 1
   float *part_acc;      // [nchunks][n_kv][T*G][hd]
   float2 *part_ml;      // [nchunks][n_kv][T*G]
 };

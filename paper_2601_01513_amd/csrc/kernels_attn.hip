@@ -15,7 +15,7 @@
 // straight from registers: the k-index of that product is permuted to match
 // the key order the S^T accumulator leaves in each lane, and V^T is staged
 // with the same permutation (the Vt cache stores values position-contiguous).
-// Softmax runs online in the log2 domain in fp32; P is rounded to bf16 for the
+// Softmax runs online in the log2 domain in fp32; P is rounded to fp16 for the
 // PV product.
 //
 // The candidate pass may split the prefix keys into chunks (more blocks on the
@@ -31,7 +31,7 @@ constexpr int HD = 128;   // head dim of the MFMA path
 constexpr int QT = 128;   // stacked query rows per block
 constexpr int KT = 64;    // keys per tile
 
-__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ f16x8 as_f16x8(u32x4 v) { return __builtin_bit_cast(f16x8, v); }
 
 // K tile [64 keys][128 dims]: 16 chunks per key, XOR-swizzled by key.
 __device__ __forceinline__ int ks_idx(int key, int c) { return key * 16 + (c ^ (key & 7)); }
@@ -44,8 +44,8 @@ __device__ __forceinline__ int vs_idx(int d, int c) { return d * 8 + (c ^ (d & 7
 enum SegMode { SEG_ALL = 0, SEG_CAUSAL = 1, SEG_BRANCH = 2 };
 
 struct Seg {
-  const bf16 *k;   // [npos][HD] of this KV head
-  const bf16 *vt;  // [HD][npos] of this KV head
+  const f16 *k;    // [npos][HD] of this KV head
+  const f16 *vt;   // [HD][npos] of this KV head
   int npos;        // position stride of vt
   int kvalid;      // keys >= kvalid hold no data (never visible)
   int kbeg, kend;  // key range walked by the block: [kbeg, kend), kbeg % 64 == 0
@@ -57,7 +57,7 @@ struct Lane {
   int lo;    // SEG_BRANCH: first visible key
   float m, l;
   f32x16 o[HD / 32];
-  bf16x8 q[HD / 16];
+  f16x8 q[HD / 16];
 };
 
 __device__ __forceinline__ void load_tile(const Seg &sg, int kb, u32x4 (&rk)[4], u32x4 (&rv)[4]) {
@@ -116,7 +116,7 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *Ks
     const int key = b * 32 + (lane & 31);
 #pragma unroll
     for (int kk = 0; kk < HD / 16; ++kk)
-      s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(Ks[ks_idx(key, 2 * kk + h)]),
+      s[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_f16x8(Ks[ks_idx(key, 2 * kk + h)]),
                                                      L.q[kk], s[b], 0, 0, 0);
   }
   // Mask and scale; key of register r of block b: kb + 32b + 8(r/4) + 4h + r%4.
@@ -138,14 +138,14 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *Ks
   const float mref = mnew == -INFINITY ? 0.f : mnew;
   const float alpha = exp2f(L.m - mref);
   float psum = 0.f;
-  bf16x8 p[4];
+  f16x8 p[4];
 #pragma unroll
   for (int b = 0; b < 2; ++b)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const float e = exp2f(s[b][r] - mref);
       psum += e;
-      p[b * 2 + (r >> 3)][r & 7] = static_cast<bf16>(e);
+      p[b * 2 + (r >> 3)][r & 7] = static_cast<f16>(e);
     }
   psum += __shfl_xor(psum, 32, 64);
   L.l = L.l * alpha + psum;
@@ -165,8 +165,8 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *Ks
       const uint64_t *r1 =
           reinterpret_cast<const uint64_t *>(&Vs[vs_idx(d, 2 * c + 1)]) + (h ^ sw);
       uint64_t v2[2] = {*r0, *r1};
-      const bf16x8 va = __builtin_bit_cast(bf16x8, v2);
-      L.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, p[c], L.o[db], 0, 0, 0);
+      const f16x8 va = __builtin_bit_cast(f16x8, v2);
+      L.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, p[c], L.o[db], 0, 0, 0);
     }
   }
 }
@@ -216,7 +216,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   {
     const u32x4 *qp = reinterpret_cast<const u32x4 *>(a.q + ((long)L.tok * a.n_heads + head) * HD);
 #pragma unroll
-    for (int kk = 0; kk < HD / 16; ++kk) L.q[kk] = as_bf16x8(qp[2 * kk + (lane >> 5)]);
+    for (int kk = 0; kk < HD / 16; ++kk) L.q[kk] = as_f16x8(qp[2 * kk + (lane >> 5)]);
   }
   const float scale_log2 = 1.4426950408889634f * rsqrtf((float)HD);
   const int tok_last = min(q0 + QT - 1, TG - 1) / G;
@@ -244,15 +244,15 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const int h = lane >> 5;
   if (MODE == 0 || a.nchunks == 1) {
     const float inv = 1.f / L.l;
-    bf16 *op = a.out + ((long)L.tok * a.n_heads + head) * HD;
+    f16 *op = a.out + ((long)L.tok * a.n_heads + head) * HD;
 #pragma unroll
     for (int db = 0; db < HD / 32; ++db)
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
-        bf16x4 v;
+        f16x4 v;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = static_cast<bf16>(L.o[db][g4 * 4 + j] * inv);
-        *reinterpret_cast<bf16x4 *>(op + db * 32 + 8 * g4 + 4 * h) = v;
+        for (int j = 0; j < 4; ++j) v[j] = static_cast<f16>(L.o[db][g4 * 4 + j] * inv);
+        *reinterpret_cast<f16x4 *>(op + db * 32 + 8 * g4 + 4 * h) = v;
       }
   } else {
     const long prow = ((long)chunk * a.n_kv + kvh) * TG + row;
@@ -288,9 +288,9 @@ __global__ __launch_bounds__(64) void k_attn_merge(AttnArgs a) {
     o1 += a.part_acc[prow * HD + 64 + lane] * wgt;
   }
   const float inv = 1.f / Lsum;
-  bf16 *op = a.out + ((long)t * a.n_heads + head) * HD;
-  op[lane] = static_cast<bf16>(o0 * inv);
-  op[64 + lane] = static_cast<bf16>(o1 * inv);
+  f16 *op = a.out + ((long)t * a.n_heads + head) * HD;
+  op[lane] = static_cast<f16>(o0 * inv);
+  op[64 + lane] = static_cast<f16>(o1 * inv);
 }
 
 }  // namespace

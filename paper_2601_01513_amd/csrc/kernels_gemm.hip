@@ -2,14 +2,16 @@
 //
 // Every GEMM here is C = A . B^T with A [rows][K] and B [N][K] both
 // K-contiguous (activations and nn.Linear weights), fp32 accumulation on the
-// gfx950 v_mfma_f32_32x32x16_bf16 matrix cores. A 256-thread block owns a
+// gfx950 v_mfma_f32_32x32x16_f16 matrix cores. Activations are fp16; the bf16
+// weight operand is converted to fp16 in registers on its way into LDS (exact:
+// a bf16 value's 8 significant bits fit fp16's 11). A 256-thread block owns a
 // BM x BN tile; its four waves form a WM x WN grid and each wave owns a
 // (BM/WM) x (BN/WN) sub-tile of 32x32 MFMA blocks. K advances in steps of 64:
 // the next A/B panels are fetched into registers while the MFMAs consume the
 // current panels from LDS (16-byte chunks, XOR-swizzled by row so that both
 // the panel stores and the fragment loads are free of bank conflicts).
 //
-// MFMA 32x32x16 lane layout (lane l, element e, accumulator register r):
+// MFMA 32x32x16 (f16 and bf16 alike) lane layout (lane l, element e, accumulator register r):
 //   A operand: A[i = l % 32][k = 8 (l / 32) + e]
 //   B operand: B[k = 8 (l / 32) + e][j = l % 32]
 //   result   : C[i = 8 (r / 4) + 4 (l / 32) + r % 4][j = l % 32]
@@ -34,7 +36,25 @@ struct Tile {
 
 __device__ __forceinline__ int swz(int row, int c) { return row * 8 + (c ^ (row & 7)); }
 
-__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ f16x8 as_f16x8(u32x4 v) { return __builtin_bit_cast(f16x8, v); }
+
+// Eight bf16 values -> eight fp16 values (exact for |v| in [2^-17, 65504];
+// smaller magnitudes truncate below 2^-24).
+__device__ __forceinline__ u32x4 bf16x8_to_f16x8(u32x4 v) {
+  u32x4 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float lo = __uint_as_float(v[i] << 16);
+    const float hi = __uint_as_float(v[i] & 0xFFFF0000u);
+    r[i] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(lo, hi));
+  }
+  return r;
+}
+template <bool CVT>
+__device__ __forceinline__ u32x4 stage(u32x4 v) {
+  if constexpr (CVT) return bf16x8_to_f16x8(v);
+  return v;
+}
 
 // Output row / column (within the block tile) of accumulator register r of
 // MFMA block (fm, fn) for this lane.
@@ -49,11 +69,14 @@ __device__ __forceinline__ int acc_col(int wn, int fn, int lane) {
 
 // Main loop: acc += A[m0 .. m0+BM) . B[rows given by brow(lr)]^T over all of K.
 // A rows past `rows` are clamped to the last row (their results are never
-// stored); brow must return an in-range B row for every lr < BN.
-template <class TL, class BRow>
-__device__ __forceinline__ void mainloop(const bf16 *__restrict__ A, int rows, int m0,
-                                         const bf16 *__restrict__ B, BRow brow, int K,
+// stored); brow must return an in-range B row for every lr < BN. CVT_A / CVT_B
+// mark an operand stored as bf16 in memory (converted to fp16 when staged).
+template <class TL, bool CVT_A, bool CVT_B, class BRow>
+__device__ __forceinline__ void mainloop(const void *__restrict__ Av, int rows, int m0,
+                                         const void *__restrict__ Bv, BRow brow, int K,
                                          u32x4 *lds, f32x16 (&acc)[TL::FM][TL::FN]) {
+  const uint16_t *A = static_cast<const uint16_t *>(Av);
+  const uint16_t *B = static_cast<const uint16_t *>(Bv);
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int wm = w / TL::WN, wn = w % TL::WN;
   u32x4 *As = lds;
@@ -89,9 +112,9 @@ __device__ __forceinline__ void mainloop(const bf16 *__restrict__ A, int rows, i
 #pragma unroll
   for (int i = 0; i < TL::B_LOADS; ++i) rb[i] = gb[i][0];
 #pragma unroll
-  for (int i = 0; i < TL::A_LOADS; ++i) As[la[i]] = ra[i];
+  for (int i = 0; i < TL::A_LOADS; ++i) As[la[i]] = stage<CVT_A>(ra[i]);
 #pragma unroll
-  for (int i = 0; i < TL::B_LOADS; ++i) Bs[lb[i]] = rb[i];
+  for (int i = 0; i < TL::B_LOADS; ++i) Bs[lb[i]] = stage<CVT_B>(rb[i]);
   __syncthreads();
 
   // Fragment rows of this lane.
@@ -114,24 +137,24 @@ __device__ __forceinline__ void mainloop(const bf16 *__restrict__ A, int rows, i
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       const int c = ks * 2 + hc;
-      bf16x8 af[TL::FM], bfr[TL::FN];
+      f16x8 af[TL::FM], bfr[TL::FN];
 #pragma unroll
-      for (int fm = 0; fm < TL::FM; ++fm) af[fm] = as_bf16x8(As[swz(fa[fm], c)]);
+      for (int fm = 0; fm < TL::FM; ++fm) af[fm] = as_f16x8(As[swz(fa[fm], c)]);
 #pragma unroll
-      for (int fn = 0; fn < TL::FN; ++fn) bfr[fn] = as_bf16x8(Bs[swz(fb[fn], c)]);
+      for (int fn = 0; fn < TL::FN; ++fn) bfr[fn] = as_f16x8(Bs[swz(fb[fn], c)]);
 #pragma unroll
       for (int fm = 0; fm < TL::FM; ++fm)
 #pragma unroll
         for (int fn = 0; fn < TL::FN; ++fn)
           acc[fm][fn] =
-              __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[fm], bfr[fn], acc[fm][fn], 0, 0, 0);
+              __builtin_amdgcn_mfma_f32_32x32x16_f16(af[fm], bfr[fn], acc[fm][fn], 0, 0, 0);
     }
     __syncthreads();
     if (more) {
 #pragma unroll
-      for (int i = 0; i < TL::A_LOADS; ++i) As[la[i]] = ra[i];
+      for (int i = 0; i < TL::A_LOADS; ++i) As[la[i]] = stage<CVT_A>(ra[i]);
 #pragma unroll
-      for (int i = 0; i < TL::B_LOADS; ++i) Bs[lb[i]] = rb[i];
+      for (int i = 0; i < TL::B_LOADS; ++i) Bs[lb[i]] = stage<CVT_B>(rb[i]);
       __syncthreads();
     }
   }
@@ -145,13 +168,14 @@ typedef Tile<128, 256, 2, 2> TileStd;
 
 // ------------------------------------------------------- residual (O, down)
 template <class TL>
-__global__ __launch_bounds__(256) void k_gemm_residual(const bf16 *__restrict__ A,
+__global__ __launch_bounds__(256) void k_gemm_residual(const f16 *__restrict__ A,
                                                        const bf16 *__restrict__ W, int rows,
                                                        int N, int K, float *__restrict__ x) {
   __shared__ u32x4 lds[TL::LDS_CHUNKS];
   const int n0 = blockIdx.x * TL::BN, m0 = blockIdx.y * TL::BM;
   f32x16 acc[TL::FM][TL::FN];
-  mainloop<TL>(A, rows, m0, W, [=](int r) { return min(n0 + r, N - 1); }, K, lds, acc);
+  mainloop<TL, false, true>(A, rows, m0, W, [=](int r) { return min(n0 + r, N - 1); }, K, lds,
+                            acc);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w / TL::WN, wn = w % TL::WN;
 #pragma unroll
@@ -168,7 +192,7 @@ __global__ __launch_bounds__(256) void k_gemm_residual(const bf16 *__restrict__ 
   }
 }
 
-hipError_t gemm_residual(const bf16 *A, const bf16 *W, int rows, int N, int K, float *x,
+hipError_t gemm_residual(const f16 *A, const bf16 *W, int rows, int N, int K, float *x,
                          hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
@@ -183,14 +207,14 @@ hipError_t gemm_residual(const bf16 *A, const bf16 *W, int rows, int N, int K, f
 // rows, so MFMA blocks fn and fn+2 of a wave hold gate and up of the same
 // output columns.
 template <class TL>
-__global__ __launch_bounds__(256) void k_gemm_swiglu(const bf16 *__restrict__ A,
+__global__ __launch_bounds__(256) void k_gemm_swiglu(const f16 *__restrict__ A,
                                                      const bf16 *__restrict__ W, int rows,
-                                                     int F, int K, bf16 *__restrict__ h) {
+                                                     int F, int K, f16 *__restrict__ h) {
   static_assert(TL::WN == 2 && TL::TN == 128, "gate/up pairing needs 128-column waves");
   __shared__ u32x4 lds[TL::LDS_CHUNKS];
   const int o0 = blockIdx.x * 128, m0 = blockIdx.y * TL::BM;
   f32x16 acc[TL::FM][TL::FN];
-  mainloop<TL>(A, rows, m0, W,
+  mainloop<TL, false, true>(A, rows, m0, W,
                [=](int r) {
                  const int q = r & 127;
                  const int oc = min(o0 + (r >> 7) * 64 + (q & 63), F - 1);
@@ -210,12 +234,12 @@ __global__ __launch_bounds__(256) void k_gemm_swiglu(const bf16 *__restrict__ A,
         const int row = m0 + acc_row<TL>(wm, fm, r, lane);
         if (row >= rows) continue;
         const float g = acc[fm][fn][r], u = acc[fm][fn + 2][r];
-        h[(long)row * F + col] = static_cast<bf16>(g / (1.f + __expf(-g)) * u);
+        h[(long)row * F + col] = static_cast<f16>(g / (1.f + __expf(-g)) * u);
       }
   }
 }
 
-hipError_t gemm_swiglu(const bf16 *A, const bf16 *W, int rows, int F, int K, bf16 *h,
+hipError_t gemm_swiglu(const f16 *A, const bf16 *W, int rows, int F, int K, f16 *h,
                        hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
@@ -229,16 +253,17 @@ hipError_t gemm_swiglu(const bf16 *A, const bf16 *W, int rows, int F, int K, bf1
 // head slot 2 blockIdx.x + wn. MFMA blocks fn and fn+2 hold head dims d and
 // d + 64, the rotate-half pair.
 template <class TL>
-__global__ __launch_bounds__(256) void k_gemm_qkv(const bf16 *__restrict__ A,
+__global__ __launch_bounds__(256) void k_gemm_qkv(const f16 *__restrict__ A,
                                                   const bf16 *__restrict__ W, int rows, int K,
-                                                  int n_heads, int n_kv, QKVOut<bf16> o) {
+                                                  int n_heads, int n_kv, QKVOut<f16> o) {
   static_assert(TL::WN == 2 && TL::TN == 128, "one head per wave");
   __shared__ u32x4 lds[TL::LDS_CHUNKS];
   const int nslots = n_heads + 2 * n_kv;
   const int n0 = blockIdx.x * 256, m0 = blockIdx.y * TL::BM;
   const int nrows = nslots * 128;
   f32x16 acc[TL::FM][TL::FN];
-  mainloop<TL>(A, rows, m0, W, [=](int r) { return min(n0 + r, nrows - 1); }, K, lds, acc);
+  mainloop<TL, false, true>(A, rows, m0, W, [=](int r) { return min(n0 + r, nrows - 1); }, K,
+                            lds, acc);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w / TL::WN, wn = w % TL::WN;
   const int slot = blockIdx.x * 2 + wn;
@@ -262,24 +287,24 @@ __global__ __launch_bounds__(256) void k_gemm_qkv(const bf16 *__restrict__ A,
           x2 = y2;
         }
         if (slot < n_heads) {
-          bf16 *q = o.q + ((long)row * n_heads + slot) * 128;
-          q[d] = static_cast<bf16>(x1);
-          q[d + 64] = static_cast<bf16>(x2);
+          f16 *q = o.q + ((long)row * n_heads + slot) * 128;
+          q[d] = static_cast<f16>(x1);
+          q[d + 64] = static_cast<f16>(x2);
         } else if (rot) {
-          bf16 *k = o.k + ((long)(slot - n_heads) * o.kv_npos + row) * 128;
-          k[d] = static_cast<bf16>(x1);
-          k[d + 64] = static_cast<bf16>(x2);
+          f16 *k = o.k + ((long)(slot - n_heads) * o.kv_npos + row) * 128;
+          k[d] = static_cast<f16>(x1);
+          k[d + 64] = static_cast<f16>(x2);
         } else {
-          bf16 *vt = o.vt + (long)(slot - n_heads - n_kv) * 128 * o.kv_npos;
-          vt[(long)d * o.kv_npos + row] = static_cast<bf16>(x1);
-          vt[(long)(d + 64) * o.kv_npos + row] = static_cast<bf16>(x2);
+          f16 *vt = o.vt + (long)(slot - n_heads - n_kv) * 128 * o.kv_npos;
+          vt[(long)d * o.kv_npos + row] = static_cast<f16>(x1);
+          vt[(long)(d + 64) * o.kv_npos + row] = static_cast<f16>(x2);
         }
       }
     }
 }
 
-hipError_t gemm_qkv_rope(const bf16 *A, const bf16 *W, int rows, int K, int n_heads, int n_kv,
-                         const QKVOut<bf16> &out, hipStream_t s) {
+hipError_t gemm_qkv_rope(const f16 *A, const bf16 *W, int rows, int K, int n_heads, int n_kv,
+                         const QKVOut<f16> &out, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
   const int nslots = n_heads + 2 * n_kv;
@@ -297,7 +322,7 @@ hipError_t gemm_qkv_rope(const bf16 *A, const bf16 *W, int rows, int K, int n_he
 // vocabulary rows, and the target logit when the target falls in the tile.
 // The [tokens x vocab] logits never leave registers.
 template <class TL>
-__global__ __launch_bounds__(256) void k_gemm_lmhead(const bf16 *__restrict__ Hn,
+__global__ __launch_bounds__(256) void k_gemm_lmhead(const f16 *__restrict__ Hn,
                                                      const bf16 *__restrict__ Wlm, int T,
                                                      int vocab, int K,
                                                      const int32_t *__restrict__ lm_tgt,
@@ -307,7 +332,8 @@ __global__ __launch_bounds__(256) void k_gemm_lmhead(const bf16 *__restrict__ Hn
   __shared__ float red[TL::WM][TL::BN];
   const int n0 = blockIdx.x * TL::BN, m0 = blockIdx.y * TL::BM;
   f32x16 acc[TL::FM][TL::FN];
-  mainloop<TL>(Wlm, vocab, m0, Hn, [=](int r) { return min(n0 + r, T - 1); }, K, lds, acc);
+  mainloop<TL, true, false>(Wlm, vocab, m0, Hn, [=](int r) { return min(n0 + r, T - 1); }, K,
+                            lds, acc);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w / TL::WN, wn = w % TL::WN;
 
@@ -374,7 +400,7 @@ __global__ __launch_bounds__(256) void k_gemm_lmhead(const bf16 *__restrict__ Hn
 
 int lmhead_chunks(int vocab) { return (vocab + TileStd::BM - 1) / TileStd::BM; }
 
-hipError_t gemm_lmhead(const bf16 *A, const bf16 *W, int rows, int vocab, int K,
+hipError_t gemm_lmhead(const f16 *A, const bf16 *W, int rows, int vocab, int K,
                        const int32_t *lm_tgt, float2 *part, float *tgt_logit, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;

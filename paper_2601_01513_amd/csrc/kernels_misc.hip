@@ -112,9 +112,9 @@ hipError_t launch_embed_rows(const int32_t *ids, int rows, const T *embed, int d
 }
 
 // ------------------------------------------------------------------ RMSNorm
-template <typename T>
-__device__ __forceinline__ void norm_row(const float *src, const T *g, int d, float eps,
-                                         T *dst, float *red) {
+template <typename TW, typename TA>
+__device__ __forceinline__ void norm_row(const float *src, const TW *g, int d, float eps,
+                                         TA *dst, float *red) {
   float ss = 0.f;
   for (int c = threadIdx.x; c < d; c += 256) {
     const float v = src[c];
@@ -122,40 +122,40 @@ __device__ __forceinline__ void norm_row(const float *src, const T *g, int d, fl
   }
   ss = block_sum256(ss, red);
   const float r = rsqrtf(ss / (float)d + eps);
-  for (int c = threadIdx.x; c < d; c += 256) dst[c] = from_f32<T>(src[c] * r * to_f32(g[c]));
+  for (int c = threadIdx.x; c < d; c += 256) dst[c] = from_f32<TA>(src[c] * r * to_f32(g[c]));
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void k_rmsnorm(const float *x, const T *g, int d, float eps,
-                                                 T *y) {
+template <typename TW, typename TA>
+__global__ __launch_bounds__(256) void k_rmsnorm(const float *x, const TW *g, int d, float eps,
+                                                 TA *y) {
   __shared__ float red[4];
   const long r = blockIdx.x;
-  norm_row<T>(x + r * d, g, d, eps, y + r * d, red);
+  norm_row(x + r * d, g, d, eps, y + r * d, red);
 }
 
-template <typename T>
-hipError_t launch_rmsnorm(const float *x, const T *g, int rows, int d, float eps, T *y,
+template <typename TW, typename TA>
+hipError_t launch_rmsnorm(const float *x, const TW *g, int rows, int d, float eps, TA *y,
                           hipStream_t s) {
   if (rows == 0) return hipSuccess;
-  k_rmsnorm<T><<<rows, 256, 0, s>>>(x, g, d, eps, y);
+  k_rmsnorm<TW, TA><<<rows, 256, 0, s>>>(x, g, d, eps, y);
   return hipGetLastError();
 }
 
-template <typename T>
+template <typename TW, typename TA>
 __global__ __launch_bounds__(256) void k_lm_inputs(const float *x, const float *h_last,
-                                                   const int32_t *row_lo, const T *g, int d,
-                                                   float eps, T *y) {
+                                                   const int32_t *row_lo, const TW *g, int d,
+                                                   float eps, TA *y) {
   __shared__ float red[4];
   const int t = blockIdx.x;
   const float *src = (row_lo[t] == t) ? h_last : x + (long)(t - 1) * d;
-  norm_row<T>(src, g, d, eps, y + (long)t * d, red);
+  norm_row(src, g, d, eps, y + (long)t * d, red);
 }
 
-template <typename T>
+template <typename TW, typename TA>
 hipError_t launch_lm_inputs(const float *x, const float *h_last, const int32_t *row_lo,
-                            const T *g, int T_rows, int d, float eps, T *y, hipStream_t s) {
+                            const TW *g, int T_rows, int d, float eps, TA *y, hipStream_t s) {
   if (T_rows == 0) return hipSuccess;
-  k_lm_inputs<T><<<T_rows, 256, 0, s>>>(x, h_last, row_lo, g, d, eps, y);
+  k_lm_inputs<TW, TA><<<T_rows, 256, 0, s>>>(x, h_last, row_lo, g, d, eps, y);
   return hipGetLastError();
 }
 
@@ -230,13 +230,17 @@ hipError_t launch_reduce_select(const Branches &br, const float *logprobs, float
   template hipError_t launch_embed_prefix<T>(const T *, int, const int32_t *, int, const T *, \
                                              int, int, float *, hipStream_t);               \
   template hipError_t launch_embed_rows<T>(const int32_t *, int, const T *, int, float *,     \
-                                           hipStream_t);                                    \
-  template hipError_t launch_rmsnorm<T>(const float *, const T *, int, int, float, T *,      \
-                                        hipStream_t);                                       \
-  template hipError_t launch_lm_inputs<T>(const float *, const float *, const int32_t *,     \
-                                          const T *, int, int, float, T *, hipStream_t);
+                                           hipStream_t);
 VSR_INST(float)
 VSR_INST(bf16)
 #undef VSR_INST
+#define VSR_INST2(TW, TA)                                                                     \
+  template hipError_t launch_rmsnorm<TW, TA>(const float *, const TW *, int, int, float,      \
+                                             TA *, hipStream_t);                              \
+  template hipError_t launch_lm_inputs<TW, TA>(const float *, const float *, const int32_t *, \
+                                               const TW *, int, int, float, TA *, hipStream_t);
+VSR_INST2(float, float)
+VSR_INST2(bf16, f16)
+#undef VSR_INST2
 
 }  // namespace vsr

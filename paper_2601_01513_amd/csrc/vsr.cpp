@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "common.h"
@@ -131,6 +132,36 @@ struct vsr_ctx {
   std::vector<const void *> attn_norm, wqkv, wo, ffn_norm, wgu, wdown;
   std::string err;
 
+  // Stage timing (vsr_profile_*): event pairs recorded around each launch.
+  struct Rec {
+    int stage;
+    hipEvent_t a, b;
+  };
+  bool prof = false;
+  int phase = 0;  // 0 prefix pass, 1 candidate pass
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
+  hipEvent_t event() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    return hipEventCreate(&e) == hipSuccess ? e : nullptr;
+  }
+  void drop_records() {
+    for (auto &r : recs) {
+      pool.push_back(r.a);
+      pool.push_back(r.b);
+    }
+    recs.clear();
+  }
+  ~vsr_ctx() {
+    drop_records();
+    for (hipEvent_t e : pool) (void)hipEventDestroy(e);
+  }
+
   template <typename T>
   T *at(size_t off) const {
     return reinterpret_cast<T *>(ws + off);
@@ -151,6 +182,30 @@ struct vsr_ctx {
     hipError_t e_ = (expr);                                                               \
     if (e_ != hipSuccess)                                                                 \
       return (ctx)->fail(VSR_EHIP, "HIP error in %s: %s", stage, hipGetErrorString(e_)); \
+  } while (0)
+
+enum StageKind {
+  K_EMBED = 0, K_NORM, K_QKV, K_ATTN, K_MERGE, K_OPROJ, K_GATEUP, K_DOWN, K_LMIN, K_LMHEAD,
+  K_LSE, K_SELECT, K_ROWS, K_COPY
+};
+static_assert(K_COPY + 1 == VSR_STAGE_KINDS, "stage kinds");
+
+// Launch the expression as stage `kind`; with timing on, bracket it with events.
+#define STAGE(ctx, kind, name, ...)                                                     \
+  do {                                                                                  \
+    hipEvent_t a_ = nullptr;                                                            \
+    if ((ctx)->prof) {                                                                  \
+      a_ = (ctx)->event();                                                              \
+      if (!a_) return (ctx)->fail(VSR_EHIP, "hipEventCreate failed");                   \
+      HIPCHECK(ctx, "profile event", hipEventRecord(a_, (ctx)->stream));                \
+    }                                                                                   \
+    HIPCHECK(ctx, name, (__VA_ARGS__));                                                 \
+    if ((ctx)->prof) {                                                                  \
+      hipEvent_t b_ = (ctx)->event();                                                   \
+      if (!b_) return (ctx)->fail(VSR_EHIP, "hipEventCreate failed");                   \
+      HIPCHECK(ctx, "profile event", hipEventRecord(b_, (ctx)->stream));                \
+      (ctx)->recs.push_back({(ctx)->phase * VSR_STAGE_KINDS + (kind), a_, b_});         \
+    }                                                                                   \
   } while (0)
 
 extern "C" size_t vsr_workspace_size(const vsr_config *cfg) {
@@ -232,27 +287,29 @@ namespace {
 
 // One decoder block over `rows` rows whose residual stream is x. `mode` 0 is
 // the prefix (causal, caches of layer l), 1 the candidates (cascade).
-template <typename T>
+// TW is the weight type, TA the activation type (bf16 / fp16 on the MFMA
+// path, float / float on the plain path).
+template <typename TW, typename TA>
 int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
+  constexpr bool kMfma = std::is_same<TA, f16>::value;
   const vsr_config &cf = c->cfg;
   const Plan &p = c->plan;
   const int d = cf.d_model, Hq = cf.n_heads, Hkv = cf.n_kv_heads, hd = cf.head_dim, F = cf.d_ff;
-  const bool mfma = cf.dtype == VSR_BF16;
   float *x = c->at<float>(p.x);
-  T *xn = c->at<T>(p.xn), *q = c->at<T>(p.q), *attn = c->at<T>(p.attn), *h = c->at<T>(p.h);
+  TA *xn = c->at<TA>(p.xn), *q = c->at<TA>(p.q), *attn = c->at<TA>(p.attn), *h = c->at<TA>(p.h);
   const size_t layer_cache = (size_t)Hkv * p.kv_npos * hd;
   hipStream_t s = c->stream;
   for (int l = 0; l < cf.n_layers; ++l) {
-    const T *wqkv = static_cast<const T *>(c->wqkv[l]);
-    const T *wo = static_cast<const T *>(c->wo[l]);
-    const T *wgu = static_cast<const T *>(c->wgu[l]);
-    const T *wdown = static_cast<const T *>(c->wdown[l]);
-    T *kc = c->at<T>(p.kc) + l * layer_cache;
-    T *vtc = c->at<T>(p.vtc) + l * layer_cache;
-    HIPCHECK(c, "attention norm",
-             launch_rmsnorm<T>(x, static_cast<const T *>(c->attn_norm[l]), rows, d, cf.rms_eps,
-                               xn, s));
-    QKVOut<T> qo;
+    const TW *wqkv = static_cast<const TW *>(c->wqkv[l]);
+    const TW *wo = static_cast<const TW *>(c->wo[l]);
+    const TW *wgu = static_cast<const TW *>(c->wgu[l]);
+    const TW *wdown = static_cast<const TW *>(c->wdown[l]);
+    TA *kc = c->at<TA>(p.kc) + l * layer_cache;
+    TA *vtc = c->at<TA>(p.vtc) + l * layer_cache;
+    STAGE(c, K_NORM, "attention norm",
+             launch_rmsnorm<TW, TA>(x, static_cast<const TW *>(c->attn_norm[l]), rows, d,
+                                    cf.rms_eps, xn, s));
+    QKVOut<TA> qo;
     qo.q = q;
     qo.rope = c->at<float2>(p.rope);
     if (mode == 0) {
@@ -261,24 +318,25 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       qo.kv_npos = p.kv_npos;
       qo.row_pos = nullptr;
     } else {
-      qo.k = c->at<T>(p.bk);
-      qo.vt = c->at<T>(p.bvt);
+      qo.k = c->at<TA>(p.bk);
+      qo.vt = c->at<TA>(p.bvt);
       qo.kv_npos = p.bk_npos;
       qo.row_pos = c->at<int32_t>(p.row_pos);
     }
-    if constexpr (sizeof(T) == 2) {
-      HIPCHECK(c, "qkv projection", gemm_qkv_rope(xn, wqkv, rows, d, Hq, Hkv, qo, s));
+    if constexpr (kMfma) {
+      STAGE(c, K_QKV, "qkv projection", gemm_qkv_rope(xn, wqkv, rows, d, Hq, Hkv, qo, s));
     } else {
-      HIPCHECK(c, "qkv projection", simple_qkv_rope<T>(xn, wqkv, rows, d, Hq, Hkv, hd, qo, s));
+      STAGE(c, K_QKV, "qkv projection",
+            simple_qkv_rope<TA>(xn, wqkv, rows, d, Hq, Hkv, hd, qo, s));
     }
-    if (mfma) {
+    if constexpr (kMfma) {
       AttnArgs a{};
-      a.q = reinterpret_cast<const bf16 *>(q);
-      a.k = reinterpret_cast<const bf16 *>(kc);
-      a.vt = reinterpret_cast<const bf16 *>(vtc);
+      a.q = q;
+      a.k = kc;
+      a.vt = vtc;
       a.kv_npos = p.kv_npos;
-      a.bk = c->at<bf16>(p.bk);
-      a.bvt = c->at<bf16>(p.bvt);
+      a.bk = c->at<f16>(p.bk);
+      a.bvt = c->at<f16>(p.bvt);
       a.bk_npos = p.bk_npos;
       a.row_lo = c->at<int32_t>(p.row_lo);
       a.T = rows;
@@ -287,14 +345,14 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       a.n_kv = Hkv;
       a.nchunks = split.nchunks;
       a.chunk = split.chunk;
-      a.out = reinterpret_cast<bf16 *>(attn);
+      a.out = attn;
       a.part_acc = c->at<float>(p.part_acc);
       a.part_ml = c->at<float2>(p.part_ml);
       if (mode == 0) {
-        HIPCHECK(c, "prefill attention", attn_prefill(a, s));
+        STAGE(c, K_ATTN, "prefill attention", attn_prefill(a, s));
       } else {
-        HIPCHECK(c, "cascade attention", attn_cascade(a, s));
-        HIPCHECK(c, "cascade merge", attn_merge(a, s));
+        STAGE(c, K_ATTN, "cascade attention", attn_cascade(a, s));
+        STAGE(c, K_MERGE, "cascade merge", attn_merge(a, s));
       }
     } else {
       SimpleAttnArgs a{};
@@ -302,8 +360,8 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       a.k = kc;
       a.vt = vtc;
       a.kv_npos = p.kv_npos;
-      a.bk = c->at<T>(p.bk);
-      a.bvt = c->at<T>(p.bvt);
+      a.bk = c->at<TA>(p.bk);
+      a.bvt = c->at<TA>(p.bvt);
       a.bk_npos = p.bk_npos;
       a.row_lo = c->at<int32_t>(p.row_lo);
       a.T = rows;
@@ -313,49 +371,51 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       a.hd = hd;
       a.mode = mode;
       a.out = attn;
-      HIPCHECK(c, "attention", simple_attn<T>(a, s));
+      STAGE(c, K_ATTN, "attention", simple_attn<TA>(a, s));
     }
-    if constexpr (sizeof(T) == 2) {
-      HIPCHECK(c, "output projection", gemm_residual(attn, wo, rows, d, Hq * hd, x, s));
+    if constexpr (kMfma) {
+      STAGE(c, K_OPROJ, "output projection", gemm_residual(attn, wo, rows, d, Hq * hd, x, s));
     } else {
-      HIPCHECK(c, "output projection", simple_residual<T>(attn, wo, rows, d, Hq * hd, x, s));
+      STAGE(c, K_OPROJ, "output projection",
+            simple_residual<TA>(attn, wo, rows, d, Hq * hd, x, s));
     }
-    HIPCHECK(c, "ffn norm",
-             launch_rmsnorm<T>(x, static_cast<const T *>(c->ffn_norm[l]), rows, d, cf.rms_eps,
-                               xn, s));
-    if constexpr (sizeof(T) == 2) {
-      HIPCHECK(c, "gate/up projection", gemm_swiglu(xn, wgu, rows, F, d, h, s));
-      HIPCHECK(c, "down projection", gemm_residual(h, wdown, rows, d, F, x, s));
+    STAGE(c, K_NORM, "ffn norm",
+             launch_rmsnorm<TW, TA>(x, static_cast<const TW *>(c->ffn_norm[l]), rows, d,
+                                    cf.rms_eps, xn, s));
+    if constexpr (kMfma) {
+      STAGE(c, K_GATEUP, "gate/up projection", gemm_swiglu(xn, wgu, rows, F, d, h, s));
+      STAGE(c, K_DOWN, "down projection", gemm_residual(h, wdown, rows, d, F, x, s));
     } else {
-      HIPCHECK(c, "gate/up projection", simple_swiglu<T>(xn, wgu, rows, F, d, h, s));
-      HIPCHECK(c, "down projection", simple_residual<T>(h, wdown, rows, d, F, x, s));
+      STAGE(c, K_GATEUP, "gate/up projection", simple_swiglu<TA>(xn, wgu, rows, F, d, h, s));
+      STAGE(c, K_DOWN, "down projection", simple_residual<TA>(h, wdown, rows, d, F, x, s));
     }
   }
   return VSR_OK;
 }
 
-template <typename T>
+template <typename TW, typename TA>
 int prefill_impl(vsr_ctx *c, const void *visual, int nv, const int32_t *ids, int nt) {
   const vsr_config &cf = c->cfg;
   const Plan &p = c->plan;
   const int P = nv + nt;
   float *x = c->at<float>(p.x);
-  HIPCHECK(c, "prefix embedding",
-           launch_embed_prefix<T>(static_cast<const T *>(visual), nv, ids, nt,
-                                  static_cast<const T *>(c->embed), cf.vocab, cf.d_model, x,
-                                  c->stream));
+  STAGE(c, K_EMBED, "prefix embedding",
+           launch_embed_prefix<TW>(static_cast<const TW *>(visual), nv, ids, nt,
+                                   static_cast<const TW *>(c->embed), cf.vocab, cf.d_model, x,
+                                   c->stream));
   c->P = P;
-  const int rc = run_layers<T>(c, P, 0, Split{1, 0});
+  const int rc = run_layers<TW, TA>(c, P, 0, Split{1, 0});
   if (rc) return rc;
-  HIPCHECK(c, "last prefix row",
+  STAGE(c, K_COPY, "last prefix row",
            hipMemcpyAsync(c->at<float>(p.h_last), x + (size_t)(P - 1) * cf.d_model,
                           (size_t)cf.d_model * 4, hipMemcpyDeviceToDevice, c->stream));
   return VSR_OK;
 }
 
-template <typename T>
+template <typename TW, typename TA>
 int score_impl(vsr_ctx *c, const Branches &br, const int32_t *cand_ids, float *logprobs,
                float *scores, int32_t *argmax) {
+  constexpr bool kMfma = std::is_same<TA, f16>::value;
   const vsr_config &cf = c->cfg;
   const Plan &p = c->plan;
   const int T_rows = br.cu[br.M];
@@ -366,35 +426,34 @@ int score_impl(vsr_ctx *c, const Branches &br, const int32_t *cand_ids, float *l
   float *tgt = c->at<float>(p.tgt);
   int lm_chunks = 1;
   if (T_rows > 0) {
-    HIPCHECK(c, "row tables",
+    STAGE(c, K_ROWS, "row tables",
              launch_row_tables(br, c->P, cand_ids, cf.vocab, row_lo, row_pos, lm_tgt, s));
     float *x = c->at<float>(p.x);
-    HIPCHECK(c, "candidate embedding",
-             launch_embed_rows<T>(lm_tgt, T_rows, static_cast<const T *>(c->embed), cf.d_model,
-                                  x, s));
-    const Split split = cf.dtype == VSR_BF16
-                            ? cascade_split(T_rows, c->P, cf.n_heads, cf.n_kv_heads)
-                            : Split{1, 0};
-    const int rc = run_layers<T>(c, T_rows, 1, split);
+    STAGE(c, K_EMBED, "candidate embedding",
+             launch_embed_rows<TW>(lm_tgt, T_rows, static_cast<const TW *>(c->embed),
+                                   cf.d_model, x, s));
+    const Split split =
+        kMfma ? cascade_split(T_rows, c->P, cf.n_heads, cf.n_kv_heads) : Split{1, 0};
+    const int rc = run_layers<TW, TA>(c, T_rows, 1, split);
     if (rc) return rc;
-    T *lm_in = c->at<T>(p.xn);
-    HIPCHECK(c, "lm inputs",
-             launch_lm_inputs<T>(x, c->at<float>(p.h_last), row_lo,
-                                 static_cast<const T *>(c->final_norm), T_rows, cf.d_model,
-                                 cf.rms_eps, lm_in, s));
-    if constexpr (sizeof(T) == 2) {
+    TA *lm_in = c->at<TA>(p.xn);
+    STAGE(c, K_LMIN, "lm inputs",
+          launch_lm_inputs<TW, TA>(x, c->at<float>(p.h_last), row_lo,
+                                   static_cast<const TW *>(c->final_norm), T_rows, cf.d_model,
+                                   cf.rms_eps, lm_in, s));
+    if constexpr (kMfma) {
       lm_chunks = lmhead_chunks(cf.vocab);
-      HIPCHECK(c, "lm head",
-               gemm_lmhead(lm_in, static_cast<const bf16 *>(c->lm_head), T_rows, cf.vocab,
-                           cf.d_model, lm_tgt, lm_part, tgt, s));
+      STAGE(c, K_LMHEAD, "lm head",
+            gemm_lmhead(lm_in, static_cast<const bf16 *>(c->lm_head), T_rows, cf.vocab,
+                        cf.d_model, lm_tgt, lm_part, tgt, s));
     } else {
-      HIPCHECK(c, "lm head",
-               simple_lmhead<T>(lm_in, static_cast<const T *>(c->lm_head), T_rows, cf.vocab,
-                                cf.d_model, lm_tgt, lm_part, tgt, s));
+      STAGE(c, K_LMHEAD, "lm head",
+            simple_lmhead<TA>(lm_in, static_cast<const TW *>(c->lm_head), T_rows, cf.vocab,
+                              cf.d_model, lm_tgt, lm_part, tgt, s));
     }
   }
-  HIPCHECK(c, "lse gather", launch_lse_gather(br, lm_part, lm_chunks, tgt, logprobs, s));
-  HIPCHECK(c, "reduce/select", launch_reduce_select(br, logprobs, scores, argmax, s));
+  STAGE(c, K_LSE, "lse gather", launch_lse_gather(br, lm_part, lm_chunks, tgt, logprobs, s));
+  STAGE(c, K_SELECT, "reduce/select", launch_reduce_select(br, logprobs, scores, argmax, s));
   return VSR_OK;
 }
 
@@ -422,8 +481,10 @@ extern "C" int vsr_prefill(vsr_ctx *ctx, const void *visual, int32_t n_visual,
   int rc = set_device(ctx);
   if (rc) return rc;
   ctx->prefilled = false;
-  rc = ctx->cfg.dtype == VSR_BF16 ? prefill_impl<bf16>(ctx, visual, n_visual, ids, n_text)
-                                  : prefill_impl<float>(ctx, visual, n_visual, ids, n_text);
+  ctx->phase = 0;
+  rc = ctx->cfg.dtype == VSR_BF16
+           ? prefill_impl<bf16, f16>(ctx, visual, n_visual, ids, n_text)
+           : prefill_impl<float, float>(ctx, visual, n_visual, ids, n_text);
   if (rc == VSR_OK) ctx->prefilled = true;
   return rc;
 }
@@ -452,9 +513,10 @@ extern "C" int vsr_score(vsr_ctx *ctx, const int32_t *cand_ids, const int32_t *c
   }
   const int rc = set_device(ctx);
   if (rc) return rc;
+  ctx->phase = 1;
   return ctx->cfg.dtype == VSR_BF16
-             ? score_impl<bf16>(ctx, br, cand_ids, logprobs, scores, argmax)
-             : score_impl<float>(ctx, br, cand_ids, logprobs, scores, argmax);
+             ? score_impl<bf16, f16>(ctx, br, cand_ids, logprobs, scores, argmax)
+             : score_impl<float, float>(ctx, br, cand_ids, logprobs, scores, argmax);
 }
 
 extern "C" const char *vsr_last_error(const vsr_ctx *ctx) {
@@ -462,3 +524,29 @@ extern "C" const char *vsr_last_error(const vsr_ctx *ctx) {
 }
 
 extern "C" void vsr_destroy(vsr_ctx *ctx) { delete ctx; }
+
+extern "C" int vsr_profile_enable(vsr_ctx *ctx, int enable) {
+  if (!ctx) return VSR_EINVAL;
+  if (!ctx->recs.empty()) HIPCHECK(ctx, "profile sync", hipStreamSynchronize(ctx->stream));
+  ctx->drop_records();
+  ctx->prof = enable != 0;
+  return VSR_OK;
+}
+
+extern "C" int vsr_profile_read(vsr_ctx *ctx, double *ms, int32_t *launches) {
+  if (!ctx) return VSR_EINVAL;
+  if (!ms || !launches) return ctx->fail(VSR_EINVAL, "profile_read: NULL output");
+  for (int i = 0; i < VSR_STAGES; ++i) {
+    ms[i] = 0.0;
+    launches[i] = 0;
+  }
+  if (!ctx->recs.empty()) HIPCHECK(ctx, "profile sync", hipStreamSynchronize(ctx->stream));
+  for (const auto &r : ctx->recs) {
+    float t = 0.f;
+    HIPCHECK(ctx, "hipEventElapsedTime", hipEventElapsedTime(&t, r.a, r.b));
+    ms[r.stage] += t;
+    launches[r.stage] += 1;
+  }
+  ctx->drop_records();
+  return VSR_OK;
+}

@@ -54,7 +54,14 @@ def run_oracle(wl, dtype=np.float64, cand_ids=None, cand_len=None):
     vis = W.to_host_f32(wl.visual)
     cids = wl.cand_ids if cand_ids is None else cand_ids
     lens = wl.cand_len if cand_len is None else cand_len
-    return oracle.score_shared_prefix(wl.cfg, hw, vis, wl.prefix_ids, cids, lens, dtype=dtype)
+    t0 = time.time()
+    every = max(1, wl.cfg.n_layers // 7)
+
+    def progress(layer):
+        if (layer + 1) % every == 0:
+            _say(f"  oracle layer {layer + 1}/{wl.cfg.n_layers} at {time.time() - t0:.0f}s")
+    return oracle.score_shared_prefix(wl.cfg, hw, vis, wl.prefix_ids, cids, lens, dtype=dtype,
+                                      progress=progress)
 
 
 def check(cfg, gpu, ora, lens):
