@@ -100,14 +100,17 @@ struct QKVOut {
 // ------------------------------------------------------------ MFMA path
 // C = A[rows][K] . W[N][K]^T with fused epilogues; A fp16 activations, W bf16
 // weights (converted to fp16 on their way into LDS), fp32 accumulation.
+// Shapes with few output tiles split K; `part` is fp32 scratch of
+// gemm_split_floats(rows, N, K) floats (N = B rows) for the partials.
+size_t gemm_split_floats(int rows, int N, int K);
 hipError_t gemm_qkv_rope(const f16 *A, const bf16 *W, int rows, int K, int n_heads,
-                         int n_kv, const QKVOut<f16> &out, hipStream_t s);
+                         int n_kv, const QKVOut<f16> &out, float *part, hipStream_t s);
 // x[rows][N] += A . W^T (residual stream, fp32).
 hipError_t gemm_residual(const f16 *A, const bf16 *W, int rows, int N, int K, float *x,
-                         hipStream_t s);
+                         float *part, hipStream_t s);
 // h[rows][F] = silu(A . Wg^T) * (A . Wu^T), W = [Wg; Wu] ([2F][K]).
 hipError_t gemm_swiglu(const f16 *A, const bf16 *W, int rows, int F, int K, f16 *h,
-                       hipStream_t s);
+                       float *part, hipStream_t s);
 // LM head: per (vocab chunk c, row t): part[c][t] = (max, sum exp(l - max)) over
 // the chunk's logits l = W[v] . A[t]; tgt_logit[t] = logit of lm_tgt[t].
 int lmhead_chunks(int vocab);

@@ -1,41 +1,61 @@
-// bf16 MFMA GEMMs of the verifier scoring pass with fused epilogues.
+// MFMA GEMMs of the verifier scoring pass with fused epilogues.
 //
 // Every GEMM here is C = A . B^T with A [rows][K] and B [N][K] both
 // K-contiguous (activations and nn.Linear weights), fp32 accumulation on the
-// gfx950 v_mfma_f32_32x32x16_f16 matrix cores. Activations are fp16; the bf16
+// gfx950 v_mfma_f32_32x32x16_f16 matrix cores. Activations are fp16; a bf16
 // weight operand is converted to fp16 in registers on its way into LDS (exact:
-// a bf16 value's 8 significant bits fit fp16's 11). A 256-thread block owns a
-// BM x BN tile; its four waves form a WM x WN grid and each wave owns a
-// (BM/WM) x (BN/WN) sub-tile of 32x32 MFMA blocks. K advances in steps of 64:
-// the next A/B panels are fetched into registers while the MFMAs consume the
-// current panels from LDS (16-byte chunks, XOR-swizzled by row so that both
-// the panel stores and the fragment loads are free of bank conflicts).
+// a bf16 value's 8 significant bits fit fp16's 11).
 //
-// MFMA 32x32x16 (f16 and bf16 alike) lane layout (lane l, element e, accumulator register r):
+// Block: 512 threads = 8 waves (two per SIMD) on a 256 x 256 tile; the waves
+// form a 4 x 2 grid, each owning 64 x 128 outputs (2 x 4 MFMA 32x32 blocks).
+// K advances in panels of 64 through a two-stage LDS ring (2 x 64 KB): while
+// the MFMAs consume panel k, panel k+1 is in flight -- fp16 operands straight
+// from global memory into LDS (global_load_lds, no registers), bf16 operands
+// through registers and the converter. One barrier per panel. LDS rows are
+// 16-byte chunks XOR-swizzled by row, so panel stores and fragment loads are
+// free of bank conflicts; for the direct loads the swizzle is applied to the
+// global addresses (a direct load writes lane l's 16 bytes at base + 16 l).
+//
+// Blocks are numbered so that the ones resident on one XCD at the same time
+// share A and B panels in that XCD's L2 (the hardware deals block b to XCD
+// b % 8). Optional split-K: blocks of one tile take disjoint K ranges and
+// write fp32 partials that a reduction kernel sums in a fixed order.
+//
+// MFMA 32x32x16 lane layout (lane l, element e, accumulator register r):
 //   A operand: A[i = l % 32][k = 8 (l / 32) + e]
 //   B operand: B[k = 8 (l / 32) + e][j = l % 32]
 //   result   : C[i = 8 (r / 4) + 4 (l / 32) + r % 4][j = l % 32]
 // so each lane holds one output column and sixteen output rows; epilogues
 // work directly on the registers.
+#include <algorithm>
+
 #include "common.h"
 
 namespace vsr {
 
-constexpr int BK = 64;  // K elements per panel (8 chunks of 16 bytes per row)
+namespace {
+
+constexpr int BK = 64;        // K elements per panel (8 chunks of 16 bytes per row)
+constexpr int NT = 512;       // threads per block
+constexpr int NWAVES = NT / 64;
 
 template <int BM_, int BN_, int WM_, int WN_>
 struct Tile {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
   static constexpr int TM = BM / WM, TN = BN / WN;  // wave sub-tile
   static constexpr int FM = TM / 32, FN = TN / 32;  // MFMA blocks per wave
-  static constexpr int A_LOADS = BM * 8 / 256, B_LOADS = BN * 8 / 256;
-  static constexpr int LDS_CHUNKS = (BM + BN) * 8;
-  static_assert(WM * WN == 4, "four waves");
+  static constexpr int STAGE = (BM + BN) * 8;       // 16-byte chunks per LDS stage
+  static_assert(WM * WN == NWAVES, "eight waves");
   static_assert(TM % 32 == 0 && TN % 32 == 0, "32x32 MFMA blocks");
+  static_assert(BM % 64 == 0 && BN % 64 == 0, "operand loads cover 64-row groups");
 };
 
-__device__ __forceinline__ int swz(int row, int c) { return row * 8 + (c ^ (row & 7)); }
+// 256 x 256 tile, waves 4 x 2 of 64 x 128: a wave's 128 columns hold a whole
+// attention head (QKV) or 64 gate + 64 up columns (SwiGLU), so the rotary
+// pairs and the gate/up pairs sit in the same lane and register.
+typedef Tile<256, 256, 4, 2> TileStd;
 
+__device__ __forceinline__ int swz(int row, int c) { return row * 8 + (c ^ (row & 7)); }
 __device__ __forceinline__ f16x8 as_f16x8(u32x4 v) { return __builtin_bit_cast(f16x8, v); }
 
 // Eight bf16 values -> eight fp16 values (exact for |v| in [2^-17, 65504];
@@ -50,10 +70,123 @@ __device__ __forceinline__ u32x4 bf16x8_to_f16x8(u32x4 v) {
   }
   return r;
 }
-template <bool CVT>
-__device__ __forceinline__ u32x4 stage(u32x4 v) {
-  if constexpr (CVT) return bf16x8_to_f16x8(v);
-  return v;
+
+// One operand (ROWS rows of a panel). CVT: stored as bf16, staged through
+// registers and converted; otherwise fp16, loaded straight into LDS.
+template <int ROWS, bool CVT>
+struct Operand {
+  static constexpr int PER_THREAD = ROWS * 8 / NT;  // 16-byte chunks per thread
+  const uint16_t *g[PER_THREAD];                     // row base + chunk, K-tile 0
+  int slot[PER_THREAD];                              // LDS chunk (register path)
+  u32x4 r[CVT ? PER_THREAD : 1];
+
+  template <class RowFn>
+  __device__ __forceinline__ void init(const void *base, int K, RowFn row_of) {
+    const uint16_t *p = static_cast<const uint16_t *>(base);
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < PER_THREAD; ++i) {
+      int row, c;
+      if constexpr (CVT) {
+        const int id = i * NT + t;
+        row = id >> 3;
+        c = id & 7;
+        slot[i] = swz(row, c);
+      } else {
+        // Direct load i of wave w fills LDS rows 8 (i * NWAVES + w) .. +7;
+        // lane l lands in physical chunk l % 8 of row l / 8.
+        const int w = t >> 6, l = t & 63;
+        row = (i * NWAVES + w) * 8 + (l >> 3);
+        c = (l & 7) ^ (row & 7);
+        slot[i] = 0;
+      }
+      g[i] = p + (long)row_of(row) * K + c * 8;
+    }
+  }
+  // Starts loading K-panel kt into LDS stage `dst` (direct) or registers.
+  __device__ __forceinline__ void issue(int kt, u32x4 *dst) {
+#pragma unroll
+    for (int i = 0; i < PER_THREAD; ++i) {
+      if constexpr (CVT) {
+        r[i] = *reinterpret_cast<const u32x4 *>(g[i] + kt * BK);
+      } else {
+        const int w = threadIdx.x >> 6;
+        __builtin_amdgcn_global_load_lds(g[i] + kt * BK, dst + (i * NWAVES + w) * 64, 16, 0, 0);
+      }
+    }
+  }
+  // Register path: convert and store the panel into LDS stage `dst`.
+  __device__ __forceinline__ void commit(u32x4 *dst) {
+    if constexpr (CVT) {
+#pragma unroll
+      for (int i = 0; i < PER_THREAD; ++i) dst[slot[i]] = bf16x8_to_f16x8(r[i]);
+    }
+  }
+};
+
+// acc += A[rows arow(0..BM)] . B[rows brow(0..BN)]^T over K-panels [kt0, kt1).
+// The row functions must return in-range rows (results of clamped rows are
+// never stored). CVT_A / CVT_B mark an operand stored as bf16.
+template <class TL, bool CVT_A, bool CVT_B, class ARow, class BRow>
+__device__ __forceinline__ void mainloop(const void *A, ARow arow, const void *B, BRow brow,
+                                         int K, int kt0, int kt1, u32x4 *lds,
+                                         f32x16 (&acc)[TL::FM][TL::FN]) {
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int wm = w / TL::WN, wn = w % TL::WN;
+  Operand<TL::BM, CVT_A> oa;
+  Operand<TL::BN, CVT_B> ob;
+  oa.init(A, K, arow);
+  ob.init(B, K, brow);
+#pragma unroll
+  for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < TL::FN; ++fn) acc[fm][fn] = f32x16{};
+  if (kt1 <= kt0) return;
+
+  int fa[TL::FM], fb[TL::FN];
+#pragma unroll
+  for (int fm = 0; fm < TL::FM; ++fm) fa[fm] = wm * TL::TM + fm * 32 + (lane & 31);
+#pragma unroll
+  for (int fn = 0; fn < TL::FN; ++fn) fb[fn] = TL::BM + wn * TL::TN + fn * 32 + (lane & 31);
+  const int hc = lane >> 5;
+
+  oa.issue(kt0, lds);
+  ob.issue(kt0, lds + TL::BM * 8);
+  oa.commit(lds);
+  ob.commit(lds + TL::BM * 8);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  for (int kt = kt0; kt < kt1; ++kt) {
+    u32x4 *cur = lds + ((kt - kt0) & 1) * TL::STAGE;
+    u32x4 *nxt = lds + (((kt - kt0) & 1) ^ 1) * TL::STAGE;
+    const bool more = kt + 1 < kt1;
+    if (more) {
+      oa.issue(kt + 1, nxt);
+      ob.issue(kt + 1, nxt + TL::BM * 8);
+    }
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int c = ks * 2 + hc;
+      f16x8 af[TL::FM], bfr[TL::FN];
+#pragma unroll
+      for (int fm = 0; fm < TL::FM; ++fm) af[fm] = as_f16x8(cur[swz(fa[fm], c)]);
+#pragma unroll
+      for (int fn = 0; fn < TL::FN; ++fn) bfr[fn] = as_f16x8(cur[swz(fb[fn], c)]);
+#pragma unroll
+      for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < TL::FN; ++fn)
+          acc[fm][fn] =
+              __builtin_amdgcn_mfma_f32_32x32x16_f16(af[fm], bfr[fn], acc[fm][fn], 0, 0, 0);
+    }
+    if (more) {
+      oa.commit(nxt);
+      ob.commit(nxt + TL::BM * 8);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  }
 }
 
 // Output row / column (within the block tile) of accumulator register r of
@@ -67,115 +200,90 @@ __device__ __forceinline__ int acc_col(int wn, int fn, int lane) {
   return wn * TL::TN + fn * 32 + (lane & 31);
 }
 
-// Main loop: acc += A[m0 .. m0+BM) . B[rows given by brow(lr)]^T over all of K.
-// A rows past `rows` are clamped to the last row (their results are never
-// stored); brow must return an in-range B row for every lr < BN. CVT_A / CVT_B
-// mark an operand stored as bf16 in memory (converted to fp16 when staged).
-template <class TL, bool CVT_A, bool CVT_B, class BRow>
-__device__ __forceinline__ void mainloop(const void *__restrict__ Av, int rows, int m0,
-                                         const void *__restrict__ Bv, BRow brow, int K,
-                                         u32x4 *lds, f32x16 (&acc)[TL::FM][TL::FN]) {
-  const uint16_t *A = static_cast<const uint16_t *>(Av);
-  const uint16_t *B = static_cast<const uint16_t *>(Bv);
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+// Block -> (m tile, n tile, split). The hardware deals block b to XCD b % 8;
+// each XCD is given a contiguous range of logical work items, and logical
+// items run GM m-tiles fastest, then n-tiles, then splits, so the blocks an
+// XCD runs together share operand panels in its L2.
+struct Work {
+  int tm, tn, split;
+};
+__device__ __forceinline__ Work block_work(int nm, int nn, int nsplit, int gm) {
+  const int nb = nm * nn * nsplit;
+  const int b = blockIdx.x;
+  const int q = nb / 8, rem = nb % 8, x = b % 8, k = b / 8;
+  const int L = (x < rem ? x * (q + 1) : rem * (q + 1) + (x - rem) * q) + k;
+  const int per_split = nm * nn;
+  const int s = L / per_split, l2 = L % per_split;
+  const int g = min(gm, nm);
+  const int grp = l2 / (g * nn);
+  const int gsz = min(g, nm - grp * g);
+  const int in = l2 - grp * g * nn;
+  return {grp * g + in % gsz, in / gsz, s};
+}
+
+struct Launch {
+  int nm, nn, nsplit, gm;
+  unsigned blocks() const { return (unsigned)(nm * nn * nsplit); }
+};
+
+// K-panel range of split s of nsplit over nk panels.
+__device__ __forceinline__ void split_range(int nk, int nsplit, int s, int &k0, int &k1) {
+  k0 = (int)((long)nk * s / nsplit);
+  k1 = (int)((long)nk * (s + 1) / nsplit);
+}
+
+// Raw fp32 partial tile of split s: part[s][row][col] (rows x ncols).
+template <class TL>
+__device__ __forceinline__ void store_partial(const f32x16 (&acc)[TL::FM][TL::FN], float *part,
+                                              int s, int rows, int ncols, int m0, int n0) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w / TL::WN, wn = w % TL::WN;
-  u32x4 *As = lds;
-  u32x4 *Bs = lds + TL::BM * 8;
-
-  const u32x4 *ga[TL::A_LOADS];
-  int la[TL::A_LOADS];
+  float *p = part + (long)s * rows * ncols;
 #pragma unroll
-  for (int i = 0; i < TL::A_LOADS; ++i) {
-    const int id = i * 256 + t, r = id >> 3, c = id & 7;
-    const int gr = min(m0 + r, rows - 1);
-    ga[i] = reinterpret_cast<const u32x4 *>(A + (long)gr * K) + c;
-    la[i] = swz(r, c);
-  }
-  const u32x4 *gb[TL::B_LOADS];
-  int lb[TL::B_LOADS];
+  for (int fn = 0; fn < TL::FN; ++fn) {
+    const int col = n0 + acc_col<TL>(wn, fn, lane);
+    if (col >= ncols) continue;
 #pragma unroll
-  for (int i = 0; i < TL::B_LOADS; ++i) {
-    const int id = i * 256 + t, r = id >> 3, c = id & 7;
-    gb[i] = reinterpret_cast<const u32x4 *>(B + (long)brow(r) * K) + c;
-    lb[i] = swz(r, c);
-  }
-
+    for (int fm = 0; fm < TL::FM; ++fm)
 #pragma unroll
-  for (int fm = 0; fm < TL::FM; ++fm)
-#pragma unroll
-    for (int fn = 0; fn < TL::FN; ++fn) acc[fm][fn] = f32x16{};
-
-  u32x4 ra[TL::A_LOADS], rb[TL::B_LOADS];
-  const int nk = K / BK;
-#pragma unroll
-  for (int i = 0; i < TL::A_LOADS; ++i) ra[i] = ga[i][0];
-#pragma unroll
-  for (int i = 0; i < TL::B_LOADS; ++i) rb[i] = gb[i][0];
-#pragma unroll
-  for (int i = 0; i < TL::A_LOADS; ++i) As[la[i]] = stage<CVT_A>(ra[i]);
-#pragma unroll
-  for (int i = 0; i < TL::B_LOADS; ++i) Bs[lb[i]] = stage<CVT_B>(rb[i]);
-  __syncthreads();
-
-  // Fragment rows of this lane.
-  int fa[TL::FM], fb[TL::FN];
-#pragma unroll
-  for (int fm = 0; fm < TL::FM; ++fm) fa[fm] = wm * TL::TM + fm * 32 + (lane & 31);
-#pragma unroll
-  for (int fn = 0; fn < TL::FN; ++fn) fb[fn] = wn * TL::TN + fn * 32 + (lane & 31);
-  const int hc = lane >> 5;
-
-  for (int kt = 0; kt < nk; ++kt) {
-    const bool more = kt + 1 < nk;
-    if (more) {
-      const int off = (kt + 1) * (BK / 8);
-#pragma unroll
-      for (int i = 0; i < TL::A_LOADS; ++i) ra[i] = ga[i][off];
-#pragma unroll
-      for (int i = 0; i < TL::B_LOADS; ++i) rb[i] = gb[i][off];
-    }
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int c = ks * 2 + hc;
-      f16x8 af[TL::FM], bfr[TL::FN];
-#pragma unroll
-      for (int fm = 0; fm < TL::FM; ++fm) af[fm] = as_f16x8(As[swz(fa[fm], c)]);
-#pragma unroll
-      for (int fn = 0; fn < TL::FN; ++fn) bfr[fn] = as_f16x8(Bs[swz(fb[fn], c)]);
-#pragma unroll
-      for (int fm = 0; fm < TL::FM; ++fm)
-#pragma unroll
-        for (int fn = 0; fn < TL::FN; ++fn)
-          acc[fm][fn] =
-              __builtin_amdgcn_mfma_f32_32x32x16_f16(af[fm], bfr[fn], acc[fm][fn], 0, 0, 0);
-    }
-    __syncthreads();
-    if (more) {
-#pragma unroll
-      for (int i = 0; i < TL::A_LOADS; ++i) As[la[i]] = stage<CVT_A>(ra[i]);
-#pragma unroll
-      for (int i = 0; i < TL::B_LOADS; ++i) Bs[lb[i]] = stage<CVT_B>(rb[i]);
-      __syncthreads();
-    }
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + acc_row<TL>(wm, fm, r, lane);
+        if (row < rows) p[(long)row * ncols + col] = acc[fm][fn][r];
+      }
   }
 }
 
-// The tile used by every GEMM of the pass: 128 x 256, waves 2 x 2 (64 x 128).
-// A wave's 128 columns hold a whole attention head (QKV) or 64 gate + 64 up
-// columns (SwiGLU), so the rotary pairs and the gate/up pairs sit in the same
-// lane and register.
-typedef Tile<128, 256, 2, 2> TileStd;
+// Split count for a GEMM of `tiles` output tiles over nk K-panels: enough
+// blocks for one round on the 256 CUs, at least 4 panels per split.
+int choose_split(int tiles, int nk, int max_split) {
+  if (tiles >= 192) return 1;
+  int s = (256 + tiles - 1) / tiles;
+  s = std::min(s, std::max(1, nk / 4));
+  return std::max(1, std::min(s, max_split));
+}
+
+__device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.f + __expf(-g)) * u; }
 
 // ------------------------------------------------------- residual (O, down)
 template <class TL>
-__global__ __launch_bounds__(256) void k_gemm_residual(const f16 *__restrict__ A,
-                                                       const bf16 *__restrict__ W, int rows,
-                                                       int N, int K, float *__restrict__ x) {
-  __shared__ u32x4 lds[TL::LDS_CHUNKS];
-  const int n0 = blockIdx.x * TL::BN, m0 = blockIdx.y * TL::BM;
+__global__ __launch_bounds__(NT) void k_gemm_residual(const f16 *__restrict__ A,
+                                                      const bf16 *__restrict__ W, int rows,
+                                                      int N, int K, Launch ln,
+                                                      float *__restrict__ x,
+                                                      float *__restrict__ part) {
+  __shared__ u32x4 lds[2 * TL::STAGE];
+  const Work wk = block_work(ln.nm, ln.nn, ln.nsplit, ln.gm);
+  const int m0 = wk.tm * TL::BM, n0 = wk.tn * TL::BN;
+  int k0, k1;
+  split_range(K / BK, ln.nsplit, wk.split, k0, k1);
   f32x16 acc[TL::FM][TL::FN];
-  mainloop<TL, false, true>(A, rows, m0, W, [=](int r) { return min(n0 + r, N - 1); }, K, lds,
-                            acc);
+  mainloop<TL, false, true>(
+      A, [=](int r) { return min(m0 + r, rows - 1); }, W,
+      [=](int r) { return min(n0 + r, N - 1); }, K, k0, k1, lds, acc);
+  if (ln.nsplit > 1) {
+    store_partial<TL>(acc, part, wk.split, rows, N, m0, n0);
+    return;
+  }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w / TL::WN, wn = w % TL::WN;
 #pragma unroll
@@ -192,35 +300,47 @@ __global__ __launch_bounds__(256) void k_gemm_residual(const f16 *__restrict__ A
   }
 }
 
-hipError_t gemm_residual(const f16 *A, const bf16 *W, int rows, int N, int K, float *x,
-                         hipStream_t s) {
-  if (rows == 0) return hipSuccess;
-  typedef TileStd TL;
-  dim3 grid((N + TL::BN - 1) / TL::BN, (rows + TL::BM - 1) / TL::BM);
-  k_gemm_residual<TL><<<grid, 256, 0, s>>>(A, W, rows, N, K, x);
-  return hipGetLastError();
+// x[row][col] += sum_s part[s][row][col], s in order.
+__global__ __launch_bounds__(256) void k_reduce_residual(const float *__restrict__ part,
+                                                         int nsplit, long n,
+                                                         float *__restrict__ x) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  float v = 0.f;
+  for (int s = 0; s < nsplit; ++s) v += part[s * n + i];
+  x[i] += v;
 }
 
 // ------------------------------------------------------------------- SwiGLU
-// Block column tile o0 .. o0+128 of the FFN hidden. Its 256 B rows are laid
-// out per wave: wave wn takes gate rows o0+64wn .. +63 then the matching up
-// rows, so MFMA blocks fn and fn+2 of a wave hold gate and up of the same
-// output columns.
+// Output column tile o0 .. o0+128 of the FFN hidden. Its 256 B rows are laid
+// out per wave column: wave column wn takes gate rows o0+64wn .. +63 then the
+// matching up rows, so MFMA blocks fn and fn+2 hold gate and up of the same
+// output columns. Split partials keep that B-row order: partial column
+// 256 tn + lr holds B row brow(lr).
 template <class TL>
-__global__ __launch_bounds__(256) void k_gemm_swiglu(const f16 *__restrict__ A,
-                                                     const bf16 *__restrict__ W, int rows,
-                                                     int F, int K, f16 *__restrict__ h) {
-  static_assert(TL::WN == 2 && TL::TN == 128, "gate/up pairing needs 128-column waves");
-  __shared__ u32x4 lds[TL::LDS_CHUNKS];
-  const int o0 = blockIdx.x * 128, m0 = blockIdx.y * TL::BM;
+__global__ __launch_bounds__(NT) void k_gemm_swiglu(const f16 *__restrict__ A,
+                                                    const bf16 *__restrict__ W, int rows, int F,
+                                                    int K, Launch ln, f16 *__restrict__ h,
+                                                    float *__restrict__ part) {
+  static_assert(TL::WN == 2 && TL::TN == 128 && TL::BN == 256, "gate/up pairing");
+  __shared__ u32x4 lds[2 * TL::STAGE];
+  const Work wk = block_work(ln.nm, ln.nn, ln.nsplit, ln.gm);
+  const int m0 = wk.tm * TL::BM, o0 = wk.tn * 128;
+  int k0, k1;
+  split_range(K / BK, ln.nsplit, wk.split, k0, k1);
   f32x16 acc[TL::FM][TL::FN];
-  mainloop<TL, false, true>(A, rows, m0, W,
-               [=](int r) {
-                 const int q = r & 127;
-                 const int oc = min(o0 + (r >> 7) * 64 + (q & 63), F - 1);
-                 return q < 64 ? oc : F + oc;
-               },
-               K, lds, acc);
+  mainloop<TL, false, true>(
+      A, [=](int r) { return min(m0 + r, rows - 1); }, W,
+      [=](int r) {
+        const int q = r & 127;
+        const int oc = min(o0 + (r >> 7) * 64 + (q & 63), F - 1);
+        return q < 64 ? oc : F + oc;
+      },
+      K, k0, k1, lds, acc);
+  if (ln.nsplit > 1) {
+    store_partial<TL>(acc, part, wk.split, rows, ln.nn * 256, m0, wk.tn * 256);
+    return;
+  }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w / TL::WN, wn = w % TL::WN;
 #pragma unroll
@@ -232,108 +352,139 @@ __global__ __launch_bounds__(256) void k_gemm_swiglu(const f16 *__restrict__ A,
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = m0 + acc_row<TL>(wm, fm, r, lane);
-        if (row >= rows) continue;
-        const float g = acc[fm][fn][r], u = acc[fm][fn + 2][r];
-        h[(long)row * F + col] = static_cast<f16>(g / (1.f + __expf(-g)) * u);
+        if (row < rows)
+          h[(long)row * F + col] = static_cast<f16>(silu_mul(acc[fm][fn][r], acc[fm][fn + 2][r]));
       }
   }
 }
 
-hipError_t gemm_swiglu(const f16 *A, const bf16 *W, int rows, int F, int K, f16 *h,
-                       hipStream_t s) {
-  if (rows == 0) return hipSuccess;
-  typedef TileStd TL;
-  dim3 grid((F + 127) / 128, (rows + TL::BM - 1) / TL::BM);
-  k_gemm_swiglu<TL><<<grid, 256, 0, s>>>(A, W, rows, F, K, h);
-  return hipGetLastError();
+// h[row][o] = silu(gate) * up from the summed partials (B-row order above).
+__global__ __launch_bounds__(256) void k_reduce_swiglu(const float *__restrict__ part,
+                                                       int nsplit, int rows, int F, int ncols,
+                                                       f16 *__restrict__ h) {
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long)rows * F) return;
+  const int row = (int)(i / F), o = (int)(i % F);
+  const int tn = o / 128, within = o % 128, wn = within / 64, q = within % 64;
+  const long cg = (long)tn * 256 + wn * 128 + q, cu = cg + 64;
+  const long n = (long)rows * ncols;
+  float g = 0.f, u = 0.f;
+  for (int s = 0; s < nsplit; ++s) {
+    g += part[s * n + (long)row * ncols + cg];
+    u += part[s * n + (long)row * ncols + cu];
+  }
+  h[i] = static_cast<f16>(silu_mul(g, u));
 }
 
 // ------------------------------------------------- QKV + rotary + KV caches
-// Block column tile = two heads of the stacked q|k|v projection; wave wn owns
-// head slot 2 blockIdx.x + wn. MFMA blocks fn and fn+2 hold head dims d and
-// d + 64, the rotate-half pair.
+// Column tile = two heads of the stacked q|k|v projection; wave column wn owns
+// head slot 2 tn + wn. MFMA blocks fn and fn+2 hold head dims d and d + 64,
+// the rotate-half pair.
+__device__ __forceinline__ void qkv_store(const QKVOut<f16> &o, int n_heads, int n_kv, int slot,
+                                          int row, int d, float x1, float x2) {
+  if (slot < n_heads + n_kv) {
+    const int pos = o.row_pos ? o.row_pos[row] : row;
+    const float2 cs = o.rope[(long)pos * 64 + d];
+    const float y1 = x1 * cs.x - x2 * cs.y, y2 = x2 * cs.x + x1 * cs.y;
+    x1 = y1;
+    x2 = y2;
+  }
+  if (slot < n_heads) {
+    f16 *q = o.q + ((long)row * n_heads + slot) * 128;
+    q[d] = static_cast<f16>(x1);
+    q[d + 64] = static_cast<f16>(x2);
+  } else if (slot < n_heads + n_kv) {
+    f16 *k = o.k + ((long)(slot - n_heads) * o.kv_npos + row) * 128;
+    k[d] = static_cast<f16>(x1);
+    k[d + 64] = static_cast<f16>(x2);
+  } else {
+    f16 *vt = o.vt + (long)(slot - n_heads - n_kv) * 128 * o.kv_npos;
+    vt[(long)d * o.kv_npos + row] = static_cast<f16>(x1);
+    vt[(long)(d + 64) * o.kv_npos + row] = static_cast<f16>(x2);
+  }
+}
+
 template <class TL>
-__global__ __launch_bounds__(256) void k_gemm_qkv(const f16 *__restrict__ A,
-                                                  const bf16 *__restrict__ W, int rows, int K,
-                                                  int n_heads, int n_kv, QKVOut<f16> o) {
-  static_assert(TL::WN == 2 && TL::TN == 128, "one head per wave");
-  __shared__ u32x4 lds[TL::LDS_CHUNKS];
-  const int nslots = n_heads + 2 * n_kv;
-  const int n0 = blockIdx.x * 256, m0 = blockIdx.y * TL::BM;
-  const int nrows = nslots * 128;
+__global__ __launch_bounds__(NT) void k_gemm_qkv(const f16 *__restrict__ A,
+                                                 const bf16 *__restrict__ W, int rows, int K,
+                                                 int n_heads, int n_kv, Launch ln, QKVOut<f16> o,
+                                                 float *__restrict__ part) {
+  static_assert(TL::WN == 2 && TL::TN == 128 && TL::BN == 256, "one head per wave column");
+  __shared__ u32x4 lds[2 * TL::STAGE];
+  const Work wk = block_work(ln.nm, ln.nn, ln.nsplit, ln.gm);
+  const int nslots = n_heads + 2 * n_kv, nrows = nslots * 128;
+  const int m0 = wk.tm * TL::BM, n0 = wk.tn * 256;
+  int k0, k1;
+  split_range(K / BK, ln.nsplit, wk.split, k0, k1);
   f32x16 acc[TL::FM][TL::FN];
-  mainloop<TL, false, true>(A, rows, m0, W, [=](int r) { return min(n0 + r, nrows - 1); }, K,
-                            lds, acc);
+  mainloop<TL, false, true>(
+      A, [=](int r) { return min(m0 + r, rows - 1); }, W,
+      [=](int r) { return min(n0 + r, nrows - 1); }, K, k0, k1, lds, acc);
+  if (ln.nsplit > 1) {
+    store_partial<TL>(acc, part, wk.split, rows, nrows, m0, n0);
+    return;
+  }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w / TL::WN, wn = w % TL::WN;
-  const int slot = blockIdx.x * 2 + wn;
+  const int slot = wk.tn * 2 + wn;
   if (slot >= nslots) return;
-  const bool rot = slot < n_heads + n_kv;
 #pragma unroll
   for (int fm = 0; fm < TL::FM; ++fm)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = m0 + acc_row<TL>(wm, fm, r, lane);
       if (row >= rows) continue;
-      const int pos = o.row_pos ? o.row_pos[row] : row;
 #pragma unroll
-      for (int fn = 0; fn < 2; ++fn) {
-        const int d = fn * 32 + (lane & 31);
-        float x1 = acc[fm][fn][r], x2 = acc[fm][fn + 2][r];
-        if (rot) {
-          const float2 cs = o.rope[(long)pos * 64 + d];
-          const float y1 = x1 * cs.x - x2 * cs.y, y2 = x2 * cs.x + x1 * cs.y;
-          x1 = y1;
-          x2 = y2;
-        }
-        if (slot < n_heads) {
-          f16 *q = o.q + ((long)row * n_heads + slot) * 128;
-          q[d] = static_cast<f16>(x1);
-          q[d + 64] = static_cast<f16>(x2);
-        } else if (rot) {
-          f16 *k = o.k + ((long)(slot - n_heads) * o.kv_npos + row) * 128;
-          k[d] = static_cast<f16>(x1);
-          k[d + 64] = static_cast<f16>(x2);
-        } else {
-          f16 *vt = o.vt + (long)(slot - n_heads - n_kv) * 128 * o.kv_npos;
-          vt[(long)d * o.kv_npos + row] = static_cast<f16>(x1);
-          vt[(long)(d + 64) * o.kv_npos + row] = static_cast<f16>(x2);
-        }
-      }
+      for (int fn = 0; fn < 2; ++fn)
+        qkv_store(o, n_heads, n_kv, slot, row, fn * 32 + (lane & 31), acc[fm][fn][r],
+                  acc[fm][fn + 2][r]);
     }
 }
 
-hipError_t gemm_qkv_rope(const f16 *A, const bf16 *W, int rows, int K, int n_heads, int n_kv,
-                         const QKVOut<f16> &out, hipStream_t s) {
-  if (rows == 0) return hipSuccess;
-  typedef TileStd TL;
-  const int nslots = n_heads + 2 * n_kv;
-  dim3 grid((nslots + 1) / 2, (rows + TL::BM - 1) / TL::BM);
-  k_gemm_qkv<TL><<<grid, 256, 0, s>>>(A, W, rows, K, n_heads, n_kv, out);
-  return hipGetLastError();
+// Rotary + cache scatter from the summed partials; one thread per
+// (row, head slot, d < 64).
+__global__ __launch_bounds__(256) void k_reduce_qkv(const float *__restrict__ part, int nsplit,
+                                                    int rows, int n_heads, int n_kv,
+                                                    QKVOut<f16> o) {
+  const int nslots = n_heads + 2 * n_kv, ncols = nslots * 128;
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long)rows * nslots * 64) return;
+  const int row = (int)(i / (nslots * 64));
+  const int rem = (int)(i % (nslots * 64));
+  const int slot = rem / 64, d = rem % 64;
+  const long n = (long)rows * ncols;
+  const long c = (long)row * ncols + slot * 128 + d;
+  float x1 = 0.f, x2 = 0.f;
+  for (int s = 0; s < nsplit; ++s) {
+    x1 += part[s * n + c];
+    x2 += part[s * n + c + 64];
+  }
+  qkv_store(o, n_heads, n_kv, slot, row, d, x1, x2);
 }
 
 // ------------------------------------------------------ LM head + chunk LSE
 // Transposed product: the MFMA rows are vocabulary entries (A = W_lm) and the
 // columns are scored tokens (B = normed hidden rows), so a token's reduction
 // over the vocabulary runs down a lane's registers, across the two lane
-// halves and across the WM waves. Block (vocab tile c, token tile) writes, for
-// each token t, part[c][t] = (max_v l, sum_v exp(l - max)) over its BM
-// vocabulary rows, and the target logit when the target falls in the tile.
-// The [tokens x vocab] logits never leave registers.
+// halves and across the WM waves of a column. Block (vocab tile c, token
+// tile) writes, for each token t, part[c][t] = (max_v l, sum_v exp(l - max))
+// over its BM vocabulary rows, and the target logit when the target falls in
+// the tile. The [tokens x vocab] logits never leave registers.
 template <class TL>
-__global__ __launch_bounds__(256) void k_gemm_lmhead(const f16 *__restrict__ Hn,
-                                                     const bf16 *__restrict__ Wlm, int T,
-                                                     int vocab, int K,
-                                                     const int32_t *__restrict__ lm_tgt,
-                                                     float2 *__restrict__ part,
-                                                     float *__restrict__ tgt_logit) {
-  __shared__ u32x4 lds[TL::LDS_CHUNKS];
+__global__ __launch_bounds__(NT) void k_gemm_lmhead(const f16 *__restrict__ Hn,
+                                                    const bf16 *__restrict__ Wlm, int T,
+                                                    int vocab, int K, Launch ln,
+                                                    const int32_t *__restrict__ lm_tgt,
+                                                    float2 *__restrict__ part,
+                                                    float *__restrict__ tgt_logit) {
+  __shared__ u32x4 lds[2 * TL::STAGE];
   __shared__ float red[TL::WM][TL::BN];
-  const int n0 = blockIdx.x * TL::BN, m0 = blockIdx.y * TL::BM;
+  const Work wk = block_work(ln.nm, ln.nn, 1, ln.gm);
+  const int m0 = wk.tm * TL::BM, n0 = wk.tn * TL::BN;
   f32x16 acc[TL::FM][TL::FN];
-  mainloop<TL, true, false>(Wlm, vocab, m0, Hn, [=](int r) { return min(n0 + r, T - 1); }, K,
-                            lds, acc);
+  mainloop<TL, true, false>(
+      Wlm, [=](int r) { return min(m0 + r, vocab - 1); }, Hn,
+      [=](int r) { return min(n0 + r, T - 1); }, K, 0, K / BK, lds, acc);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w / TL::WN, wn = w % TL::WN;
 
@@ -380,7 +531,7 @@ __global__ __launch_bounds__(256) void k_gemm_lmhead(const f16 *__restrict__ Hn,
       float s = red[0][c];
 #pragma unroll
       for (int i = 1; i < TL::WM; ++i) s += red[i][c];
-      part[(long)blockIdx.y * T + t] = make_float2(mx[fn], s);
+      part[(long)wk.tm * T + t] = make_float2(mx[fn], s);
     }
     // Target logit: row tr of this wave's sub-tile, held by lane half
     // (tr / 4) % 2 in register 4 (tr % 32 / 8) + tr % 4 of block tr / 32.
@@ -398,14 +549,71 @@ __global__ __launch_bounds__(256) void k_gemm_lmhead(const f16 *__restrict__ Hn,
   }
 }
 
+constexpr int kMaxSplit = 8;
+
+}  // namespace
+
+size_t gemm_split_floats(int rows, int N, int K) {
+  const int nm = (rows + TileStd::BM - 1) / TileStd::BM, nn = (N + TileStd::BN - 1) / TileStd::BN;
+  const int s = choose_split(nm * nn, K / BK, kMaxSplit);
+  return s > 1 ? (size_t)s * rows * nn * TileStd::BN : 0;
+}
+
+hipError_t gemm_residual(const f16 *A, const bf16 *W, int rows, int N, int K, float *x,
+                         float *part, hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  typedef TileStd TL;
+  Launch ln{(rows + TL::BM - 1) / TL::BM, (N + TL::BN - 1) / TL::BN, 1, 8};
+  ln.nsplit = choose_split(ln.nm * ln.nn, K / BK, kMaxSplit);
+  k_gemm_residual<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, N, K, ln, x, part);
+  if (ln.nsplit > 1) {
+    const long n = (long)rows * N;
+    k_reduce_residual<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(part, ln.nsplit, n, x);
+  }
+  return hipGetLastError();
+}
+
+hipError_t gemm_swiglu(const f16 *A, const bf16 *W, int rows, int F, int K, f16 *h, float *part,
+                       hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  typedef TileStd TL;
+  Launch ln{(rows + TL::BM - 1) / TL::BM, (F + 127) / 128, 1, 8};
+  ln.nsplit = choose_split(ln.nm * ln.nn, K / BK, kMaxSplit);
+  k_gemm_swiglu<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, F, K, ln, h, part);
+  if (ln.nsplit > 1) {
+    const long n = (long)rows * F;
+    k_reduce_swiglu<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(part, ln.nsplit, rows, F,
+                                                                 ln.nn * 256, h);
+  }
+  return hipGetLastError();
+}
+
+hipError_t gemm_qkv_rope(const f16 *A, const bf16 *W, int rows, int K, int n_heads, int n_kv,
+                         const QKVOut<f16> &out, float *part, hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  typedef TileStd TL;
+  const int nslots = n_heads + 2 * n_kv;
+  Launch ln{(rows + TL::BM - 1) / TL::BM, (nslots + 1) / 2, 1, 8};
+  ln.nsplit = choose_split(ln.nm * ln.nn, K / BK, kMaxSplit);
+  k_gemm_qkv<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, K, n_heads, n_kv, ln, out, part);
+  if (ln.nsplit > 1) {
+    const long n = (long)rows * nslots * 64;
+    k_reduce_qkv<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(part, ln.nsplit, rows, n_heads,
+                                                              n_kv, out);
+  }
+  return hipGetLastError();
+}
+
 int lmhead_chunks(int vocab) { return (vocab + TileStd::BM - 1) / TileStd::BM; }
 
 hipError_t gemm_lmhead(const f16 *A, const bf16 *W, int rows, int vocab, int K,
                        const int32_t *lm_tgt, float2 *part, float *tgt_logit, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
-  dim3 grid((rows + TL::BN - 1) / TL::BN, lmhead_chunks(vocab));
-  k_gemm_lmhead<TL><<<grid, 256, 0, s>>>(A, W, rows, vocab, K, lm_tgt, part, tgt_logit);
+  // Token tiles fastest: the blocks sharing a vocabulary tile run together.
+  Launch ln{lmhead_chunks(vocab), (rows + TL::BN - 1) / TL::BN, 1, 1};
+  k_gemm_lmhead<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, vocab, K, ln, lm_tgt, part,
+                                               tgt_logit);
   return hipGetLastError();
 }
 

@@ -42,7 +42,7 @@ Split cascade_split(int T, int P, int n_heads, int n_kv) {
 struct Plan {
   int kv_npos, bk_npos, max_t, rows_max, rope_npos, lm_chunks;
   size_t x, xn, q, attn, h, kc, vtc, bk, bvt, part_acc, part_ml, lm_part, tgt, row_lo,
-      row_pos, lm_tgt, rope, h_last, total;
+      row_pos, lm_tgt, rope, h_last, gemm_part, total;
 };
 
 // Returns an empty message if cfg is supported.
@@ -88,6 +88,20 @@ Plan make_plan(const vsr_config &c) {
       if (s.nchunks > 1) part_rows = std::max(part_rows, (size_t)s.nchunks * T * G);
     }
   }
+  // Split-K partials of the MFMA GEMMs: the largest need over every row count
+  // (the split only changes where the 256-row tile count does).
+  size_t gemm_part = 0;
+  if (c.dtype == VSR_BF16) {
+    const int qkv_n = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
+    for (int r = 256;; r += 256) {
+      const int rows = std::min(r, p.rows_max);
+      gemm_part = std::max({gemm_part, gemm_split_floats(rows, qkv_n, c.d_model),
+                            gemm_split_floats(rows, c.d_model, c.n_heads * c.head_dim),
+                            gemm_split_floats(rows, 2 * c.d_ff, c.d_model),
+                            gemm_split_floats(rows, c.d_model, c.d_ff)});
+      if (rows == p.rows_max) break;
+    }
+  }
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -113,6 +127,7 @@ Plan make_plan(const vsr_config &c) {
   p.lm_tgt = take((size_t)p.max_t * 4);
   p.rope = take((size_t)p.rope_npos * (hd / 2) * 8);
   p.h_last = take(d * 4);
+  p.gemm_part = take(gemm_part * 4);
   p.total = off;
   return p;
 }
@@ -297,6 +312,7 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
   const int d = cf.d_model, Hq = cf.n_heads, Hkv = cf.n_kv_heads, hd = cf.head_dim, F = cf.d_ff;
   float *x = c->at<float>(p.x);
   TA *xn = c->at<TA>(p.xn), *q = c->at<TA>(p.q), *attn = c->at<TA>(p.attn), *h = c->at<TA>(p.h);
+  float *gpart = c->at<float>(p.gemm_part);
   const size_t layer_cache = (size_t)Hkv * p.kv_npos * hd;
   hipStream_t s = c->stream;
   for (int l = 0; l < cf.n_layers; ++l) {
@@ -324,7 +340,7 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       qo.row_pos = c->at<int32_t>(p.row_pos);
     }
     if constexpr (kMfma) {
-      STAGE(c, K_QKV, "qkv projection", gemm_qkv_rope(xn, wqkv, rows, d, Hq, Hkv, qo, s));
+      STAGE(c, K_QKV, "qkv projection", gemm_qkv_rope(xn, wqkv, rows, d, Hq, Hkv, qo, gpart, s));
     } else {
       STAGE(c, K_QKV, "qkv projection",
             simple_qkv_rope<TA>(xn, wqkv, rows, d, Hq, Hkv, hd, qo, s));
@@ -374,7 +390,8 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       STAGE(c, K_ATTN, "attention", simple_attn<TA>(a, s));
     }
     if constexpr (kMfma) {
-      STAGE(c, K_OPROJ, "output projection", gemm_residual(attn, wo, rows, d, Hq * hd, x, s));
+      STAGE(c, K_OPROJ, "output projection",
+            gemm_residual(attn, wo, rows, d, Hq * hd, x, gpart, s));
     } else {
       STAGE(c, K_OPROJ, "output projection",
             simple_residual<TA>(attn, wo, rows, d, Hq * hd, x, s));
@@ -383,8 +400,8 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
              launch_rmsnorm<TW, TA>(x, static_cast<const TW *>(c->ffn_norm[l]), rows, d,
                                     cf.rms_eps, xn, s));
     if constexpr (kMfma) {
-      STAGE(c, K_GATEUP, "gate/up projection", gemm_swiglu(xn, wgu, rows, F, d, h, s));
-      STAGE(c, K_DOWN, "down projection", gemm_residual(h, wdown, rows, d, F, x, s));
+      STAGE(c, K_GATEUP, "gate/up projection", gemm_swiglu(xn, wgu, rows, F, d, h, gpart, s));
+      STAGE(c, K_DOWN, "down projection", gemm_residual(h, wdown, rows, d, F, x, gpart, s));
     } else {
       STAGE(c, K_GATEUP, "gate/up projection", simple_swiglu<TA>(xn, wgu, rows, F, d, h, s));
       STAGE(c, K_DOWN, "down projection", simple_residual<TA>(h, wdown, rows, d, F, x, s));
