@@ -46,21 +46,45 @@ def log(msg):
 
 
 def stage_flops(cfg, P, lens):
-    """Algorithmic FLOPs of one verify pass per stage (multiply-add = 2)."""
+    """Algorithmic FLOPs of one verify pass per stage (multiply-add = 2).
+
+    The prefix pass's last layer needs keys/values for every prefix row but
+    attention, projections and FFN only for the last row (the one predicting
+    candidate token 0), which is all the library computes there.
+    """
     d, hq, hd, F, V = cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ff, cfg.vocab
     L = cfg.n_layers
     T = int(sum(lens))
     f = {}
-    for ph, rows in (("prefill", P), ("score", T)):
+    for ph, rows, rows_tail in (("prefill", P, 1), ("score", T, T)):
+        body = rows * (L - 1) + rows_tail if L else 0
         f[f"{ph}.qkv_rope"] = 2.0 * rows * cfg.qkv_rows * d * L
-        f[f"{ph}.o_proj"] = 2.0 * rows * d * hq * hd * L
-        f[f"{ph}.gate_up_swiglu"] = 2.0 * rows * 2 * F * d * L
-        f[f"{ph}.down_proj"] = 2.0 * rows * d * F * L
+        f[f"{ph}.o_proj"] = 2.0 * body * d * hq * hd
+        f[f"{ph}.gate_up_swiglu"] = 2.0 * body * 2 * F * d
+        f[f"{ph}.down_proj"] = 2.0 * body * d * F
     # QK^T and PV over the visible keys of every query (causal / cascade).
-    f["prefill.attention"] = 4.0 * hd * hq * (P * (P + 1) / 2) * L
+    f["prefill.attention"] = 4.0 * hd * hq * ((P * (P + 1) / 2) * (L - 1) + P) if L else 0.0
     f["score.attention"] = 4.0 * hd * hq * sum(n * P + n * (n + 1) / 2 for n in lens) * L
     f["score.lm_head_lse"] = 2.0 * T * V * d
     return f
+
+
+def measured_traffic(kname):
+    """HBM bytes per launch of `kname` from the committed counter runs
+    (profiles/traffic.json), or None if absent or if the kernel source has
+    changed since they were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        rec = json.load(open(path))
+        src = os.path.join(ROOT, rec["source"])
+        if rec.get("kernel") != kname:
+            return None
+        if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+            return None
+        return round(rec["hbm_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(wl, log_fn):
@@ -110,6 +134,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--stages", action="store_true", help="print per-stage times to stderr")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only copy MIB MiB device-to-device (counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the scoring pass is "
@@ -118,6 +144,16 @@ def main():
 
     import torch
     from paper_2601_01513_amd.binding import Verifier
+
+    if args.copy_probe:
+        n = args.copy_probe << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n, "copies": 3}))
+        return
 
     cfg = W.CONFIGS[args.workload]
     dev = torch.device("cuda:0")
@@ -175,7 +211,7 @@ def main():
     achieved = kflops / launches / (avg_ms * 1e-3) / 1e12
     roofline = {"kernel": kname, "bound": "mfma", "achieved": round(achieved, 1),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic(kname),
                 "launches": launches, "avg_launch_ms": round(avg_ms, 4),
                 "flop_per_launch": kflops / launches}
 

@@ -8,7 +8,7 @@ What is computed (Section 3.1, Eq. 6-7; Algorithm 1 final selection):
   the verifier scores every drafted answer a_i against the shared conditioning
   (Q, V) and the highest-scoring draft is selected. The score is read as the
   verifier's teacher-forced sequence log-likelihood of the draft (the
-  "self-consistent" strategy of Section 4.5 / Table 3, which ranks drafts by
+  "self-consistent" strategy of Section 4.6, Table 3, which ranks drafts by
   the verifier's own likelihood and is sensitive to draft length, i.e. an
   unnormalised sum):
 

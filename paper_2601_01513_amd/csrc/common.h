@@ -84,7 +84,10 @@ hipError_t launch_reduce_select(const Branches &br, const float *logprobs, float
 
 // ----- layouts of the caches -----------------------------------------------
 // K cache  : [n_kv][npos][hd]  (rotated keys, position-major)
-// Vt cache : [n_kv][hd][npos]  (values, transposed: position-contiguous)
+// Vt cache : [n_kv][hd][npos]  (values, transposed: position-contiguous). On
+//            the MFMA path position p is stored at (p & ~12) | ((p & 4) << 1)
+//            | ((p & 8) >> 1) (quarters 1 and 2 of each 16-group swapped),
+//            the key order of the attention kernel's PV operand.
 
 // Destinations of the QKV projection epilogue.
 template <typename T>
@@ -132,7 +135,8 @@ struct AttnArgs {
   const f16 *bvt;       // mode 1: branch Vt [n_kv][hd][bk_npos]
   int bk_npos;
   const int32_t *row_lo;  // mode 1
-  int T;                // query tokens
+  int T;                // tokens (queries are tokens t0 .. T-1; keys up to T-1)
+  int t0;               // first query token
   int P;                // mode 1: prefix length
   int n_heads, n_kv;
   int nchunks;          // mode 1: prefix split (partials when > 1)
@@ -141,6 +145,7 @@ struct AttnArgs {
   float *part_acc;      // [nchunks][n_kv][T*G][hd]
   float2 *part_ml;      // [nchunks][n_kv][T*G]
 };
+int attn_query_tile();  // stacked query rows per attention block
 hipError_t attn_prefill(const AttnArgs &a, hipStream_t s);
 hipError_t attn_cascade(const AttnArgs &a, hipStream_t s);
 hipError_t attn_merge(const AttnArgs &a, hipStream_t s);
@@ -165,7 +170,7 @@ struct SimpleAttnArgs {
   const void *q, *k, *vt, *bk, *bvt;
   int kv_npos, bk_npos;
   const int32_t *row_lo;
-  int T, P, n_heads, n_kv, hd;
+  int T, t0, P, n_heads, n_kv, hd;  // query tokens t0 .. T-1
   int mode;
   void *out;
 };

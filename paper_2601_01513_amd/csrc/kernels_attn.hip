@@ -3,20 +3,22 @@
 // One kernel serves the prefix prefill (causal) and the candidate pass
 // (cascade: the shared prefix keys, then each candidate's own causal block).
 // For KV head h the query rows of all G = n_heads / n_kv query heads that read
-// it are stacked, row r = (token r / G, head h G + r % G), so every key tile
-// staged in LDS is used by all of them -- and, in the candidate pass, by all
-// M candidates at once: the prefix keys are read once per query tile, not
+// it are stacked, row r = (token t0 + r / G, head h G + r % G), so every key
+// tile staged in LDS is used by all of them -- and, in the candidate pass, by
+// all M candidates at once: the prefix keys are read once per query tile, not
 // once per candidate.
 //
-// A 256-thread block owns 128 stacked query rows (32 per wave) and walks 64-key
-// tiles. Each wave computes S^T = K . Q^T on MFMA 32x32x16 (keys as MFMA rows,
-// queries as columns), so a lane owns one query's scores and every per-query
-// softmax quantity is a per-lane scalar. The probabilities feed O^T += V^T . P^T
-// straight from registers: the k-index of that product is permuted to match
-// the key order the S^T accumulator leaves in each lane, and V^T is staged
-// with the same permutation (the Vt cache stores values position-contiguous).
-// Softmax runs online in the log2 domain in fp32; P is rounded to fp16 for the
-// PV product.
+// A 512-thread block owns 256 stacked query rows (32 per wave, two waves per
+// SIMD) and walks 64-key tiles through a two-stage LDS ring filled by direct
+// global->LDS loads. Each wave computes S^T = K . Q^T on MFMA 32x32x16 (keys
+// as MFMA rows, queries as columns), so a lane owns one query's scores and
+// every per-query softmax quantity is a per-lane scalar. The probabilities
+// feed O^T += V^T . P^T straight from registers: the MFMA k-index of that
+// product is permuted to the key order the S^T accumulator leaves in each
+// lane, and the Vt cache stores positions in the matching order (within each
+// aligned group of 16 positions the middle two quarters are swapped), so a
+// lane's V^T operand is one 16-byte LDS read. Softmax runs online in the log2
+// domain in fp32; operands (queries, keys, values, probabilities) are fp16.
 //
 // The candidate pass may split the prefix keys into chunks (more blocks on the
 // chip); each chunk writes (max, sum, unnormalised output) partials and
@@ -28,28 +30,35 @@ namespace vsr {
 namespace {
 
 constexpr int HD = 128;   // head dim of the MFMA path
-constexpr int QT = 128;   // stacked query rows per block
+constexpr int NT = 512;   // threads per block
+constexpr int NW = NT / 64;
+constexpr int QT = NW * 32;  // stacked query rows per block
 constexpr int KT = 64;    // keys per tile
+constexpr int KCH = KT * 16;   // 16-byte chunks of a K tile  [64 keys][128 dims]
+constexpr int VCH = HD * 8;    // 16-byte chunks of a V^T tile [128 dims][64 keys]
+constexpr int STAGE = KCH + VCH;
 
 __device__ __forceinline__ f16x8 as_f16x8(u32x4 v) { return __builtin_bit_cast(f16x8, v); }
 
-// K tile [64 keys][128 dims]: 16 chunks per key, XOR-swizzled by key.
-__device__ __forceinline__ int ks_idx(int key, int c) { return key * 16 + (c ^ (key & 7)); }
-// V^T tile [128 dims][64 keys]: 8 chunks per dim row, XOR-swizzled by row;
-// rows with bit 3 set store their two 8-byte halves swapped so that the
-// 8-byte fragment reads of 16 consecutive rows hit distinct banks.
-__device__ __forceinline__ int vs_idx(int d, int c) { return d * 8 + (c ^ (d & 7)); }
+// LDS serves 256 bytes (64 banks) per cycle; the 16 lanes of a 16-byte load
+// served together must hit distinct bank groups.
+// K tile: a key row is 256 bytes (16 chunks); chunk c of key k at c ^ (k % 16).
+__device__ __forceinline__ int ks_idx(int key, int c) { return key * 16 + (c ^ (key & 15)); }
+// V^T tile: a row is 128 bytes (8 chunks), two rows per bank window; chunk c
+// of row d at c ^ ((d / 2) % 8).
+__device__ __forceinline__ int vs_idx(int d, int c) { return d * 8 + (c ^ ((d >> 1) & 7)); }
 
 // Key visibility of one key segment.
 enum SegMode { SEG_ALL = 0, SEG_CAUSAL = 1, SEG_BRANCH = 2 };
 
 struct Seg {
   const f16 *k;    // [npos][HD] of this KV head
-  const f16 *vt;   // [HD][npos] of this KV head
+  const f16 *vt;   // [HD][npos] of this KV head (interleaved positions)
   int npos;        // position stride of vt
   int kvalid;      // keys >= kvalid hold no data (never visible)
   int kbeg, kend;  // key range walked by the block: [kbeg, kend), kbeg % 64 == 0
   int mode;
+  int tok_min;     // smallest query token of the block (mask-free tile test)
 };
 
 struct Lane {
@@ -57,135 +66,121 @@ struct Lane {
   int lo;    // SEG_BRANCH: first visible key
   float m, l;
   f32x16 o[HD / 32];
-  f16x8 q[HD / 16];
+  const u32x4 *qs;  // the block's query tile in LDS [QT rows][16 chunks]
+  int qrow;         // this lane's row in it
 };
 
-__device__ __forceinline__ void load_tile(const Seg &sg, int kb, u32x4 (&rk)[4], u32x4 (&rv)[4]) {
-  const int t = threadIdx.x;
+// Direct loads of key tile kb into an LDS stage. Load i of wave w fills K
+// rows 4 (i NW + w) .. +3 and V^T rows 8 (i NW + w) .. +7; lane l lands in
+// 16-byte slot l of that 1 KB, i.e. physical chunk l % 16 of K row l / 16, or
+// l % 8 of V^T row l / 8; the global address carries the logical chunk.
+__device__ __forceinline__ void load_tile(const Seg &sg, int kb, u32x4 *stage) {
+  const int t = threadIdx.x, w = t >> 6, l = t & 63;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int id = i * 256 + t;
-    const int key = id >> 4, c = id & 15;
-    rk[i] = reinterpret_cast<const u32x4 *>(sg.k + (long)(kb + key) * HD)[c];
+  for (int i = 0; i < KCH / NT; ++i) {
+    const int j = i * NW + w, key = j * 4 + (l >> 4), c = (l & 15) ^ (key & 15);
+    __builtin_amdgcn_global_load_lds(sg.k + (long)(kb + key) * HD + c * 8, stage + j * 64, 16,
+                                     0, 0);
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int id = i * 256 + t;
-    const int d = id >> 3, c = id & 7;
-    const int k0 = kb + c * 8;
-    u32x4 v = reinterpret_cast<const u32x4 *>(sg.vt + (long)d * sg.npos + k0)[0];
-    if (k0 + 8 > sg.kvalid) {  // zero values past the written keys (P = 0 there)
-      uint32_t *e = reinterpret_cast<uint32_t *>(&v);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t lo = (k0 + 2 * j < sg.kvalid) ? 0x0000FFFFu : 0u;
-        const uint32_t hi = (k0 + 2 * j + 1 < sg.kvalid) ? 0xFFFF0000u : 0u;
-        e[j] &= (lo | hi);
-      }
-    }
-    rv[i] = v;
-  }
-}
-
-__device__ __forceinline__ void store_tile(u32x4 *Ks, u32x4 *Vs, const u32x4 (&rk)[4],
-                                           const u32x4 (&rv)[4]) {
-  const int t = threadIdx.x;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int id = i * 256 + t;
-    Ks[ks_idx(id >> 4, id & 15)] = rk[i];
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int id = i * 256 + t;
-    const int d = id >> 3;
-    u32x4 v = rv[i];
-    if (d & 8) v = u32x4{v.z, v.w, v.x, v.y};
-    Vs[vs_idx(d, id & 7)] = v;
+  for (int i = 0; i < VCH / NT; ++i) {
+    const int j = i * NW + w, d = j * 8 + (l >> 3), c = (l & 7) ^ ((d >> 1) & 7);
+    __builtin_amdgcn_global_load_lds(sg.vt + (long)d * sg.npos + kb + c * 8,
+                                     stage + KCH + j * 64, 16, 0, 0);
   }
 }
 
 // One 64-key tile against this wave's 32 query rows.
-__device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *Ks,
-                                          const u32x4 *Vs, Lane &L, float scale_log2) {
+template <bool MASK>
+__device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *st, Lane &L,
+                                          float scale_log2) {
   const int lane = threadIdx.x & 63, h = lane >> 5;
-  f32x16 s[2];
+  const u32x4 *Ks = st, *Vs = st + KCH;
+  f32x16 s[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    s[b] = f32x16{};
-    const int key = b * 32 + (lane & 31);
+  for (int kk = 0; kk < HD / 16; ++kk) {
+    const f16x8 qf = as_f16x8(L.qs[ks_idx(L.qrow, 2 * kk + h)]);
 #pragma unroll
-    for (int kk = 0; kk < HD / 16; ++kk)
-      s[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_f16x8(Ks[ks_idx(key, 2 * kk + h)]),
-                                                     L.q[kk], s[b], 0, 0, 0);
+    for (int b = 0; b < 2; ++b)
+      s[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+          as_f16x8(Ks[ks_idx(b * 32 + (lane & 31), 2 * kk + h)]), qf, s[b], 0, 0, 0);
   }
-  // Mask and scale; key of register r of block b: kb + 32b + 8(r/4) + 4h + r%4.
+  // Scale (and mask); key of register r of block b: kb + 32b + 8(r/4) + 4h + r%4.
   float mloc = -INFINITY;
 #pragma unroll
   for (int b = 0; b < 2; ++b)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int key = kb + b * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-      bool vis = key < sg.kvalid;
-      if (sg.mode == SEG_CAUSAL) vis = vis && key <= L.tok;
-      if (sg.mode == SEG_BRANCH) vis = vis && key >= L.lo && key <= L.tok;
-      const float v = vis ? s[b][r] * scale_log2 : -INFINITY;
+      float v = s[b][r] * scale_log2;
+      if constexpr (MASK) {
+        const int key = kb + b * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        bool vis = key < sg.kvalid;
+        if (sg.mode == SEG_CAUSAL) vis = vis && key <= L.tok;
+        if (sg.mode == SEG_BRANCH) vis = vis && key >= L.lo && key <= L.tok;
+        v = vis ? v : -INFINITY;
+      }
       s[b][r] = v;
       mloc = fmaxf(mloc, v);
     }
   mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
   const float mnew = fmaxf(L.m, mloc);
   const float mref = mnew == -INFINITY ? 0.f : mnew;
-  const float alpha = exp2f(L.m - mref);
   float psum = 0.f;
   f16x8 p[4];
 #pragma unroll
   for (int b = 0; b < 2; ++b)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const float e = exp2f(s[b][r] - mref);
+      const float e = __builtin_amdgcn_exp2f(s[b][r] - mref);
       psum += e;
       p[b * 2 + (r >> 3)][r & 7] = static_cast<f16>(e);
     }
   psum += __shfl_xor(psum, 32, 64);
-  L.l = L.l * alpha + psum;
+  if (mnew != L.m) {  // rescale only when this lane's running max moved
+    const float alpha = __builtin_amdgcn_exp2f(L.m - mref);
+    L.l *= alpha;
+#pragma unroll
+    for (int db = 0; db < HD / 32; ++db) L.o[db] *= alpha;
+  }
+  L.l += psum;
   L.m = mnew;
-#pragma unroll
-  for (int db = 0; db < HD / 32; ++db) L.o[db] *= alpha;
   // O^T[d][q] += V^T[d][key] P^T[key][q]; for 16-key chunk c the MFMA k-index
-  // 8h' + e of lane half h' is key 16c + 8(e/4) + 4h' + e%4.
+  // 8h' + e of lane half h' is key 16c + 8(e/4) + 4h' + e%4, which the Vt
+  // position interleave places at chunk 2c + h' of the row.
 #pragma unroll
-  for (int c = 0; c < 4; ++c) {
+  for (int c = 0; c < 4; ++c)
 #pragma unroll
     for (int db = 0; db < HD / 32; ++db) {
       const int d = db * 32 + (lane & 31);
-      const int sw = (d >> 3) & 1;  // halves swapped on this row
-      const uint64_t *r0 =
-          reinterpret_cast<const uint64_t *>(&Vs[vs_idx(d, 2 * c)]) + (h ^ sw);
-      const uint64_t *r1 =
-          reinterpret_cast<const uint64_t *>(&Vs[vs_idx(d, 2 * c + 1)]) + (h ^ sw);
-      uint64_t v2[2] = {*r0, *r1};
-      const f16x8 va = __builtin_bit_cast(f16x8, v2);
-      L.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, p[c], L.o[db], 0, 0, 0);
+      L.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_f16x8(Vs[vs_idx(d, 2 * c + h)]), p[c],
+                                                       L.o[db], 0, 0, 0);
     }
-  }
 }
 
-__device__ __forceinline__ void walk_segment(const Seg &sg, u32x4 *Ks, u32x4 *Vs, Lane &L, float scale_log2) {
+// Whether tile kb can skip the per-key mask for every row of the block.
+__device__ __forceinline__ bool tile_clear(const Seg &sg, int kb) {
+  if (kb + KT > sg.kvalid) return false;
+  if (sg.mode == SEG_CAUSAL) return kb + KT - 1 <= sg.tok_min;
+  return sg.mode == SEG_ALL;
+}
+
+__device__ __forceinline__ void walk_segment(const Seg &sg, u32x4 *lds, Lane &L,
+                                             float scale_log2) {
   if (sg.kend <= sg.kbeg) return;
-  u32x4 rk[4], rv[4];
-  load_tile(sg, sg.kbeg, rk, rv);
-  store_tile(Ks, Vs, rk, rv);
+  load_tile(sg, sg.kbeg, lds);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  int stage = 0;
   for (int kb = sg.kbeg; kb < sg.kend; kb += KT) {
-    const bool more = kb + KT < sg.kend;
-    if (more) load_tile(sg, kb + KT, rk, rv);
-    tile_step(sg, kb, Ks, Vs, L, scale_log2);
+    u32x4 *cur = lds + stage * STAGE;
+    if (kb + KT < sg.kend) load_tile(sg, kb + KT, lds + (stage ^ 1) * STAGE);
+    if (tile_clear(sg, kb))
+      tile_step<false>(sg, kb, cur, L, scale_log2);
+    else
+      tile_step<true>(sg, kb, cur, L, scale_log2);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (more) {
-      store_tile(Ks, Vs, rk, rv);
-      __syncthreads();
-    }
+    stage ^= 1;
   }
 }
 
@@ -193,10 +188,10 @@ __device__ __forceinline__ void walk_segment(const Seg &sg, u32x4 *Ks, u32x4 *Vs
 // mode 1: candidate pass (prefix chunk blockIdx.z; the last chunk also walks
 //         the candidate's own keys).
 template <int MODE>
-__global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
-  __shared__ u32x4 Ks[KT * 16];
-  __shared__ u32x4 Vs[HD * 8];
-  const int G = a.n_heads / a.n_kv, TG = a.T * G;
+__global__ __launch_bounds__(NT) void k_attn(AttnArgs a) {
+  __shared__ u32x4 lds[2 * STAGE];
+  __shared__ u32x4 qlds[QT * 16];
+  const int G = a.n_heads / a.n_kv, TG = (a.T - a.t0) * G;
   const int kvh = blockIdx.y;
   // Prefill tiles with more keys first.
   const int qt = MODE == 0 ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
@@ -206,37 +201,46 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const int rowc = min(row, TG - 1);
 
   Lane L;
-  L.tok = rowc / G;
+  L.tok = a.t0 + rowc / G;
   const int head = kvh * G + rowc % G;
   L.lo = MODE == 1 ? a.row_lo[L.tok] : 0;
   L.m = -INFINITY;
   L.l = 0.f;
 #pragma unroll
   for (int db = 0; db < HD / 32; ++db) L.o[db] = f32x16{};
+  // Query tile -> LDS (same layout and swizzle as a K tile): wave w's rows
+  // 32 w .. 32 w + 31, four rows per direct load.
   {
-    const u32x4 *qp = reinterpret_cast<const u32x4 *>(a.q + ((long)L.tok * a.n_heads + head) * HD);
 #pragma unroll
-    for (int kk = 0; kk < HD / 16; ++kk) L.q[kk] = as_f16x8(qp[2 * kk + (lane >> 5)]);
+    for (int i = 0; i < 8; ++i) {
+      const int rl = w * 32 + i * 4 + (lane >> 4);          // LDS row
+      const int rg = min(q0 + rl, TG - 1);                   // stacked row it holds
+      const int c = (lane & 15) ^ (rl & 15);
+      const f16 *src = a.q + ((long)(a.t0 + rg / G) * a.n_heads + kvh * G + rg % G) * HD + c * 8;
+      __builtin_amdgcn_global_load_lds(src, qlds + (w * 32 + i * 4) * 16, 16, 0, 0);
+    }
   }
+  L.qs = qlds;
+  L.qrow = w * 32 + (lane & 31);
   const float scale_log2 = 1.4426950408889634f * rsqrtf((float)HD);
-  const int tok_last = min(q0 + QT - 1, TG - 1) / G;
+  const int tok_first = a.t0 + q0 / G;
+  const int tok_last = a.t0 + min(q0 + QT - 1, TG - 1) / G;
 
   const int chunk = blockIdx.z;
   if (MODE == 0) {
     Seg sg{a.k + (long)kvh * a.kv_npos * HD, a.vt + (long)kvh * HD * a.kv_npos, a.kv_npos,
-           a.T, 0, tok_last + 1, SEG_CAUSAL};
-    walk_segment(sg, Ks, Vs, L, scale_log2);
+           a.T, 0, tok_last + 1, SEG_CAUSAL, tok_first};
+    walk_segment(sg, lds, L, scale_log2);
   } else {
     const int kb = chunk * a.chunk, ke = min(a.P, kb + a.chunk);
     Seg sp{a.k + (long)kvh * a.kv_npos * HD, a.vt + (long)kvh * HD * a.kv_npos, a.kv_npos,
-           a.P, kb, ke, SEG_ALL};
-    walk_segment(sp, Ks, Vs, L, scale_log2);
+           a.P, kb, ke, SEG_ALL, tok_first};
+    walk_segment(sp, lds, L, scale_log2);
     if (chunk == a.nchunks - 1) {
-      const int tok_first = q0 / G;
       const int lo = a.row_lo[tok_first] & ~(KT - 1);
       Seg sb{a.bk + (long)kvh * a.bk_npos * HD, a.bvt + (long)kvh * HD * a.bk_npos, a.bk_npos,
-             a.T, lo, tok_last + 1, SEG_BRANCH};
-      walk_segment(sb, Ks, Vs, L, scale_log2);
+             a.T, lo, tok_last + 1, SEG_BRANCH, tok_first};
+      walk_segment(sb, lds, L, scale_log2);
     }
   }
 
@@ -295,11 +299,13 @@ __global__ __launch_bounds__(64) void k_attn_merge(AttnArgs a) {
 
 }  // namespace
 
+int attn_query_tile() { return QT; }
+
 hipError_t attn_prefill(const AttnArgs &a, hipStream_t s) {
-  if (a.T == 0) return hipSuccess;
+  if (a.T <= a.t0) return hipSuccess;
   const int G = a.n_heads / a.n_kv;
-  dim3 grid((a.T * G + QT - 1) / QT, a.n_kv, 1);
-  k_attn<0><<<grid, 256, 0, s>>>(a);
+  dim3 grid(((a.T - a.t0) * G + QT - 1) / QT, a.n_kv, 1);
+  k_attn<0><<<grid, NT, 0, s>>>(a);
   return hipGetLastError();
 }
 
@@ -307,7 +313,7 @@ hipError_t attn_cascade(const AttnArgs &a, hipStream_t s) {
   if (a.T == 0) return hipSuccess;
   const int G = a.n_heads / a.n_kv;
   dim3 grid((a.T * G + QT - 1) / QT, a.n_kv, a.nchunks);
-  k_attn<1><<<grid, 256, 0, s>>>(a);
+  k_attn<1><<<grid, NT, 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -12,9 +12,12 @@
 // the MFMAs consume panel k, panel k+1 is in flight -- fp16 operands straight
 // from global memory into LDS (global_load_lds, no registers), bf16 operands
 // through registers and the converter. One barrier per panel. LDS rows are
-// 16-byte chunks XOR-swizzled by row, so panel stores and fragment loads are
-// free of bank conflicts; for the direct loads the swizzle is applied to the
-// global addresses (a direct load writes lane l's 16 bytes at base + 16 l).
+// eight 16-byte chunks; gfx950 LDS serves 256 bytes (64 banks) per cycle, so
+// two consecutive 128-byte rows share a bank window: chunk c of row r sits at
+// c ^ ((r / 2) % 8), which gives the 16 lanes of a 16-byte fragment load
+// (rows r..r+15, one chunk) 16 distinct bank groups. For the direct loads the
+// swizzle is applied to the global addresses (a direct load writes lane l's
+// 16 bytes at base + 16 l).
 //
 // Blocks are numbered so that the ones resident on one XCD at the same time
 // share A and B panels in that XCD's L2 (the hardware deals block b to XCD
@@ -55,7 +58,7 @@ struct Tile {
 // pairs and the gate/up pairs sit in the same lane and register.
 typedef Tile<256, 256, 4, 2> TileStd;
 
-__device__ __forceinline__ int swz(int row, int c) { return row * 8 + (c ^ (row & 7)); }
+__device__ __forceinline__ int swz(int row, int c) { return row * 8 + (c ^ ((row >> 1) & 7)); }
 __device__ __forceinline__ f16x8 as_f16x8(u32x4 v) { return __builtin_bit_cast(f16x8, v); }
 
 // Eight bf16 values -> eight fp16 values (exact for |v| in [2^-17, 65504];
@@ -97,7 +100,7 @@ struct Operand {
         // lane l lands in physical chunk l % 8 of row l / 8.
         const int w = t >> 6, l = t & 63;
         row = (i * NWAVES + w) * 8 + (l >> 3);
-        c = (l & 7) ^ (row & 7);
+        c = (l & 7) ^ ((row >> 1) & 7);
         slot[i] = 0;
       }
       g[i] = p + (long)row_of(row) * K + c * 8;
@@ -124,9 +127,40 @@ struct Operand {
   }
 };
 
+// Fragment loads of one 16-wide k-step and the MFMAs that consume them.
+template <class TL>
+struct Frags {
+  f16x8 a[TL::FM], b[TL::FN];
+  __device__ __forceinline__ void load(const u32x4 *stage, const int (&fa)[TL::FM],
+                                       const int (&fb)[TL::FN], int c) {
+#pragma unroll
+    for (int fm = 0; fm < TL::FM; ++fm) a[fm] = as_f16x8(stage[swz(fa[fm], c)]);
+#pragma unroll
+    for (int fn = 0; fn < TL::FN; ++fn) b[fn] = as_f16x8(stage[swz(fb[fn], c)]);
+  }
+  __device__ __forceinline__ void mma(f32x16 (&acc)[TL::FM][TL::FN]) const {
+#pragma unroll
+    for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < TL::FN; ++fn)
+        acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[fm], b[fn], acc[fm][fn], 0, 0, 0);
+  }
+};
+
+// Scheduling hints: interleave the next k-step's LDS reads (and the
+// register-path panel conversion) with the current k-step's MFMAs.
+__device__ __forceinline__ void interleave_reads(int nreads, int nmfma) {
+  for (int i = 0; i < nmfma; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+    if (i < nreads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+  }
+}
+
 // acc += A[rows arow(0..BM)] . B[rows brow(0..BN)]^T over K-panels [kt0, kt1).
 // The row functions must return in-range rows (results of clamped rows are
-// never stored). CVT_A / CVT_B mark an operand stored as bf16.
+// never stored). CVT_A / CVT_B mark an operand stored as bf16. Fragments are
+// double-buffered in registers: the LDS reads of k-step s+1 are in flight
+// while the MFMAs of k-step s run.
 template <class TL, bool CVT_A, bool CVT_B, class ARow, class BRow>
 __device__ __forceinline__ void mainloop(const void *A, ARow arow, const void *B, BRow brow,
                                          int K, int kt0, int kt1, u32x4 *lds,
@@ -149,6 +183,7 @@ __device__ __forceinline__ void mainloop(const void *A, ARow arow, const void *B
 #pragma unroll
   for (int fn = 0; fn < TL::FN; ++fn) fb[fn] = TL::BM + wn * TL::TN + fn * 32 + (lane & 31);
   const int hc = lane >> 5;
+  constexpr int NR = TL::FM + TL::FN, NM = TL::FM * TL::FN;
 
   oa.issue(kt0, lds);
   ob.issue(kt0, lds + TL::BM * 8);
@@ -157,6 +192,8 @@ __device__ __forceinline__ void mainloop(const void *A, ARow arow, const void *B
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
+  Frags<TL> f0, f1;
+  f0.load(lds, fa, fb, hc);
   for (int kt = kt0; kt < kt1; ++kt) {
     u32x4 *cur = lds + ((kt - kt0) & 1) * TL::STAGE;
     u32x4 *nxt = lds + (((kt - kt0) & 1) ^ 1) * TL::STAGE;
@@ -165,27 +202,23 @@ __device__ __forceinline__ void mainloop(const void *A, ARow arow, const void *B
       oa.issue(kt + 1, nxt);
       ob.issue(kt + 1, nxt + TL::BM * 8);
     }
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int c = ks * 2 + hc;
-      f16x8 af[TL::FM], bfr[TL::FN];
-#pragma unroll
-      for (int fm = 0; fm < TL::FM; ++fm) af[fm] = as_f16x8(cur[swz(fa[fm], c)]);
-#pragma unroll
-      for (int fn = 0; fn < TL::FN; ++fn) bfr[fn] = as_f16x8(cur[swz(fb[fn], c)]);
-#pragma unroll
-      for (int fm = 0; fm < TL::FM; ++fm)
-#pragma unroll
-        for (int fn = 0; fn < TL::FN; ++fn)
-          acc[fm][fn] =
-              __builtin_amdgcn_mfma_f32_32x32x16_f16(af[fm], bfr[fn], acc[fm][fn], 0, 0, 0);
-    }
+    f1.load(cur, fa, fb, 2 + hc);
+    f0.mma(acc);
+    interleave_reads(NR, NM);
+    f0.load(cur, fa, fb, 4 + hc);
+    f1.mma(acc);
+    interleave_reads(NR, NM);
+    f1.load(cur, fa, fb, 6 + hc);
+    f0.mma(acc);
+    interleave_reads(NR, NM);
     if (more) {
       oa.commit(nxt);
       ob.commit(nxt + TL::BM * 8);
     }
+    f1.mma(acc);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+    if (more) f0.load(nxt, fa, fb, hc);
   }
 }
 
@@ -200,31 +233,73 @@ __device__ __forceinline__ int acc_col(int wn, int fn, int lane) {
   return wn * TL::TN + fn * 32 + (lane & 31);
 }
 
-// Block -> (m tile, n tile, split). The hardware deals block b to XCD b % 8;
-// each XCD is given a contiguous range of logical work items, and logical
-// items run GM m-tiles fastest, then n-tiles, then splits, so the blocks an
-// XCD runs together share operand panels in its L2.
+// Work of one launch: ntiles = nm x nn output tiles. The first ndp tiles
+// (whole rounds of the 256 CUs) run one block per tile; the remaining ntail
+// tiles run nsplit blocks each over disjoint K ranges, writing fp32 partial
+// tiles that a reduction kernel sums in a fixed order. Tiles are numbered GM
+// m-tiles fastest, then n-tiles, so neighbouring tiles share operand panels.
+struct Launch {
+  int nm, nn, gm;
+  int ndp, ntail, nsplit;
+  unsigned blocks() const { return (unsigned)(ndp + ntail * nsplit); }
+};
+
 struct Work {
   int tm, tn, split;
+  int tail;  // index among the tail tiles, -1 for a whole-K tile
 };
-__device__ __forceinline__ Work block_work(int nm, int nn, int nsplit, int gm) {
-  const int nb = nm * nn * nsplit;
-  const int b = blockIdx.x;
-  const int q = nb / 8, rem = nb % 8, x = b % 8, k = b / 8;
-  const int L = (x < rem ? x * (q + 1) : rem * (q + 1) + (x - rem) * q) + k;
-  const int per_split = nm * nn;
-  const int s = L / per_split, l2 = L % per_split;
+
+__device__ __forceinline__ void tile_coords(int L, int nm, int nn, int gm, int &tm, int &tn) {
   const int g = min(gm, nm);
-  const int grp = l2 / (g * nn);
+  const int grp = L / (g * nn);
   const int gsz = min(g, nm - grp * g);
-  const int in = l2 - grp * g * nn;
-  return {grp * g + in % gsz, in / gsz, s};
+  const int in = L - grp * g * nn;
+  tm = grp * g + in % gsz;
+  tn = in / gsz;
 }
 
-struct Launch {
-  int nm, nn, nsplit, gm;
-  unsigned blocks() const { return (unsigned)(nm * nn * nsplit); }
-};
+// The hardware deals block b to XCD b % 8; each XCD is given a contiguous
+// range of whole-K tiles, so the blocks it runs together share panels in
+// its L2.
+__device__ __forceinline__ Work block_work(const Launch &ln) {
+  const int b = blockIdx.x;
+  Work w;
+  int L;
+  if (b < ln.ndp) {
+    const int q = ln.ndp / 8, rem = ln.ndp % 8, x = b % 8, k = b / 8;
+    L = (x < rem ? x * (q + 1) : rem * (q + 1) + (x - rem) * q) + k;
+    w.split = 0;
+    w.tail = -1;
+  } else {
+    const int bt = b - ln.ndp;
+    w.tail = bt / ln.nsplit;
+    w.split = bt % ln.nsplit;
+    L = ln.ndp + w.tail;
+  }
+  tile_coords(L, ln.nm, ln.nn, ln.gm, w.tm, w.tn);
+  return w;
+}
+
+constexpr int kMaxSplit = 8;
+constexpr int kTileElems = 256 * 256;
+
+// Whole rounds data-parallel, the tail split so that it fills one round.
+Launch plan_launch(int nm, int nn, int gm, int nk) {
+  Launch ln{nm, nn, gm, 0, 0, 1};
+  const int tiles = nm * nn;
+  const int tail = tiles % 256;
+  ln.ndp = tiles - tail;
+  ln.ntail = tail;
+  if (tail > 0) {
+    int s = std::min(256 / tail, std::min(kMaxSplit, std::max(1, nk / 4)));
+    ln.nsplit = std::max(1, s);
+    if (ln.nsplit == 1) {  // nothing to split: all tiles whole-K
+      ln.ndp = tiles;
+      ln.ntail = 0;
+    }
+  }
+  return ln;
+}
 
 // K-panel range of split s of nsplit over nk panels.
 __device__ __forceinline__ void split_range(int nk, int nsplit, int s, int &k0, int &k1) {
@@ -232,34 +307,31 @@ __device__ __forceinline__ void split_range(int nk, int nsplit, int s, int &k0, 
   k1 = (int)((long)nk * (s + 1) / nsplit);
 }
 
-// Raw fp32 partial tile of split s: part[s][row][col] (rows x ncols).
+// Raw fp32 partial tile: part[(tail * nsplit + split)][256][256], local
+// coordinates (rows / columns past the matrix edge hold unused values).
 template <class TL>
 __device__ __forceinline__ void store_partial(const f32x16 (&acc)[TL::FM][TL::FN], float *part,
-                                              int s, int rows, int ncols, int m0, int n0) {
+                                              const Launch &ln, const Work &wk) {
+  static_assert(TL::BM == 256 && TL::BN == 256, "partial tiles are 256 x 256");
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w / TL::WN, wn = w % TL::WN;
-  float *p = part + (long)s * rows * ncols;
+  float *p = part + ((long)wk.tail * ln.nsplit + wk.split) * kTileElems;
 #pragma unroll
   for (int fn = 0; fn < TL::FN; ++fn) {
-    const int col = n0 + acc_col<TL>(wn, fn, lane);
-    if (col >= ncols) continue;
+    const int col = acc_col<TL>(wn, fn, lane);
 #pragma unroll
     for (int fm = 0; fm < TL::FM; ++fm)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + acc_row<TL>(wm, fm, r, lane);
-        if (row < rows) p[(long)row * ncols + col] = acc[fm][fn][r];
-      }
+      for (int r = 0; r < 16; ++r) p[acc_row<TL>(wm, fm, r, lane) * 256 + col] = acc[fm][fn][r];
   }
 }
 
-// Split count for a GEMM of `tiles` output tiles over nk K-panels: enough
-// blocks for one round on the 256 CUs, at least 4 panels per split.
-int choose_split(int tiles, int nk, int max_split) {
-  if (tiles >= 192) return 1;
-  int s = (256 + tiles - 1) / tiles;
-  s = std::min(s, std::max(1, nk / 4));
-  return std::max(1, std::min(s, max_split));
+// Sum of the partials of local element e (row * 256 + col) of tail tile i.
+__device__ __forceinline__ float sum_partials(const float *part, const Launch &ln, int i, int e) {
+  const float *p = part + (long)i * ln.nsplit * kTileElems + e;
+  float v = 0.f;
+  for (int s = 0; s < ln.nsplit; ++s) v += p[(long)s * kTileElems];
+  return v;
 }
 
 __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.f + __expf(-g)) * u; }
@@ -272,16 +344,17 @@ __global__ __launch_bounds__(NT) void k_gemm_residual(const f16 *__restrict__ A,
                                                       float *__restrict__ x,
                                                       float *__restrict__ part) {
   __shared__ u32x4 lds[2 * TL::STAGE];
-  const Work wk = block_work(ln.nm, ln.nn, ln.nsplit, ln.gm);
+  const Work wk = block_work(ln);
   const int m0 = wk.tm * TL::BM, n0 = wk.tn * TL::BN;
-  int k0, k1;
-  split_range(K / BK, ln.nsplit, wk.split, k0, k1);
+  const bool split = wk.tail >= 0;
+  int k0 = 0, k1 = K / BK;
+  if (split) split_range(K / BK, ln.nsplit, wk.split, k0, k1);
   f32x16 acc[TL::FM][TL::FN];
   mainloop<TL, false, true>(
       A, [=](int r) { return min(m0 + r, rows - 1); }, W,
       [=](int r) { return min(n0 + r, N - 1); }, K, k0, k1, lds, acc);
-  if (ln.nsplit > 1) {
-    store_partial<TL>(acc, part, wk.split, rows, N, m0, n0);
+  if (split) {
+    store_partial<TL>(acc, part, ln, wk);
     return;
   }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -300,23 +373,23 @@ __global__ __launch_bounds__(NT) void k_gemm_residual(const f16 *__restrict__ A,
   }
 }
 
-// x[row][col] += sum_s part[s][row][col], s in order.
+// Tail tiles: x += sum of the partials. Block (tail tile, 256-element slab).
 __global__ __launch_bounds__(256) void k_reduce_residual(const float *__restrict__ part,
-                                                         int nsplit, long n,
+                                                         Launch ln, int rows, int N,
                                                          float *__restrict__ x) {
-  const long i = (long)blockIdx.x * 256 + threadIdx.x;
-  if (i >= n) return;
-  float v = 0.f;
-  for (int s = 0; s < nsplit; ++s) v += part[s * n + i];
-  x[i] += v;
+  const int i = blockIdx.x / 256, e = (blockIdx.x % 256) * 256 + threadIdx.x;
+  int tm, tn;
+  tile_coords(ln.ndp + i, ln.nm, ln.nn, ln.gm, tm, tn);
+  const int row = tm * 256 + e / 256, col = tn * 256 + e % 256;
+  if (row >= rows || col >= N) return;
+  x[(long)row * N + col] += sum_partials(part, ln, i, e);
 }
 
 // ------------------------------------------------------------------- SwiGLU
 // Output column tile o0 .. o0+128 of the FFN hidden. Its 256 B rows are laid
 // out per wave column: wave column wn takes gate rows o0+64wn .. +63 then the
 // matching up rows, so MFMA blocks fn and fn+2 hold gate and up of the same
-// output columns. Split partials keep that B-row order: partial column
-// 256 tn + lr holds B row brow(lr).
+// output columns (partial tiles keep that column order).
 template <class TL>
 __global__ __launch_bounds__(NT) void k_gemm_swiglu(const f16 *__restrict__ A,
                                                     const bf16 *__restrict__ W, int rows, int F,
@@ -324,10 +397,11 @@ __global__ __launch_bounds__(NT) void k_gemm_swiglu(const f16 *__restrict__ A,
                                                     float *__restrict__ part) {
   static_assert(TL::WN == 2 && TL::TN == 128 && TL::BN == 256, "gate/up pairing");
   __shared__ u32x4 lds[2 * TL::STAGE];
-  const Work wk = block_work(ln.nm, ln.nn, ln.nsplit, ln.gm);
+  const Work wk = block_work(ln);
   const int m0 = wk.tm * TL::BM, o0 = wk.tn * 128;
-  int k0, k1;
-  split_range(K / BK, ln.nsplit, wk.split, k0, k1);
+  const bool split = wk.tail >= 0;
+  int k0 = 0, k1 = K / BK;
+  if (split) split_range(K / BK, ln.nsplit, wk.split, k0, k1);
   f32x16 acc[TL::FM][TL::FN];
   mainloop<TL, false, true>(
       A, [=](int r) { return min(m0 + r, rows - 1); }, W,
@@ -337,8 +411,8 @@ __global__ __launch_bounds__(NT) void k_gemm_swiglu(const f16 *__restrict__ A,
         return q < 64 ? oc : F + oc;
       },
       K, k0, k1, lds, acc);
-  if (ln.nsplit > 1) {
-    store_partial<TL>(acc, part, wk.split, rows, ln.nn * 256, m0, wk.tn * 256);
+  if (split) {
+    store_partial<TL>(acc, part, ln, wk);
     return;
   }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -358,22 +432,21 @@ __global__ __launch_bounds__(NT) void k_gemm_swiglu(const f16 *__restrict__ A,
   }
 }
 
-// h[row][o] = silu(gate) * up from the summed partials (B-row order above).
+// Tail tiles: h = silu(gate) * up from the summed partials. Block (tail tile,
+// half of its 256 rows); thread -> (row, output column oc < 128).
 __global__ __launch_bounds__(256) void k_reduce_swiglu(const float *__restrict__ part,
-                                                       int nsplit, int rows, int F, int ncols,
+                                                       Launch ln, int rows, int F,
                                                        f16 *__restrict__ h) {
-  const long i = (long)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (long)rows * F) return;
-  const int row = (int)(i / F), o = (int)(i % F);
-  const int tn = o / 128, within = o % 128, wn = within / 64, q = within % 64;
-  const long cg = (long)tn * 256 + wn * 128 + q, cu = cg + 64;
-  const long n = (long)rows * ncols;
-  float g = 0.f, u = 0.f;
-  for (int s = 0; s < nsplit; ++s) {
-    g += part[s * n + (long)row * ncols + cg];
-    u += part[s * n + (long)row * ncols + cu];
-  }
-  h[i] = static_cast<f16>(silu_mul(g, u));
+  const int i = blockIdx.x / 128, e = (blockIdx.x % 128) * 256 + threadIdx.x;
+  int tm, tn;
+  tile_coords(ln.ndp + i, ln.nm, ln.nn, ln.gm, tm, tn);
+  const int lr = e / 128, oc = e % 128;
+  const int row = tm * 256 + lr, o = tn * 128 + oc;
+  if (row >= rows || o >= F) return;
+  const int cg = (oc / 64) * 128 + oc % 64;
+  const float g = sum_partials(part, ln, i, lr * 256 + cg);
+  const float u = sum_partials(part, ln, i, lr * 256 + cg + 64);
+  h[(long)row * F + o] = static_cast<f16>(silu_mul(g, u));
 }
 
 // ------------------------------------------------- QKV + rotary + KV caches
@@ -398,9 +471,12 @@ __device__ __forceinline__ void qkv_store(const QKVOut<f16> &o, int n_heads, int
     k[d] = static_cast<f16>(x1);
     k[d + 64] = static_cast<f16>(x2);
   } else {
+    // Values go to the Vt cache at the attention kernel's interleaved
+    // position: within each aligned group of 16, quarters 1 and 2 swap.
     f16 *vt = o.vt + (long)(slot - n_heads - n_kv) * 128 * o.kv_npos;
-    vt[(long)d * o.kv_npos + row] = static_cast<f16>(x1);
-    vt[(long)(d + 64) * o.kv_npos + row] = static_cast<f16>(x2);
+    const int pp = (row & ~12) | ((row & 4) << 1) | ((row & 8) >> 1);
+    vt[(long)d * o.kv_npos + pp] = static_cast<f16>(x1);
+    vt[(long)(d + 64) * o.kv_npos + pp] = static_cast<f16>(x2);
   }
 }
 
@@ -411,17 +487,18 @@ __global__ __launch_bounds__(NT) void k_gemm_qkv(const f16 *__restrict__ A,
                                                  float *__restrict__ part) {
   static_assert(TL::WN == 2 && TL::TN == 128 && TL::BN == 256, "one head per wave column");
   __shared__ u32x4 lds[2 * TL::STAGE];
-  const Work wk = block_work(ln.nm, ln.nn, ln.nsplit, ln.gm);
+  const Work wk = block_work(ln);
   const int nslots = n_heads + 2 * n_kv, nrows = nslots * 128;
   const int m0 = wk.tm * TL::BM, n0 = wk.tn * 256;
-  int k0, k1;
-  split_range(K / BK, ln.nsplit, wk.split, k0, k1);
+  const bool split = wk.tail >= 0;
+  int k0 = 0, k1 = K / BK;
+  if (split) split_range(K / BK, ln.nsplit, wk.split, k0, k1);
   f32x16 acc[TL::FM][TL::FN];
   mainloop<TL, false, true>(
       A, [=](int r) { return min(m0 + r, rows - 1); }, W,
       [=](int r) { return min(n0 + r, nrows - 1); }, K, k0, k1, lds, acc);
-  if (ln.nsplit > 1) {
-    store_partial<TL>(acc, part, wk.split, rows, nrows, m0, n0);
+  if (split) {
+    store_partial<TL>(acc, part, ln, wk);
     return;
   }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -441,24 +518,20 @@ __global__ __launch_bounds__(NT) void k_gemm_qkv(const f16 *__restrict__ A,
     }
 }
 
-// Rotary + cache scatter from the summed partials; one thread per
-// (row, head slot, d < 64).
-__global__ __launch_bounds__(256) void k_reduce_qkv(const float *__restrict__ part, int nsplit,
+// Tail tiles: rotary + cache scatter from the summed partials. Block (tail
+// tile, half of its 256 rows); thread -> (row, head of the pair, d < 64).
+__global__ __launch_bounds__(256) void k_reduce_qkv(const float *__restrict__ part, Launch ln,
                                                     int rows, int n_heads, int n_kv,
                                                     QKVOut<f16> o) {
-  const int nslots = n_heads + 2 * n_kv, ncols = nslots * 128;
-  const long i = (long)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (long)rows * nslots * 64) return;
-  const int row = (int)(i / (nslots * 64));
-  const int rem = (int)(i % (nslots * 64));
-  const int slot = rem / 64, d = rem % 64;
-  const long n = (long)rows * ncols;
-  const long c = (long)row * ncols + slot * 128 + d;
-  float x1 = 0.f, x2 = 0.f;
-  for (int s = 0; s < nsplit; ++s) {
-    x1 += part[s * n + c];
-    x2 += part[s * n + c + 64];
-  }
+  const int i = blockIdx.x / 128, e = (blockIdx.x % 128) * 256 + threadIdx.x;
+  int tm, tn;
+  tile_coords(ln.ndp + i, ln.nm, ln.nn, ln.gm, tm, tn);
+  const int lr = e / 128, hh = (e % 128) / 64, d = e % 64;
+  const int row = tm * 256 + lr, slot = tn * 2 + hh;
+  if (row >= rows || slot >= n_heads + 2 * n_kv) return;
+  const int c = hh * 128 + d;
+  const float x1 = sum_partials(part, ln, i, lr * 256 + c);
+  const float x2 = sum_partials(part, ln, i, lr * 256 + c + 64);
   qkv_store(o, n_heads, n_kv, slot, row, d, x1, x2);
 }
 
@@ -479,7 +552,7 @@ __global__ __launch_bounds__(NT) void k_gemm_lmhead(const f16 *__restrict__ Hn,
                                                     float *__restrict__ tgt_logit) {
   __shared__ u32x4 lds[2 * TL::STAGE];
   __shared__ float red[TL::WM][TL::BN];
-  const Work wk = block_work(ln.nm, ln.nn, 1, ln.gm);
+  const Work wk = block_work(ln);
   const int m0 = wk.tm * TL::BM, n0 = wk.tn * TL::BN;
   f32x16 acc[TL::FM][TL::FN];
   mainloop<TL, true, false>(
@@ -549,27 +622,21 @@ __global__ __launch_bounds__(NT) void k_gemm_lmhead(const f16 *__restrict__ Hn,
   }
 }
 
-constexpr int kMaxSplit = 8;
-
 }  // namespace
 
 size_t gemm_split_floats(int rows, int N, int K) {
-  const int nm = (rows + TileStd::BM - 1) / TileStd::BM, nn = (N + TileStd::BN - 1) / TileStd::BN;
-  const int s = choose_split(nm * nn, K / BK, kMaxSplit);
-  return s > 1 ? (size_t)s * rows * nn * TileStd::BN : 0;
+  const Launch ln = plan_launch((rows + 255) / 256, (N + 255) / 256, 8, K / BK);
+  return (size_t)ln.ntail * ln.nsplit * kTileElems;
 }
 
 hipError_t gemm_residual(const f16 *A, const bf16 *W, int rows, int N, int K, float *x,
                          float *part, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
-  Launch ln{(rows + TL::BM - 1) / TL::BM, (N + TL::BN - 1) / TL::BN, 1, 8};
-  ln.nsplit = choose_split(ln.nm * ln.nn, K / BK, kMaxSplit);
+  const Launch ln = plan_launch((rows + TL::BM - 1) / TL::BM, (N + TL::BN - 1) / TL::BN, 8, K / BK);
   k_gemm_residual<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, N, K, ln, x, part);
-  if (ln.nsplit > 1) {
-    const long n = (long)rows * N;
-    k_reduce_residual<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(part, ln.nsplit, n, x);
-  }
+  if (ln.ntail > 0)
+    k_reduce_residual<<<ln.ntail * 256, 256, 0, s>>>(part, ln, rows, N, x);
   return hipGetLastError();
 }
 
@@ -577,14 +644,9 @@ hipError_t gemm_swiglu(const f16 *A, const bf16 *W, int rows, int F, int K, f16 
                        hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
-  Launch ln{(rows + TL::BM - 1) / TL::BM, (F + 127) / 128, 1, 8};
-  ln.nsplit = choose_split(ln.nm * ln.nn, K / BK, kMaxSplit);
+  const Launch ln = plan_launch((rows + TL::BM - 1) / TL::BM, (F + 127) / 128, 8, K / BK);
   k_gemm_swiglu<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, F, K, ln, h, part);
-  if (ln.nsplit > 1) {
-    const long n = (long)rows * F;
-    k_reduce_swiglu<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(part, ln.nsplit, rows, F,
-                                                                 ln.nn * 256, h);
-  }
+  if (ln.ntail > 0) k_reduce_swiglu<<<ln.ntail * 128, 256, 0, s>>>(part, ln, rows, F, h);
   return hipGetLastError();
 }
 
@@ -593,14 +655,10 @@ hipError_t gemm_qkv_rope(const f16 *A, const bf16 *W, int rows, int K, int n_hea
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
   const int nslots = n_heads + 2 * n_kv;
-  Launch ln{(rows + TL::BM - 1) / TL::BM, (nslots + 1) / 2, 1, 8};
-  ln.nsplit = choose_split(ln.nm * ln.nn, K / BK, kMaxSplit);
+  const Launch ln = plan_launch((rows + TL::BM - 1) / TL::BM, (nslots + 1) / 2, 8, K / BK);
   k_gemm_qkv<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, K, n_heads, n_kv, ln, out, part);
-  if (ln.nsplit > 1) {
-    const long n = (long)rows * nslots * 64;
-    k_reduce_qkv<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(part, ln.nsplit, rows, n_heads,
-                                                              n_kv, out);
-  }
+  if (ln.ntail > 0)
+    k_reduce_qkv<<<ln.ntail * 128, 256, 0, s>>>(part, ln, rows, n_heads, n_kv, out);
   return hipGetLastError();
 }
 
@@ -610,8 +668,11 @@ hipError_t gemm_lmhead(const f16 *A, const bf16 *W, int rows, int vocab, int K,
                        const int32_t *lm_tgt, float2 *part, float *tgt_logit, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
-  // Token tiles fastest: the blocks sharing a vocabulary tile run together.
-  Launch ln{lmhead_chunks(vocab), (rows + TL::BN - 1) / TL::BN, 1, 1};
+  // Token tiles fastest (GM = 1): the blocks sharing a vocabulary tile run
+  // together. No K split (every block writes whole-vocabulary-tile LSE
+  // partials).
+  const int nm = lmhead_chunks(vocab), nn = (rows + TL::BN - 1) / TL::BN;
+  const Launch ln{nm, nn, 1, nm * nn, 0, 1};
   k_gemm_lmhead<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, vocab, K, ln, lm_tgt, part,
                                                tgt_logit);
   return hipGetLastError();

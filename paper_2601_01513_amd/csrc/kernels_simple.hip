@@ -164,7 +164,7 @@ __device__ __forceinline__ void attend_keys(const T *kc, const T *vtc, int npos,
 
 template <typename T>
 __global__ __launch_bounds__(64) void k_simple_attn(SimpleAttnArgs a) {
-  const int t = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+  const int t = a.t0 + blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
   const int G = a.n_heads / a.n_kv, kv = h / G, hd = a.hd;
   const T *q = (const T *)a.q + ((long)t * a.n_heads + h) * hd;
   float qr[4], acc[4] = {0.f, 0.f, 0.f, 0.f};
@@ -187,8 +187,8 @@ __global__ __launch_bounds__(64) void k_simple_attn(SimpleAttnArgs a) {
 
 template <typename T>
 hipError_t simple_attn(const SimpleAttnArgs &a, hipStream_t s) {
-  if (a.T == 0) return hipSuccess;
-  k_simple_attn<T><<<dim3(a.T, a.n_heads), 64, 0, s>>>(a);
+  if (a.T <= a.t0) return hipSuccess;
+  k_simple_attn<T><<<dim3(a.T - a.t0, a.n_heads), 64, 0, s>>>(a);
   return hipGetLastError();
 }
 

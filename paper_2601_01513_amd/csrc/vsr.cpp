@@ -30,7 +30,8 @@ struct Split {
 };
 Split cascade_split(int T, int P, int n_heads, int n_kv) {
   const int G = n_heads / n_kv;
-  const int qtiles = (T * G + 127) / 128 * n_kv;
+  const int qt = attn_query_tile();
+  const int qtiles = (T * G + qt - 1) / qt * n_kv;
   int n = std::max(1, (512 + qtiles - 1) / qtiles);
   n = std::min(n, std::max(1, P / 256));
   n = std::min(n, 32);
@@ -264,6 +265,10 @@ extern "C" int vsr_create(const vsr_config *cfg, void *workspace, size_t ws_byte
   c->device = dev;
   e = launch_rope_table(c->at<float2>(plan.rope), plan.rope_npos, cfg->head_dim, cfg->rope_base,
                         c->stream);
+  // Cache slots past the written positions are read (and masked) by whole
+  // key tiles: start them at zero so they are finite.
+  if (e == hipSuccess)
+    e = hipMemsetAsync(c->ws + plan.kc, 0, plan.part_acc - plan.kc, c->stream);
   if (e != hipSuccess) {
     g_create_error = std::string("HIP error in rope table: ") + hipGetErrorString(e);
     delete c;
@@ -345,8 +350,14 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       STAGE(c, K_QKV, "qkv projection",
             simple_qkv_rope<TA>(xn, wqkv, rows, d, Hq, Hkv, hd, qo, s));
     }
+    // The prefix's last layer only feeds the last prefix row (the hidden state
+    // that predicts candidate token 0): its keys/values are needed for every
+    // row, its attention output, projections and FFN for row P-1 only.
+    const bool tail = mode == 0 && l == cf.n_layers - 1;
+    const int r0 = tail ? rows - 1 : 0, nr = tail ? 1 : rows;
     if constexpr (kMfma) {
       AttnArgs a{};
+      a.t0 = r0;
       a.q = q;
       a.k = kc;
       a.vt = vtc;
@@ -385,26 +396,29 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       a.n_heads = Hq;
       a.n_kv = Hkv;
       a.hd = hd;
+      a.t0 = r0;
       a.mode = mode;
       a.out = attn;
       STAGE(c, K_ATTN, "attention", simple_attn<TA>(a, s));
     }
+    const TA *attn_r = attn + (size_t)r0 * Hq * hd;
+    float *x_r = x + (size_t)r0 * d;
     if constexpr (kMfma) {
       STAGE(c, K_OPROJ, "output projection",
-            gemm_residual(attn, wo, rows, d, Hq * hd, x, gpart, s));
+            gemm_residual(attn_r, wo, nr, d, Hq * hd, x_r, gpart, s));
     } else {
       STAGE(c, K_OPROJ, "output projection",
-            simple_residual<TA>(attn, wo, rows, d, Hq * hd, x, s));
+            simple_residual<TA>(attn_r, wo, nr, d, Hq * hd, x_r, s));
     }
     STAGE(c, K_NORM, "ffn norm",
-             launch_rmsnorm<TW, TA>(x, static_cast<const TW *>(c->ffn_norm[l]), rows, d,
-                                    cf.rms_eps, xn, s));
+          launch_rmsnorm<TW, TA>(x_r, static_cast<const TW *>(c->ffn_norm[l]), nr, d,
+                                 cf.rms_eps, xn, s));
     if constexpr (kMfma) {
-      STAGE(c, K_GATEUP, "gate/up projection", gemm_swiglu(xn, wgu, rows, F, d, h, gpart, s));
-      STAGE(c, K_DOWN, "down projection", gemm_residual(h, wdown, rows, d, F, x, gpart, s));
+      STAGE(c, K_GATEUP, "gate/up projection", gemm_swiglu(xn, wgu, nr, F, d, h, gpart, s));
+      STAGE(c, K_DOWN, "down projection", gemm_residual(h, wdown, nr, d, F, x_r, gpart, s));
     } else {
-      STAGE(c, K_GATEUP, "gate/up projection", simple_swiglu<TA>(xn, wgu, rows, F, d, h, s));
-      STAGE(c, K_DOWN, "down projection", simple_residual<TA>(h, wdown, rows, d, F, x, s));
+      STAGE(c, K_GATEUP, "gate/up projection", simple_swiglu<TA>(xn, wgu, nr, F, d, h, s));
+      STAGE(c, K_DOWN, "down projection", simple_residual<TA>(h, wdown, nr, d, F, x_r, s));
     }
   }
   return VSR_OK;

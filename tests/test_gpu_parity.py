@@ -49,7 +49,7 @@ def run_gpu(wl, cand_ids=None, cand_len=None, verifier=None):
     return lp.cpu().numpy(), sc.cpu().numpy(), int(am.cpu()[0]), v
 
 
-def run_oracle(wl, dtype=np.float64, cand_ids=None, cand_len=None):
+def run_oracle(wl, dtype=np.float64, cand_ids=None, cand_len=None, cands=None):
     hw = W.host_weights(wl.weights, lazy=True)
     vis = W.to_host_f32(wl.visual)
     cids = wl.cand_ids if cand_ids is None else cand_ids
@@ -61,7 +61,7 @@ def run_oracle(wl, dtype=np.float64, cand_ids=None, cand_len=None):
         if (layer + 1) % every == 0:
             _say(f"  oracle layer {layer + 1}/{wl.cfg.n_layers} at {time.time() - t0:.0f}s")
     return oracle.score_shared_prefix(wl.cfg, hw, vis, wl.prefix_ids, cids, lens, dtype=dtype,
-                                      progress=progress)
+                                      cands=cands, progress=progress)
 
 
 def check(cfg, gpu, ora, lens):
@@ -181,3 +181,46 @@ def test_full_width_two_layers(cfg):
     ora = run_oracle(wl, dtype=np.float32)
     _say(f"  oracle done in {time.time() - t0:.1f}s")
     check(cfg2, gpu, ora, wl.cand_len)
+
+
+def check_sampled(cfg, gpu, ora, lens, cands):
+    """Element-wise check of the sampled candidates; properties for all."""
+    lp_g, sc_g, am_g = gpu[:3]
+    lp_o, sc_o, _ = ora
+    cmax = lp_g.shape[1]
+    valid = np.arange(cmax)[None, :] < np.asarray(lens)[:, None]
+    assert np.all(np.isfinite(lp_g)) and np.all(lp_g[~valid] == 0.0)
+    assert np.all(lp_g[valid] < 0.0)
+    np.testing.assert_allclose(sc_g, lp_g.sum(axis=1), rtol=1e-5, atol=1e-4)
+    assert am_g == int(np.argmax(sc_g))
+    for m in cands:
+        err = np.abs(lp_g[m, :lens[m]] - lp_o[m, :lens[m]])
+        _say(f"  candidate {m}: max |dlp| = {err.max():.3e}, score gpu {sc_g[m]:.3f} "
+             f"oracle {sc_o[m]:.3f}")
+        assert err.max() <= 2e-2
+        assert abs(sc_g[m] - sc_o[m]) <= 1e-2 * abs(sc_o[m])
+
+
+@pytest.mark.timeout(900)
+def test_full_depth_7b_sampled():
+    """The 7B-class workload at full depth and size; the oracle (float32)
+    scores two of the eight candidates."""
+    wl = _case(W.B7, 1)
+    gpu = run_gpu(wl)
+    cands = [0, 5]
+    ora = run_oracle(wl, dtype=np.float32, cands=cands)
+    check_sampled(wl.cfg, gpu, ora, wl.cand_len, cands)
+
+
+@pytest.mark.timeout(900)
+def test_full_depth_32b_short_prefix_sampled():
+    """All 64 layers of the 32B-class workload (depth is what amplifies
+    rounding) on a 1024-row prefix; the oracle (float32) scores two of four
+    candidates."""
+    cfg = W.B32.replace(name="32B-class bf16 P1024 M4x128 (64 layers)", n_prefix=1024,
+                        n_visual=512, n_cands=4)
+    wl = _case(cfg, 0)
+    gpu = run_gpu(wl)
+    cands = [0, 3]
+    ora = run_oracle(wl, dtype=np.float32, cands=cands)
+    check_sampled(cfg, gpu, ora, wl.cand_len, cands)
