@@ -69,6 +69,16 @@ typedef struct vsr_config {
   int32_t max_prefix;   /* largest P = n_visual + n_text passed to prefill */
   int32_t max_cands;    /* largest M passed to score (<= VSR_MAX_CANDS)    */
   int32_t max_cand_len; /* largest Cmax passed to score                    */
+  /* VSR_BF16 arithmetic: weights stay bf16 and are converted exactly to fp16
+   * operands; activations are fp16 with fp32 accumulation. The first
+   * split_layers decoder layers (0 <= split_layers <= n_layers) are precise
+   * layers: every GEMM activation operand is carried as an fp16 value plus
+   * its fp16 remainder (about 22 significant bits, twice the matrix-core
+   * work), and attention carries queries, keys, values and probabilities the
+   * same way (three products each, plus remainder caches of those layers in
+   * the workspace): the earliest layers set the rounding that a deep decoder
+   * amplifies. Ignored by VSR_F32 contexts (fp32 throughout). */
+  int32_t split_layers;
 } vsr_config;
 
 #define VSR_MAX_CANDS 256

@@ -36,7 +36,7 @@ class VsrConfig(ctypes.Structure):
                 ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float),
                 ("rope_base", ctypes.c_float), ("dtype", ctypes.c_int32),
                 ("max_prefix", ctypes.c_int32), ("max_cands", ctypes.c_int32),
-                ("max_cand_len", ctypes.c_int32)]
+                ("max_cand_len", ctypes.c_int32), ("split_layers", ctypes.c_int32)]
 
 
 _PP = ctypes.POINTER(ctypes.c_void_p)
@@ -93,13 +93,23 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     return lib
 
 
+def default_split_layers(n_layers: int) -> int:
+    """Precise leading layers for a decoder of this depth: one up to 63 layers,
+    two at 64 (rounding amplification grows with depth)."""
+    return min(n_layers, max(1, n_layers // 32))
+
+
 def make_config(cfg, max_prefix: Optional[int] = None, max_cands: Optional[int] = None,
-                max_cand_len: Optional[int] = None) -> VsrConfig:
-    """vsr_config from a workload.VerifierConfig (maxima default to its sizes)."""
+                max_cand_len: Optional[int] = None,
+                split_layers: Optional[int] = None) -> VsrConfig:
+    """vsr_config from a workload.VerifierConfig (maxima default to its sizes;
+    split_layers defaults to default_split_layers(n_layers))."""
+    if split_layers is None:
+        split_layers = default_split_layers(cfg.n_layers)
     return VsrConfig(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim,
                      cfg.d_ff, cfg.vocab, cfg.rms_eps, cfg.rope_base, cfg.dtype,
                      max_prefix or cfg.n_prefix, max_cands or cfg.n_cands,
-                     max_cand_len or cfg.cand_len)
+                     max_cand_len or cfg.cand_len, split_layers)
 
 
 def workspace_size(c: VsrConfig) -> int:
@@ -114,12 +124,12 @@ class Verifier:
     """One vsr context: workspace, borrowed weights and the current prefix."""
 
     def __init__(self, cfg, weights: Dict, device="cuda", stream=None,
-                 max_prefix=None, max_cands=None, max_cand_len=None):
+                 max_prefix=None, max_cands=None, max_cand_len=None, split_layers=None):
         import torch
         self._torch = torch
         self.lib = load_library()
         self.cfg = cfg
-        self.c = make_config(cfg, max_prefix, max_cands, max_cand_len)
+        self.c = make_config(cfg, max_prefix, max_cands, max_cand_len, split_layers)
         size = self.lib.vsr_workspace_size(ctypes.byref(self.c))
         if size == 0:
             raise VsrError(VSR_EINVAL, "unsupported config")

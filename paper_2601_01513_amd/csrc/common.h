@@ -64,10 +64,11 @@ template <typename T>
 hipError_t launch_embed_rows(const int32_t *ids, int rows, const T *embed, int d, float *x,
                              hipStream_t s);
 
-// y[r] = TA(x[r] / sqrt(mean(x[r]^2) + eps) * g) for rows r < rows.
+// y[r] = TA(x[r] / sqrt(mean(x[r]^2) + eps) * g) for rows r < rows; with
+// split = 2 the rows of y are [hi | lo] (2d wide).
 template <typename TW, typename TA>
 hipError_t launch_rmsnorm(const float *x, const TW *g, int rows, int d, float eps, TA *y,
-                          hipStream_t s);
+                          int split, hipStream_t s);
 // LM-head inputs of a score call: y[t] = norm(h_last) if t is the first row
 // of its candidate, else norm(x[t - 1]).
 template <typename TW, typename TA>
@@ -98,6 +99,9 @@ struct QKVOut {
   int kv_npos;     // position stride of the caches (their capacity)
   const int32_t *row_pos;  // rotary position of each row (NULL: position = row)
   const float2 *rope;      // rotary table [npos][hd/2]
+  // Precise layers (MFMA path): the fp16 remainders x - fp16(x) of q, k, v in
+  // planes laid out like q, k, vt (NULL: not written).
+  T *q_lo = nullptr, *k_lo = nullptr, *vt_lo = nullptr;
 };
 
 // ------------------------------------------------------------ MFMA path
@@ -105,14 +109,18 @@ struct QKVOut {
 // weights (converted to fp16 on their way into LDS), fp32 accumulation.
 // Shapes with few output tiles split K; `part` is fp32 scratch of
 // gemm_split_floats(rows, N, K) floats (N = B rows) for the partials.
+// asplit = 2: each A row is [hi | lo] (2K wide), an fp16 value and its fp16
+// remainder, multiplied by the same W (about 22-bit operands); outputs that
+// feed a split GEMM are written the same way.
 size_t gemm_split_floats(int rows, int N, int K);
-hipError_t gemm_qkv_rope(const f16 *A, const bf16 *W, int rows, int K, int n_heads,
+hipError_t gemm_qkv_rope(const f16 *A, const bf16 *W, int rows, int K, int asplit, int n_heads,
                          int n_kv, const QKVOut<f16> &out, float *part, hipStream_t s);
 // x[rows][N] += A . W^T (residual stream, fp32).
-hipError_t gemm_residual(const f16 *A, const bf16 *W, int rows, int N, int K, float *x,
-                         float *part, hipStream_t s);
-// h[rows][F] = silu(A . Wg^T) * (A . Wu^T), W = [Wg; Wu] ([2F][K]).
-hipError_t gemm_swiglu(const f16 *A, const bf16 *W, int rows, int F, int K, f16 *h,
+hipError_t gemm_residual(const f16 *A, const bf16 *W, int rows, int N, int K, int asplit,
+                         float *x, float *part, hipStream_t s);
+// h[rows][F] = silu(A . Wg^T) * (A . Wu^T), W = [Wg; Wu] ([2F][K]); h rows are
+// [hi | lo] (2F wide) when asplit == 2.
+hipError_t gemm_swiglu(const f16 *A, const bf16 *W, int rows, int F, int K, int asplit, f16 *h,
                        float *part, hipStream_t s);
 // LM head: per (vocab chunk c, row t): part[c][t] = (max, sum exp(l - max)) over
 // the chunk's logits l = W[v] . A[t]; tgt_logit[t] = logit of lm_tgt[t].
@@ -141,13 +149,18 @@ struct AttnArgs {
   int n_heads, n_kv;
   int nchunks;          // mode 1: prefix split (partials when > 1)
   int chunk;            // prefix keys per split
-  f16 *out;             // [T][n_heads][hd] when nchunks == 1
+  f16 *out;             // [T][out_split][n_heads][hd] when nchunks == 1 (or merged)
+  int out_split;        // 2: [hi | lo] rows for a split output projection
   float *part_acc;      // [nchunks][n_kv][T*G][hd]
   float2 *part_ml;      // [nchunks][n_kv][T*G]
+  // Precise layers: remainder planes of q, k, vt (and bk, bvt), same layouts.
+  const f16 *q_lo, *k_lo, *vt_lo, *bk_lo, *bvt_lo;
 };
 int attn_query_tile();  // stacked query rows per attention block
-hipError_t attn_prefill(const AttnArgs &a, hipStream_t s);
-hipError_t attn_cascade(const AttnArgs &a, hipStream_t s);
+// precise = true: q/k/v and the probabilities are carried as fp16 value +
+// remainder (three MFMAs per product); needs the *_lo planes of AttnArgs.
+hipError_t attn_prefill(const AttnArgs &a, bool precise, hipStream_t s);
+hipError_t attn_cascade(const AttnArgs &a, bool precise, hipStream_t s);
 hipError_t attn_merge(const AttnArgs &a, hipStream_t s);
 
 // ------------------------------------------------------ simple (fp32) path

@@ -23,6 +23,13 @@
 // The candidate pass may split the prefix keys into chunks (more blocks on the
 // chip); each chunk writes (max, sum, unnormalised output) partials and
 // attn_merge combines them.
+//
+// Precise variant (the leading layers of a deep model, where rounding is
+// amplified most): queries, keys and values arrive as fp16 value + fp16
+// remainder planes and the probabilities are split the same way; each product
+// takes three MFMAs (hi.hi + hi.lo + lo.hi), which leaves an error of the
+// order of fp32 rounding. Its blocks hold 128 query rows on 4 waves with the
+// queries in registers, so that the doubled key/value ring fits in LDS.
 #include "common.h"
 
 namespace vsr {
@@ -30,13 +37,20 @@ namespace vsr {
 namespace {
 
 constexpr int HD = 128;   // head dim of the MFMA path
-constexpr int NT = 512;   // threads per block
-constexpr int NW = NT / 64;
-constexpr int QT = NW * 32;  // stacked query rows per block
 constexpr int KT = 64;    // keys per tile
 constexpr int KCH = KT * 16;   // 16-byte chunks of a K tile  [64 keys][128 dims]
 constexpr int VCH = HD * 8;    // 16-byte chunks of a V^T tile [128 dims][64 keys]
-constexpr int STAGE = KCH + VCH;
+
+// Block shape of the fast (PREC = false) and precise (PREC = true) variants.
+// An LDS stage holds [K | V^T] tiles, precise: [K | V^T | K lo | V^T lo].
+template <bool PREC>
+struct Shape {
+  static constexpr int NW = PREC ? 4 : 8;  // waves per block
+  static constexpr int NT = NW * 64;
+  static constexpr int QT = NW * 32;       // stacked query rows per block
+  static constexpr int STAGE = (PREC ? 2 : 1) * (KCH + VCH);
+};
+constexpr int QT_FAST = Shape<false>::QT;
 
 __device__ __forceinline__ f16x8 as_f16x8(u32x4 v) { return __builtin_bit_cast(f16x8, v); }
 
@@ -54,6 +68,7 @@ enum SegMode { SEG_ALL = 0, SEG_CAUSAL = 1, SEG_BRANCH = 2 };
 struct Seg {
   const f16 *k;    // [npos][HD] of this KV head
   const f16 *vt;   // [HD][npos] of this KV head (interleaved positions)
+  const f16 *k_lo, *vt_lo;  // their remainder planes (precise variant)
   int npos;        // position stride of vt
   int kvalid;      // keys >= kvalid hold no data (never visible)
   int kbeg, kend;  // key range walked by the block: [kbeg, kend), kbeg % 64 == 0
@@ -66,44 +81,64 @@ struct Lane {
   int lo;    // SEG_BRANCH: first visible key
   float m, l;
   f32x16 o[HD / 32];
-  const u32x4 *qs;  // the block's query tile in LDS [QT rows][16 chunks]
-  int qrow;         // this lane's row in it
+  const u32x4 *qs;  // fast: the block's query tile in LDS [QT rows][16 chunks]
+  int qrow;         // fast: this lane's row in it
+  f16x8 qh[HD / 16], ql[HD / 16];  // precise: chunks 2kk + h of the row, hi / lo
 };
 
 // Direct loads of key tile kb into an LDS stage. Load i of wave w fills K
 // rows 4 (i NW + w) .. +3 and V^T rows 8 (i NW + w) .. +7; lane l lands in
 // 16-byte slot l of that 1 KB, i.e. physical chunk l % 16 of K row l / 16, or
 // l % 8 of V^T row l / 8; the global address carries the logical chunk.
-__device__ __forceinline__ void load_tile(const Seg &sg, int kb, u32x4 *stage) {
+template <int NW>
+__device__ __forceinline__ void load_kv(const f16 *k, const f16 *vt, int npos, int kb,
+                                        u32x4 *stage) {
   const int t = threadIdx.x, w = t >> 6, l = t & 63;
 #pragma unroll
-  for (int i = 0; i < KCH / NT; ++i) {
+  for (int i = 0; i < KCH / (NW * 64); ++i) {
     const int j = i * NW + w, key = j * 4 + (l >> 4), c = (l & 15) ^ (key & 15);
-    __builtin_amdgcn_global_load_lds(sg.k + (long)(kb + key) * HD + c * 8, stage + j * 64, 16,
-                                     0, 0);
+    __builtin_amdgcn_global_load_lds(k + (long)(kb + key) * HD + c * 8, stage + j * 64, 16, 0,
+                                     0);
   }
 #pragma unroll
-  for (int i = 0; i < VCH / NT; ++i) {
+  for (int i = 0; i < VCH / (NW * 64); ++i) {
     const int j = i * NW + w, d = j * 8 + (l >> 3), c = (l & 7) ^ ((d >> 1) & 7);
-    __builtin_amdgcn_global_load_lds(sg.vt + (long)d * sg.npos + kb + c * 8,
-                                     stage + KCH + j * 64, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(vt + (long)d * npos + kb + c * 8, stage + KCH + j * 64, 16,
+                                     0, 0);
   }
 }
 
+template <bool PREC>
+__device__ __forceinline__ void load_tile(const Seg &sg, int kb, u32x4 *stage) {
+  load_kv<Shape<PREC>::NW>(sg.k, sg.vt, sg.npos, kb, stage);
+  if constexpr (PREC) load_kv<Shape<PREC>::NW>(sg.k_lo, sg.vt_lo, sg.npos, kb, stage + KCH + VCH);
+}
+
+__device__ __forceinline__ f32x16 mfma(f16x8 a, f16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
 // One 64-key tile against this wave's 32 query rows.
-template <bool MASK>
+template <bool MASK, bool PREC>
 __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *st, Lane &L,
                                           float scale_log2) {
   const int lane = threadIdx.x & 63, h = lane >> 5;
   const u32x4 *Ks = st, *Vs = st + KCH;
+  const u32x4 *Kl = st + KCH + VCH, *Vl = Kl + KCH;  // remainder planes (precise)
   f32x16 s[2] = {f32x16{}, f32x16{}};
 #pragma unroll
   for (int kk = 0; kk < HD / 16; ++kk) {
-    const f16x8 qf = as_f16x8(L.qs[ks_idx(L.qrow, 2 * kk + h)]);
+    const f16x8 qf = PREC ? L.qh[kk] : as_f16x8(L.qs[ks_idx(L.qrow, 2 * kk + h)]);
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
-      s[b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
-          as_f16x8(Ks[ks_idx(b * 32 + (lane & 31), 2 * kk + h)]), qf, s[b], 0, 0, 0);
+    for (int b = 0; b < 2; ++b) {
+      const int ki = ks_idx(b * 32 + (lane & 31), 2 * kk + h);
+      const f16x8 kf = as_f16x8(Ks[ki]);
+      if constexpr (PREC) {
+        s[b] = mfma(as_f16x8(Kl[ki]), qf, s[b]);
+        s[b] = mfma(kf, L.ql[kk], s[b]);
+      }
+      s[b] = mfma(kf, qf, s[b]);
+    }
   }
   // Scale (and mask); key of register r of block b: kb + 32b + 8(r/4) + 4h + r%4.
   float mloc = -INFINITY;
@@ -126,14 +161,16 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *st
   const float mnew = fmaxf(L.m, mloc);
   const float mref = mnew == -INFINITY ? 0.f : mnew;
   float psum = 0.f;
-  f16x8 p[4];
+  f16x8 p[4], pl[4];
 #pragma unroll
   for (int b = 0; b < 2; ++b)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const float e = __builtin_amdgcn_exp2f(s[b][r] - mref);
       psum += e;
-      p[b * 2 + (r >> 3)][r & 7] = static_cast<f16>(e);
+      const f16 eh = static_cast<f16>(e);
+      p[b * 2 + (r >> 3)][r & 7] = eh;
+      if constexpr (PREC) pl[b * 2 + (r >> 3)][r & 7] = static_cast<f16>(e - static_cast<float>(eh));
     }
   psum += __shfl_xor(psum, 32, 64);
   if (mnew != L.m) {  // rescale only when this lane's running max moved
@@ -151,9 +188,13 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *st
   for (int c = 0; c < 4; ++c)
 #pragma unroll
     for (int db = 0; db < HD / 32; ++db) {
-      const int d = db * 32 + (lane & 31);
-      L.o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_f16x8(Vs[vs_idx(d, 2 * c + h)]), p[c],
-                                                       L.o[db], 0, 0, 0);
+      const int vi = vs_idx(db * 32 + (lane & 31), 2 * c + h);
+      const f16x8 vf = as_f16x8(Vs[vi]);
+      if constexpr (PREC) {
+        L.o[db] = mfma(as_f16x8(Vl[vi]), p[c], L.o[db]);
+        L.o[db] = mfma(vf, pl[c], L.o[db]);
+      }
+      L.o[db] = mfma(vf, p[c], L.o[db]);
     }
 }
 
@@ -164,20 +205,22 @@ __device__ __forceinline__ bool tile_clear(const Seg &sg, int kb) {
   return sg.mode == SEG_ALL;
 }
 
+template <bool PREC>
 __device__ __forceinline__ void walk_segment(const Seg &sg, u32x4 *lds, Lane &L,
                                              float scale_log2) {
+  constexpr int STAGE = Shape<PREC>::STAGE;
   if (sg.kend <= sg.kbeg) return;
-  load_tile(sg, sg.kbeg, lds);
+  load_tile<PREC>(sg, sg.kbeg, lds);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   int stage = 0;
   for (int kb = sg.kbeg; kb < sg.kend; kb += KT) {
     u32x4 *cur = lds + stage * STAGE;
-    if (kb + KT < sg.kend) load_tile(sg, kb + KT, lds + (stage ^ 1) * STAGE);
+    if (kb + KT < sg.kend) load_tile<PREC>(sg, kb + KT, lds + (stage ^ 1) * STAGE);
     if (tile_clear(sg, kb))
-      tile_step<false>(sg, kb, cur, L, scale_log2);
+      tile_step<false, PREC>(sg, kb, cur, L, scale_log2);
     else
-      tile_step<true>(sg, kb, cur, L, scale_log2);
+      tile_step<true, PREC>(sg, kb, cur, L, scale_log2);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     stage ^= 1;
@@ -187,10 +230,11 @@ __device__ __forceinline__ void walk_segment(const Seg &sg, u32x4 *lds, Lane &L,
 // mode 0: prefill (causal over the prefix cache, one chunk, direct output);
 // mode 1: candidate pass (prefix chunk blockIdx.z; the last chunk also walks
 //         the candidate's own keys).
-template <int MODE>
-__global__ __launch_bounds__(NT) void k_attn(AttnArgs a) {
-  __shared__ u32x4 lds[2 * STAGE];
-  __shared__ u32x4 qlds[QT * 16];
+template <int MODE, bool PREC>
+__global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
+  constexpr int QT = Shape<PREC>::QT;
+  __shared__ u32x4 lds[2 * Shape<PREC>::STAGE];
+  __shared__ u32x4 qlds[PREC ? 1 : QT * 16];
   const int G = a.n_heads / a.n_kv, TG = (a.T - a.t0) * G;
   const int kvh = blockIdx.y;
   // Prefill tiles with more keys first.
@@ -208,16 +252,25 @@ __global__ __launch_bounds__(NT) void k_attn(AttnArgs a) {
   L.l = 0.f;
 #pragma unroll
   for (int db = 0; db < HD / 32; ++db) L.o[db] = f32x16{};
-  // Query tile -> LDS (same layout and swizzle as a K tile): wave w's rows
-  // 32 w .. 32 w + 31, four rows per direct load.
-  {
+  if constexpr (PREC) {
+    // Queries -> registers: the chunks this lane feeds to the S^T products.
+    const long qoff = ((long)L.tok * a.n_heads + head) * HD + 8 * (lane >> 5);
+#pragma unroll
+    for (int kk = 0; kk < HD / 16; ++kk) {
+      L.qh[kk] = *reinterpret_cast<const f16x8 *>(a.q + qoff + 16 * kk);
+      L.ql[kk] = *reinterpret_cast<const f16x8 *>(a.q_lo + qoff + 16 * kk);
+    }
+  } else {
+    // Query tile -> LDS (same layout and swizzle as a K tile): wave w's rows
+    // 32 w .. 32 w + 31, four rows per direct load.
+    u32x4 *qdst = qlds;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int rl = w * 32 + i * 4 + (lane >> 4);          // LDS row
       const int rg = min(q0 + rl, TG - 1);                   // stacked row it holds
       const int c = (lane & 15) ^ (rl & 15);
       const f16 *src = a.q + ((long)(a.t0 + rg / G) * a.n_heads + kvh * G + rg % G) * HD + c * 8;
-      __builtin_amdgcn_global_load_lds(src, qlds + (w * 32 + i * 4) * 16, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(src, qdst + (w * 32 + i * 4) * 16, 16, 0, 0);
     }
   }
   L.qs = qlds;
@@ -227,20 +280,23 @@ __global__ __launch_bounds__(NT) void k_attn(AttnArgs a) {
   const int tok_last = a.t0 + min(q0 + QT - 1, TG - 1) / G;
 
   const int chunk = blockIdx.z;
+  const long koff = (long)kvh * a.kv_npos * HD, boff = (long)kvh * a.bk_npos * HD;
   if (MODE == 0) {
-    Seg sg{a.k + (long)kvh * a.kv_npos * HD, a.vt + (long)kvh * HD * a.kv_npos, a.kv_npos,
-           a.T, 0, tok_last + 1, SEG_CAUSAL, tok_first};
-    walk_segment(sg, lds, L, scale_log2);
+    Seg sg{a.k + koff, a.vt + koff, PREC ? a.k_lo + koff : nullptr,
+           PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.T, 0, tok_last + 1, SEG_CAUSAL,
+           tok_first};
+    walk_segment<PREC>(sg, lds, L, scale_log2);
   } else {
     const int kb = chunk * a.chunk, ke = min(a.P, kb + a.chunk);
-    Seg sp{a.k + (long)kvh * a.kv_npos * HD, a.vt + (long)kvh * HD * a.kv_npos, a.kv_npos,
-           a.P, kb, ke, SEG_ALL, tok_first};
-    walk_segment(sp, lds, L, scale_log2);
+    Seg sp{a.k + koff, a.vt + koff, PREC ? a.k_lo + koff : nullptr,
+           PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.P, kb, ke, SEG_ALL, tok_first};
+    walk_segment<PREC>(sp, lds, L, scale_log2);
     if (chunk == a.nchunks - 1) {
       const int lo = a.row_lo[tok_first] & ~(KT - 1);
-      Seg sb{a.bk + (long)kvh * a.bk_npos * HD, a.bvt + (long)kvh * HD * a.bk_npos, a.bk_npos,
-             a.T, lo, tok_last + 1, SEG_BRANCH, tok_first};
-      walk_segment(sb, lds, L, scale_log2);
+      Seg sb{a.bk + boff, a.bvt + boff, PREC ? a.bk_lo + boff : nullptr,
+             PREC ? a.bvt_lo + boff : nullptr, a.bk_npos, a.T, lo, tok_last + 1, SEG_BRANCH,
+             tok_first};
+      walk_segment<PREC>(sb, lds, L, scale_log2);
     }
   }
 
@@ -248,15 +304,21 @@ __global__ __launch_bounds__(NT) void k_attn(AttnArgs a) {
   const int h = lane >> 5;
   if (MODE == 0 || a.nchunks == 1) {
     const float inv = 1.f / L.l;
-    f16 *op = a.out + ((long)L.tok * a.n_heads + head) * HD;
+    f16 *op = a.out + ((long)L.tok * a.out_split * a.n_heads + head) * HD;
+    f16 *olo = op + (long)a.n_heads * HD;  // remainder half of a split row
 #pragma unroll
     for (int db = 0; db < HD / 32; ++db)
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
-        f16x4 v;
+        f16x4 v, vl;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = static_cast<f16>(L.o[db][g4 * 4 + j] * inv);
+        for (int j = 0; j < 4; ++j) {
+          const float x = L.o[db][g4 * 4 + j] * inv;
+          v[j] = static_cast<f16>(x);
+          vl[j] = static_cast<f16>(x - static_cast<float>(v[j]));
+        }
         *reinterpret_cast<f16x4 *>(op + db * 32 + 8 * g4 + 4 * h) = v;
+        if (a.out_split == 2) *reinterpret_cast<f16x4 *>(olo + db * 32 + 8 * g4 + 4 * h) = vl;
       }
   } else {
     const long prow = ((long)chunk * a.n_kv + kvh) * TG + row;
@@ -292,29 +354,42 @@ __global__ __launch_bounds__(64) void k_attn_merge(AttnArgs a) {
     o1 += a.part_acc[prow * HD + 64 + lane] * wgt;
   }
   const float inv = 1.f / Lsum;
-  f16 *op = a.out + ((long)t * a.n_heads + head) * HD;
-  op[lane] = static_cast<f16>(o0 * inv);
-  op[64 + lane] = static_cast<f16>(o1 * inv);
+  f16 *op = a.out + ((long)t * a.out_split * a.n_heads + head) * HD;
+  const float x0 = o0 * inv, x1 = o1 * inv;
+  const f16 h0 = static_cast<f16>(x0), h1 = static_cast<f16>(x1);
+  op[lane] = h0;
+  op[64 + lane] = h1;
+  if (a.out_split == 2) {
+    f16 *olo = op + (long)a.n_heads * HD;
+    olo[lane] = static_cast<f16>(x0 - static_cast<float>(h0));
+    olo[64 + lane] = static_cast<f16>(x1 - static_cast<float>(h1));
+  }
+}
+
+template <int MODE, bool PREC>
+hipError_t launch_attn(const AttnArgs &a, hipStream_t s) {
+  using S = Shape<PREC>;
+  const int G = a.n_heads / a.n_kv;
+  dim3 grid(((a.T - a.t0) * G + S::QT - 1) / S::QT, a.n_kv, MODE == 0 ? 1 : a.nchunks);
+  k_attn<MODE, PREC><<<grid, S::NT, 0, s>>>(a);
+  return hipGetLastError();
 }
 
 }  // namespace
 
-int attn_query_tile() { return QT; }
+int attn_query_tile() { return QT_FAST; }
 
-hipError_t attn_prefill(const AttnArgs &a, hipStream_t s) {
+hipError_t attn_prefill(const AttnArgs &a, bool precise, hipStream_t s) {
   if (a.T <= a.t0) return hipSuccess;
-  const int G = a.n_heads / a.n_kv;
-  dim3 grid(((a.T - a.t0) * G + QT - 1) / QT, a.n_kv, 1);
-  k_attn<0><<<grid, NT, 0, s>>>(a);
-  return hipGetLastError();
+  if (precise && (!a.q_lo || !a.k_lo || !a.vt_lo)) return hipErrorInvalidValue;
+  return precise ? launch_attn<0, true>(a, s) : launch_attn<0, false>(a, s);
 }
 
-hipError_t attn_cascade(const AttnArgs &a, hipStream_t s) {
-  if (a.T == 0) return hipSuccess;
-  const int G = a.n_heads / a.n_kv;
-  dim3 grid((a.T * G + QT - 1) / QT, a.n_kv, a.nchunks);
-  k_attn<1><<<grid, NT, 0, s>>>(a);
-  return hipGetLastError();
+hipError_t attn_cascade(const AttnArgs &a, bool precise, hipStream_t s) {
+  if (a.T == 0 || a.t0 != 0) return a.T == 0 ? hipSuccess : hipErrorInvalidValue;
+  if (precise && (!a.q_lo || !a.k_lo || !a.vt_lo || !a.bk_lo || !a.bvt_lo))
+    return hipErrorInvalidValue;
+  return precise ? launch_attn<1, true>(a, s) : launch_attn<1, false>(a, s);
 }
 
 hipError_t attn_merge(const AttnArgs &a, hipStream_t s) {

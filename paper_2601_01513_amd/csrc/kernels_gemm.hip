@@ -84,7 +84,7 @@ struct Operand {
   u32x4 r[CVT ? PER_THREAD : 1];
 
   template <class RowFn>
-  __device__ __forceinline__ void init(const void *base, int K, RowFn row_of) {
+  __device__ __forceinline__ void init(const void *base, long ld, RowFn row_of) {
     const uint16_t *p = static_cast<const uint16_t *>(base);
     const int t = threadIdx.x;
 #pragma unroll
@@ -103,7 +103,7 @@ struct Operand {
         c = (l & 7) ^ ((row >> 1) & 7);
         slot[i] = 0;
       }
-      g[i] = p + (long)row_of(row) * K + c * 8;
+      g[i] = p + (long)row_of(row) * ld + c * 8;
     }
   }
   // Starts loading K-panel kt into LDS stage `dst` (direct) or registers.
@@ -161,15 +161,19 @@ __device__ __forceinline__ void interleave_reads(int nreads, int nmfma) {
 // never stored). CVT_A / CVT_B mark an operand stored as bf16. Fragments are
 // double-buffered in registers: the LDS reads of k-step s+1 are in flight
 // while the MFMAs of k-step s run.
+// Split operands: with asplit = 2 each A row holds [hi | lo], the fp16 value
+// and its fp16 remainder (K each), and B (K per row) is walked twice, so the
+// product is B.hi + B.lo -- an operand carried to about 22 significant bits.
 template <class TL, bool CVT_A, bool CVT_B, class ARow, class BRow>
 __device__ __forceinline__ void mainloop(const void *A, ARow arow, const void *B, BRow brow,
-                                         int K, int kt0, int kt1, u32x4 *lds,
+                                         int K, int asplit, int kt0, int kt1, u32x4 *lds,
                                          f32x16 (&acc)[TL::FM][TL::FN]) {
+  const int nkb = K / BK;  // K panels of B
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int wm = w / TL::WN, wn = w % TL::WN;
   Operand<TL::BM, CVT_A> oa;
   Operand<TL::BN, CVT_B> ob;
-  oa.init(A, K, arow);
+  oa.init(A, (long)K * asplit, arow);
   ob.init(B, K, brow);
 #pragma unroll
   for (int fm = 0; fm < TL::FM; ++fm)
@@ -186,7 +190,7 @@ __device__ __forceinline__ void mainloop(const void *A, ARow arow, const void *B
   constexpr int NR = TL::FM + TL::FN, NM = TL::FM * TL::FN;
 
   oa.issue(kt0, lds);
-  ob.issue(kt0, lds + TL::BM * 8);
+  ob.issue(kt0 >= nkb ? kt0 - nkb : kt0, lds + TL::BM * 8);
   oa.commit(lds);
   ob.commit(lds + TL::BM * 8);
   __builtin_amdgcn_s_waitcnt(0);
@@ -200,7 +204,7 @@ __device__ __forceinline__ void mainloop(const void *A, ARow arow, const void *B
     const bool more = kt + 1 < kt1;
     if (more) {
       oa.issue(kt + 1, nxt);
-      ob.issue(kt + 1, nxt + TL::BM * 8);
+      ob.issue(kt + 1 >= nkb ? kt + 1 - nkb : kt + 1, nxt + TL::BM * 8);
     }
     f1.load(cur, fa, fb, 2 + hc);
     f0.mma(acc);
@@ -336,23 +340,31 @@ __device__ __forceinline__ float sum_partials(const float *part, const Launch &l
 
 __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.f + __expf(-g)) * u; }
 
+// Activation store: fp16 value at base + col; with split = 2 also its fp16
+// remainder at base + n + col (row layout [hi | lo]).
+__device__ __forceinline__ void store_act(f16 *p, long base, int col, int n, int split, float v) {
+  const f16 hi = static_cast<f16>(v);
+  p[base + col] = hi;
+  if (split == 2) p[base + n + col] = static_cast<f16>(v - static_cast<float>(hi));
+}
+
 // ------------------------------------------------------- residual (O, down)
 template <class TL>
 __global__ __launch_bounds__(NT) void k_gemm_residual(const f16 *__restrict__ A,
                                                       const bf16 *__restrict__ W, int rows,
-                                                      int N, int K, Launch ln,
+                                                      int N, int K, int asplit, Launch ln,
                                                       float *__restrict__ x,
                                                       float *__restrict__ part) {
   __shared__ u32x4 lds[2 * TL::STAGE];
   const Work wk = block_work(ln);
   const int m0 = wk.tm * TL::BM, n0 = wk.tn * TL::BN;
   const bool split = wk.tail >= 0;
-  int k0 = 0, k1 = K / BK;
-  if (split) split_range(K / BK, ln.nsplit, wk.split, k0, k1);
+  int k0 = 0, k1 = K / BK * asplit;
+  if (split) split_range(k1, ln.nsplit, wk.split, k0, k1);
   f32x16 acc[TL::FM][TL::FN];
   mainloop<TL, false, true>(
       A, [=](int r) { return min(m0 + r, rows - 1); }, W,
-      [=](int r) { return min(n0 + r, N - 1); }, K, k0, k1, lds, acc);
+      [=](int r) { return min(n0 + r, N - 1); }, K, asplit, k0, k1, lds, acc);
   if (split) {
     store_partial<TL>(acc, part, ln, wk);
     return;
@@ -393,15 +405,15 @@ __global__ __launch_bounds__(256) void k_reduce_residual(const float *__restrict
 template <class TL>
 __global__ __launch_bounds__(NT) void k_gemm_swiglu(const f16 *__restrict__ A,
                                                     const bf16 *__restrict__ W, int rows, int F,
-                                                    int K, Launch ln, f16 *__restrict__ h,
-                                                    float *__restrict__ part) {
+                                                    int K, int asplit, Launch ln,
+                                                    f16 *__restrict__ h, float *__restrict__ part) {
   static_assert(TL::WN == 2 && TL::TN == 128 && TL::BN == 256, "gate/up pairing");
   __shared__ u32x4 lds[2 * TL::STAGE];
   const Work wk = block_work(ln);
   const int m0 = wk.tm * TL::BM, o0 = wk.tn * 128;
   const bool split = wk.tail >= 0;
-  int k0 = 0, k1 = K / BK;
-  if (split) split_range(K / BK, ln.nsplit, wk.split, k0, k1);
+  int k0 = 0, k1 = K / BK * asplit;
+  if (split) split_range(k1, ln.nsplit, wk.split, k0, k1);
   f32x16 acc[TL::FM][TL::FN];
   mainloop<TL, false, true>(
       A, [=](int r) { return min(m0 + r, rows - 1); }, W,
@@ -410,7 +422,7 @@ __global__ __launch_bounds__(NT) void k_gemm_swiglu(const f16 *__restrict__ A,
         const int oc = min(o0 + (r >> 7) * 64 + (q & 63), F - 1);
         return q < 64 ? oc : F + oc;
       },
-      K, k0, k1, lds, acc);
+      K, asplit, k0, k1, lds, acc);
   if (split) {
     store_partial<TL>(acc, part, ln, wk);
     return;
@@ -426,8 +438,8 @@ __global__ __launch_bounds__(NT) void k_gemm_swiglu(const f16 *__restrict__ A,
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = m0 + acc_row<TL>(wm, fm, r, lane);
-        if (row < rows)
-          h[(long)row * F + col] = static_cast<f16>(silu_mul(acc[fm][fn][r], acc[fm][fn + 2][r]));
+        if (row < rows) store_act(h, (long)row * F * asplit, col, F, asplit,
+                                  silu_mul(acc[fm][fn][r], acc[fm][fn + 2][r]));
       }
   }
 }
@@ -435,7 +447,7 @@ __global__ __launch_bounds__(NT) void k_gemm_swiglu(const f16 *__restrict__ A,
 // Tail tiles: h = silu(gate) * up from the summed partials. Block (tail tile,
 // half of its 256 rows); thread -> (row, output column oc < 128).
 __global__ __launch_bounds__(256) void k_reduce_swiglu(const float *__restrict__ part,
-                                                       Launch ln, int rows, int F,
+                                                       Launch ln, int rows, int F, int hsplit,
                                                        f16 *__restrict__ h) {
   const int i = blockIdx.x / 128, e = (blockIdx.x % 128) * 256 + threadIdx.x;
   int tm, tn;
@@ -446,7 +458,7 @@ __global__ __launch_bounds__(256) void k_reduce_swiglu(const float *__restrict__
   const int cg = (oc / 64) * 128 + oc % 64;
   const float g = sum_partials(part, ln, i, lr * 256 + cg);
   const float u = sum_partials(part, ln, i, lr * 256 + cg + 64);
-  h[(long)row * F + o] = static_cast<f16>(silu_mul(g, u));
+  store_act(h, (long)row * F * hsplit, o, F, hsplit, silu_mul(g, u));
 }
 
 // ------------------------------------------------- QKV + rotary + KV caches
@@ -462,41 +474,57 @@ __device__ __forceinline__ void qkv_store(const QKVOut<f16> &o, int n_heads, int
     x1 = y1;
     x2 = y2;
   }
+  const f16 h1 = static_cast<f16>(x1), h2 = static_cast<f16>(x2);
+  const f16 l1 = static_cast<f16>(x1 - static_cast<float>(h1));
+  const f16 l2 = static_cast<f16>(x2 - static_cast<float>(h2));
   if (slot < n_heads) {
-    f16 *q = o.q + ((long)row * n_heads + slot) * 128;
-    q[d] = static_cast<f16>(x1);
-    q[d + 64] = static_cast<f16>(x2);
+    const long off = ((long)row * n_heads + slot) * 128;
+    o.q[off + d] = h1;
+    o.q[off + d + 64] = h2;
+    if (o.q_lo) {
+      o.q_lo[off + d] = l1;
+      o.q_lo[off + d + 64] = l2;
+    }
   } else if (slot < n_heads + n_kv) {
-    f16 *k = o.k + ((long)(slot - n_heads) * o.kv_npos + row) * 128;
-    k[d] = static_cast<f16>(x1);
-    k[d + 64] = static_cast<f16>(x2);
+    const long off = ((long)(slot - n_heads) * o.kv_npos + row) * 128;
+    o.k[off + d] = h1;
+    o.k[off + d + 64] = h2;
+    if (o.k_lo) {
+      o.k_lo[off + d] = l1;
+      o.k_lo[off + d + 64] = l2;
+    }
   } else {
     // Values go to the Vt cache at the attention kernel's interleaved
     // position: within each aligned group of 16, quarters 1 and 2 swap.
-    f16 *vt = o.vt + (long)(slot - n_heads - n_kv) * 128 * o.kv_npos;
+    const long base = (long)(slot - n_heads - n_kv) * 128 * o.kv_npos;
     const int pp = (row & ~12) | ((row & 4) << 1) | ((row & 8) >> 1);
-    vt[(long)d * o.kv_npos + pp] = static_cast<f16>(x1);
-    vt[(long)(d + 64) * o.kv_npos + pp] = static_cast<f16>(x2);
+    const long o1 = base + (long)d * o.kv_npos + pp, o2 = base + (long)(d + 64) * o.kv_npos + pp;
+    o.vt[o1] = h1;
+    o.vt[o2] = h2;
+    if (o.vt_lo) {
+      o.vt_lo[o1] = l1;
+      o.vt_lo[o2] = l2;
+    }
   }
 }
 
 template <class TL>
 __global__ __launch_bounds__(NT) void k_gemm_qkv(const f16 *__restrict__ A,
                                                  const bf16 *__restrict__ W, int rows, int K,
-                                                 int n_heads, int n_kv, Launch ln, QKVOut<f16> o,
-                                                 float *__restrict__ part) {
+                                                 int asplit, int n_heads, int n_kv, Launch ln,
+                                                 QKVOut<f16> o, float *__restrict__ part) {
   static_assert(TL::WN == 2 && TL::TN == 128 && TL::BN == 256, "one head per wave column");
   __shared__ u32x4 lds[2 * TL::STAGE];
   const Work wk = block_work(ln);
   const int nslots = n_heads + 2 * n_kv, nrows = nslots * 128;
   const int m0 = wk.tm * TL::BM, n0 = wk.tn * 256;
   const bool split = wk.tail >= 0;
-  int k0 = 0, k1 = K / BK;
-  if (split) split_range(K / BK, ln.nsplit, wk.split, k0, k1);
+  int k0 = 0, k1 = K / BK * asplit;
+  if (split) split_range(k1, ln.nsplit, wk.split, k0, k1);
   f32x16 acc[TL::FM][TL::FN];
   mainloop<TL, false, true>(
       A, [=](int r) { return min(m0 + r, rows - 1); }, W,
-      [=](int r) { return min(n0 + r, nrows - 1); }, K, k0, k1, lds, acc);
+      [=](int r) { return min(n0 + r, nrows - 1); }, K, asplit, k0, k1, lds, acc);
   if (split) {
     store_partial<TL>(acc, part, ln, wk);
     return;
@@ -557,7 +585,7 @@ __global__ __launch_bounds__(NT) void k_gemm_lmhead(const f16 *__restrict__ Hn,
   f32x16 acc[TL::FM][TL::FN];
   mainloop<TL, true, false>(
       Wlm, [=](int r) { return min(m0 + r, vocab - 1); }, Hn,
-      [=](int r) { return min(n0 + r, T - 1); }, K, 0, K / BK, lds, acc);
+      [=](int r) { return min(n0 + r, T - 1); }, K, 1, 0, K / BK, lds, acc);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w / TL::WN, wn = w % TL::WN;
 
@@ -625,38 +653,42 @@ __global__ __launch_bounds__(NT) void k_gemm_lmhead(const f16 *__restrict__ Hn,
 }  // namespace
 
 size_t gemm_split_floats(int rows, int N, int K) {
-  const Launch ln = plan_launch((rows + 255) / 256, (N + 255) / 256, 8, K / BK);
+  const Launch ln = plan_launch((rows + 255) / 256, (N + 255) / 256, 8, K / BK);  // K: A width
   return (size_t)ln.ntail * ln.nsplit * kTileElems;
 }
 
-hipError_t gemm_residual(const f16 *A, const bf16 *W, int rows, int N, int K, float *x,
-                         float *part, hipStream_t s) {
+hipError_t gemm_residual(const f16 *A, const bf16 *W, int rows, int N, int K, int asplit,
+                         float *x, float *part, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
-  const Launch ln = plan_launch((rows + TL::BM - 1) / TL::BM, (N + TL::BN - 1) / TL::BN, 8, K / BK);
-  k_gemm_residual<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, N, K, ln, x, part);
+  const Launch ln = plan_launch((rows + TL::BM - 1) / TL::BM, (N + TL::BN - 1) / TL::BN, 8,
+                                K / BK * asplit);
+  k_gemm_residual<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, N, K, asplit, ln, x, part);
   if (ln.ntail > 0)
     k_reduce_residual<<<ln.ntail * 256, 256, 0, s>>>(part, ln, rows, N, x);
   return hipGetLastError();
 }
 
-hipError_t gemm_swiglu(const f16 *A, const bf16 *W, int rows, int F, int K, f16 *h, float *part,
-                       hipStream_t s) {
+hipError_t gemm_swiglu(const f16 *A, const bf16 *W, int rows, int F, int K, int asplit, f16 *h,
+                       float *part, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
-  const Launch ln = plan_launch((rows + TL::BM - 1) / TL::BM, (F + 127) / 128, 8, K / BK);
-  k_gemm_swiglu<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, F, K, ln, h, part);
-  if (ln.ntail > 0) k_reduce_swiglu<<<ln.ntail * 128, 256, 0, s>>>(part, ln, rows, F, h);
+  const Launch ln = plan_launch((rows + TL::BM - 1) / TL::BM, (F + 127) / 128, 8,
+                                K / BK * asplit);
+  k_gemm_swiglu<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, F, K, asplit, ln, h, part);
+  if (ln.ntail > 0)
+    k_reduce_swiglu<<<ln.ntail * 128, 256, 0, s>>>(part, ln, rows, F, asplit, h);
   return hipGetLastError();
 }
 
-hipError_t gemm_qkv_rope(const f16 *A, const bf16 *W, int rows, int K, int n_heads, int n_kv,
-                         const QKVOut<f16> &out, float *part, hipStream_t s) {
+hipError_t gemm_qkv_rope(const f16 *A, const bf16 *W, int rows, int K, int asplit, int n_heads,
+                         int n_kv, const QKVOut<f16> &out, float *part, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
   const int nslots = n_heads + 2 * n_kv;
-  const Launch ln = plan_launch((rows + TL::BM - 1) / TL::BM, (nslots + 1) / 2, 8, K / BK);
-  k_gemm_qkv<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, K, n_heads, n_kv, ln, out, part);
+  const Launch ln = plan_launch((rows + TL::BM - 1) / TL::BM, (nslots + 1) / 2, 8,
+                                K / BK * asplit);
+  k_gemm_qkv<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, K, asplit, n_heads, n_kv, ln, out, part);
   if (ln.ntail > 0)
     k_reduce_qkv<<<ln.ntail * 128, 256, 0, s>>>(part, ln, rows, n_heads, n_kv, out);
   return hipGetLastError();

@@ -114,7 +114,7 @@ hipError_t launch_embed_rows(const int32_t *ids, int rows, const T *embed, int d
 // ------------------------------------------------------------------ RMSNorm
 template <typename TW, typename TA>
 __device__ __forceinline__ void norm_row(const float *src, const TW *g, int d, float eps,
-                                         TA *dst, float *red) {
+                                         TA *dst, float *red, int split = 1) {
   float ss = 0.f;
   for (int c = threadIdx.x; c < d; c += 256) {
     const float v = src[c];
@@ -122,22 +122,27 @@ __device__ __forceinline__ void norm_row(const float *src, const TW *g, int d, f
   }
   ss = block_sum256(ss, red);
   const float r = rsqrtf(ss / (float)d + eps);
-  for (int c = threadIdx.x; c < d; c += 256) dst[c] = from_f32<TA>(src[c] * r * to_f32(g[c]));
+  for (int c = threadIdx.x; c < d; c += 256) {
+    const float v = src[c] * r * to_f32(g[c]);
+    const TA hi = from_f32<TA>(v);
+    dst[c] = hi;
+    if (split == 2) dst[d + c] = from_f32<TA>(v - to_f32(hi));
+  }
 }
 
 template <typename TW, typename TA>
 __global__ __launch_bounds__(256) void k_rmsnorm(const float *x, const TW *g, int d, float eps,
-                                                 TA *y) {
+                                                 TA *y, int split) {
   __shared__ float red[4];
   const long r = blockIdx.x;
-  norm_row(x + r * d, g, d, eps, y + r * d, red);
+  norm_row(x + r * d, g, d, eps, y + r * d * split, red, split);
 }
 
 template <typename TW, typename TA>
 hipError_t launch_rmsnorm(const float *x, const TW *g, int rows, int d, float eps, TA *y,
-                          hipStream_t s) {
+                          int split, hipStream_t s) {
   if (rows == 0) return hipSuccess;
-  k_rmsnorm<TW, TA><<<rows, 256, 0, s>>>(x, g, d, eps, y);
+  k_rmsnorm<TW, TA><<<rows, 256, 0, s>>>(x, g, d, eps, y, split);
   return hipGetLastError();
 }
 
@@ -236,7 +241,7 @@ VSR_INST(bf16)
 #undef VSR_INST
 #define VSR_INST2(TW, TA)                                                                     \
   template hipError_t launch_rmsnorm<TW, TA>(const float *, const TW *, int, int, float,      \
-                                             TA *, hipStream_t);                              \
+                                             TA *, int, hipStream_t);                         \
   template hipError_t launch_lm_inputs<TW, TA>(const float *, const float *, const int32_t *, \
                                                const TW *, int, int, float, TA *, hipStream_t);
 VSR_INST2(float, float)

@@ -42,8 +42,8 @@ Split cascade_split(int T, int P, int n_heads, int n_kv) {
 
 struct Plan {
   int kv_npos, bk_npos, max_t, rows_max, rope_npos, lm_chunks;
-  size_t x, xn, q, attn, h, kc, vtc, bk, bvt, part_acc, part_ml, lm_part, tgt, row_lo,
-      row_pos, lm_tgt, rope, h_last, gemm_part, total;
+  size_t x, xn, q, q_lo, attn, h, kc, vtc, kc_lo, vtc_lo, bk, bvt, bk_lo, bvt_lo, part_acc,
+      part_ml, lm_part, tgt, row_lo, row_pos, lm_tgt, rope, h_last, gemm_part, total;
 };
 
 // Returns an empty message if cfg is supported.
@@ -59,6 +59,8 @@ std::string check_config(const vsr_config *c) {
   if (c->max_cands > VSR_MAX_CANDS) return "max_cands exceeds VSR_MAX_CANDS";
   if ((long long)c->max_cands * c->max_cand_len > (1 << 24)) return "max_cands * max_cand_len too large";
   if (c->max_prefix > (1 << 24)) return "max_prefix too large";
+  if (c->split_layers < 0 || c->split_layers > c->n_layers)
+    return "split_layers must be in [0, n_layers]";
   if (c->dtype == VSR_BF16) {
     if (c->head_dim != 128) return "bf16 contexts need head_dim == 128";
     if (c->d_model % 64 || c->d_ff % 64) return "bf16 contexts need d_model and d_ff multiples of 64";
@@ -96,10 +98,11 @@ Plan make_plan(const vsr_config &c) {
     const int qkv_n = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
     for (int r = 256;; r += 256) {
       const int rows = std::min(r, p.rows_max);
-      gemm_part = std::max({gemm_part, gemm_split_floats(rows, qkv_n, c.d_model),
-                            gemm_split_floats(rows, c.d_model, c.n_heads * c.head_dim),
-                            gemm_split_floats(rows, 2 * c.d_ff, c.d_model),
-                            gemm_split_floats(rows, c.d_model, c.d_ff)});
+      for (int s = 1; s <= (c.split_layers > 0 ? 2 : 1); ++s)
+        gemm_part = std::max({gemm_part, gemm_split_floats(rows, qkv_n, s * c.d_model),
+                              gemm_split_floats(rows, c.d_model, s * c.n_heads * c.head_dim),
+                              gemm_split_floats(rows, 2 * c.d_ff, s * c.d_model),
+                              gemm_split_floats(rows, c.d_model, s * c.d_ff)});
       if (rows == p.rows_max) break;
     }
   }
@@ -110,15 +113,27 @@ Plan make_plan(const vsr_config &c) {
     return o;
   };
   const size_t R = p.rows_max;
+  // Precise layers (the first split_layers of the MFMA path) carry GEMM rows
+  // as [hi | lo] and q, k, v as value + remainder planes.
+  const size_t sp = (c.dtype == VSR_BF16 && c.split_layers > 0) ? 2 : 1;
+  const size_t nprec = c.dtype == VSR_BF16 ? c.split_layers : 0;
+  const size_t prefix_cache = (size_t)c.n_kv_heads * p.kv_npos * hd * E;
+  const size_t branch_cache = (size_t)c.n_kv_heads * p.bk_npos * hd * E;
   p.x = take(R * d * 4);
-  p.xn = take(R * d * E);
+  p.xn = take(R * d * E * sp);
   p.q = take(R * c.n_heads * hd * E);
-  p.attn = take(R * c.n_heads * hd * E);
-  p.h = take(R * (size_t)c.d_ff * E);
-  p.kc = take((size_t)c.n_layers * c.n_kv_heads * p.kv_npos * hd * E);
-  p.vtc = take((size_t)c.n_layers * c.n_kv_heads * p.kv_npos * hd * E);
-  p.bk = take((size_t)c.n_kv_heads * p.bk_npos * hd * E);
-  p.bvt = take((size_t)c.n_kv_heads * p.bk_npos * hd * E);
+  p.q_lo = take(nprec ? R * c.n_heads * hd * E : 0);
+  p.attn = take(R * c.n_heads * hd * E * sp);
+  p.h = take(R * (size_t)c.d_ff * E * sp);
+  // Caches (kc .. part_acc) start zeroed at create.
+  p.kc = take(c.n_layers * prefix_cache);
+  p.vtc = take(c.n_layers * prefix_cache);
+  p.kc_lo = take(nprec * prefix_cache);
+  p.vtc_lo = take(nprec * prefix_cache);
+  p.bk = take(branch_cache);
+  p.bvt = take(branch_cache);
+  p.bk_lo = take(nprec ? branch_cache : 0);
+  p.bvt_lo = take(nprec ? branch_cache : 0);
   p.part_acc = take(part_rows * c.n_kv_heads * hd * 4);
   p.part_ml = take(part_rows * c.n_kv_heads * 8);
   p.lm_part = take((size_t)p.lm_chunks * p.max_t * 8);
@@ -327,9 +342,13 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
     const TW *wdown = static_cast<const TW *>(c->wdown[l]);
     TA *kc = c->at<TA>(p.kc) + l * layer_cache;
     TA *vtc = c->at<TA>(p.vtc) + l * layer_cache;
+    // Leading layers carry their GEMM and attention operands as fp16 value +
+    // remainder.
+    const bool precise = kMfma && l < cf.split_layers;
+    const int sp = precise ? 2 : 1;
     STAGE(c, K_NORM, "attention norm",
              launch_rmsnorm<TW, TA>(x, static_cast<const TW *>(c->attn_norm[l]), rows, d,
-                                    cf.rms_eps, xn, s));
+                                    cf.rms_eps, xn, sp, s));
     QKVOut<TA> qo;
     qo.q = q;
     qo.rope = c->at<float2>(p.rope);
@@ -344,8 +363,14 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       qo.kv_npos = p.bk_npos;
       qo.row_pos = c->at<int32_t>(p.row_pos);
     }
+    if (precise) {
+      qo.q_lo = c->at<TA>(p.q_lo);
+      qo.k_lo = mode == 0 ? c->at<TA>(p.kc_lo) + l * layer_cache : c->at<TA>(p.bk_lo);
+      qo.vt_lo = mode == 0 ? c->at<TA>(p.vtc_lo) + l * layer_cache : c->at<TA>(p.bvt_lo);
+    }
     if constexpr (kMfma) {
-      STAGE(c, K_QKV, "qkv projection", gemm_qkv_rope(xn, wqkv, rows, d, Hq, Hkv, qo, gpart, s));
+      STAGE(c, K_QKV, "qkv projection",
+            gemm_qkv_rope(xn, wqkv, rows, d, sp, Hq, Hkv, qo, gpart, s));
     } else {
       STAGE(c, K_QKV, "qkv projection",
             simple_qkv_rope<TA>(xn, wqkv, rows, d, Hq, Hkv, hd, qo, s));
@@ -373,12 +398,20 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       a.nchunks = split.nchunks;
       a.chunk = split.chunk;
       a.out = attn;
+      a.out_split = sp;
       a.part_acc = c->at<float>(p.part_acc);
       a.part_ml = c->at<float2>(p.part_ml);
+      if (precise) {
+        a.q_lo = c->at<f16>(p.q_lo);
+        a.k_lo = c->at<f16>(p.kc_lo) + l * layer_cache;
+        a.vt_lo = c->at<f16>(p.vtc_lo) + l * layer_cache;
+        a.bk_lo = c->at<f16>(p.bk_lo);
+        a.bvt_lo = c->at<f16>(p.bvt_lo);
+      }
       if (mode == 0) {
-        STAGE(c, K_ATTN, "prefill attention", attn_prefill(a, s));
+        STAGE(c, K_ATTN, "prefill attention", attn_prefill(a, precise, s));
       } else {
-        STAGE(c, K_ATTN, "cascade attention", attn_cascade(a, s));
+        STAGE(c, K_ATTN, "cascade attention", attn_cascade(a, precise, s));
         STAGE(c, K_MERGE, "cascade merge", attn_merge(a, s));
       }
     } else {
@@ -401,21 +434,23 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       a.out = attn;
       STAGE(c, K_ATTN, "attention", simple_attn<TA>(a, s));
     }
-    const TA *attn_r = attn + (size_t)r0 * Hq * hd;
+    const TA *attn_r = attn + (size_t)r0 * Hq * hd * sp;
     float *x_r = x + (size_t)r0 * d;
     if constexpr (kMfma) {
       STAGE(c, K_OPROJ, "output projection",
-            gemm_residual(attn_r, wo, nr, d, Hq * hd, x_r, gpart, s));
+            gemm_residual(attn_r, wo, nr, d, Hq * hd, sp, x_r, gpart, s));
     } else {
       STAGE(c, K_OPROJ, "output projection",
             simple_residual<TA>(attn_r, wo, nr, d, Hq * hd, x_r, s));
     }
     STAGE(c, K_NORM, "ffn norm",
           launch_rmsnorm<TW, TA>(x_r, static_cast<const TW *>(c->ffn_norm[l]), nr, d,
-                                 cf.rms_eps, xn, s));
+                                 cf.rms_eps, xn, sp, s));
     if constexpr (kMfma) {
-      STAGE(c, K_GATEUP, "gate/up projection", gemm_swiglu(xn, wgu, nr, F, d, h, gpart, s));
-      STAGE(c, K_DOWN, "down projection", gemm_residual(h, wdown, nr, d, F, x_r, gpart, s));
+      STAGE(c, K_GATEUP, "gate/up projection",
+            gemm_swiglu(xn, wgu, nr, F, d, sp, h, gpart, s));
+      STAGE(c, K_DOWN, "down projection",
+            gemm_residual(h, wdown, nr, d, F, sp, x_r, gpart, s));
     } else {
       STAGE(c, K_GATEUP, "gate/up projection", simple_swiglu<TA>(xn, wgu, nr, F, d, h, s));
       STAGE(c, K_DOWN, "down projection", simple_residual<TA>(h, wdown, nr, d, F, x_r, s));

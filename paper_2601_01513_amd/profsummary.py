@@ -30,10 +30,11 @@ def _rows(path):
 def _short(name: str) -> str:
     m = re.search(r"(k_[a-z_0-9]+)", name)
     base = m.group(1) if m else name[:40]
-    if "k_attnILi0" in name or "k_attn<0>" in name:
-        base = "k_attn<0> (prefill)"
-    elif "k_attnILi1" in name or "k_attn<1>" in name:
-        base = "k_attn<1> (cascade)"
+    precise = "ELb1E" in name or ", true>" in name
+    if "k_attnILi0" in name or "k_attn<0" in name:
+        base = "k_attn<0> (prefill" + (", precise)" if precise else ")")
+    elif "k_attnILi1" in name or "k_attn<1" in name:
+        base = "k_attn<1> (cascade" + (", precise)" if precise else ")")
     return base
 
 

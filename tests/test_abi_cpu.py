@@ -40,7 +40,8 @@ def test_workspace_size_of_each_workload(cfg):
 
 @pytest.mark.parametrize("field,value", [
     ("n_heads", 5), ("head_dim", 64), ("d_model", 100), ("dtype", 7), ("max_cands", 0),
-    ("max_cands", B.VSR_MAX_CANDS + 1), ("vocab", 0), ("max_prefix", 0), ("d_ff", 96)])
+    ("max_cands", B.VSR_MAX_CANDS + 1), ("vocab", 0), ("max_prefix", 0), ("d_ff", 96),
+    ("split_layers", -1), ("split_layers", W.B1_5.n_layers + 1)])
 def test_invalid_configs_have_no_workspace(field, value):
     _lib()
     c = B.make_config(W.B1_5)
@@ -80,3 +81,21 @@ def test_workspace_grows_with_the_maxima():
     b = B.workspace_size(B.make_config(W.B7, max_prefix=2 * W.B7.n_prefix))
     c = B.workspace_size(B.make_config(W.B7, max_cands=2 * W.B7.n_cands))
     assert b > a and c > a
+
+
+def test_precise_layers_add_their_buffers():
+    """Precise layers need [hi | lo] activation rows and q/k/v remainder
+    planes: the workspace grows with split_layers (and is exactly the fast
+    size at 0); fp32 contexts ignore the field."""
+    _lib()
+    sizes = [B.workspace_size(B.make_config(W.B7, split_layers=s)) for s in (0, 1, 2, 28)]
+    assert sizes[0] < sizes[1] < sizes[2] < sizes[3]
+    f = [B.workspace_size(B.make_config(W.TINY_F32, split_layers=s)) for s in (0, 1)]
+    assert f[0] == f[1]
+
+
+def test_default_precise_layers_follow_depth():
+    assert B.default_split_layers(0) == 0
+    assert B.default_split_layers(1) == 1
+    assert B.default_split_layers(28) == 1
+    assert B.default_split_layers(64) == 2

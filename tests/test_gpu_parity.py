@@ -10,6 +10,11 @@ Sizes: small shapes that span several GEMM / attention tiles with ragged
 tails, the tiny fp32 and 1.5B-class workloads in full, and the 7B / long 7B /
 32B workloads at full width and full prefix / candidate sizes with two layers
 (same launches as the full-depth pass, the oracle finishing in seconds).
+
+bf16 contexts run their first split_layers layers as precise layers (GEMM and
+attention operands carried as fp16 value + remainder); the small cases run
+with none, some and all layers precise so that both kernel variants are
+checked at every shape.
 """
 import sys
 import time
@@ -34,11 +39,11 @@ def _say(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def run_gpu(wl, cand_ids=None, cand_len=None, verifier=None):
+def run_gpu(wl, cand_ids=None, cand_len=None, verifier=None, split_layers=None):
     torch = _torch()
     from paper_2601_01513_amd.binding import Verifier
     cfg = wl.cfg
-    v = verifier or Verifier(cfg, wl.weights, device="cuda")
+    v = verifier or Verifier(cfg, wl.weights, device="cuda", split_layers=split_layers)
     ids = torch.tensor(wl.prefix_ids, dtype=torch.int32, device="cuda") if cfg.n_text else None
     vis = wl.visual if cfg.n_visual else None
     v.prefill(vis, ids)
@@ -98,9 +103,9 @@ GQA7_BF16 = W.VerifierConfig(
     n_prefix=700, n_visual=300, n_cands=8, cand_len=64, ragged=(1, 64))
 
 
-def _case(cfg, seed, lens=None):
+def _case(cfg, seed, lens=None, split=None):
     _torch()
-    _say(f"case: {cfg.name} seed {seed}")
+    _say(f"case: {cfg.name} seed {seed}" + ("" if split is None else f" split_layers {split}"))
     wl = W.make_workload(cfg, seed, device="cuda")
     if lens is not None:
         wl.cand_len = np.asarray(lens, dtype=np.int32)
@@ -115,10 +120,11 @@ def test_tiny_fp32_workload(seed):
     check(wl.cfg, run_gpu(wl), run_oracle(wl), wl.cand_len)
 
 
+@pytest.mark.parametrize("split", [0, 1, 2])
 @pytest.mark.parametrize("seed", [0, 1])
-def test_small_bf16_ragged_with_empty_candidate(seed):
-    wl = _case(SMALL_BF16, seed, lens=[40, 1, 0, 23, 37])
-    check(wl.cfg, run_gpu(wl), run_oracle(wl), wl.cand_len)
+def test_small_bf16_ragged_with_empty_candidate(seed, split):
+    wl = _case(SMALL_BF16, seed, lens=[40, 1, 0, 23, 37], split=split)
+    check(wl.cfg, run_gpu(wl, split_layers=split), run_oracle(wl), wl.cand_len)
 
 
 def test_small_fp32_ragged_gqa():
@@ -128,10 +134,22 @@ def test_small_fp32_ragged_gqa():
     check(cfg, run_gpu(wl), run_oracle(wl), wl.cand_len)
 
 
-@pytest.mark.parametrize("seed", [0, 1, 2])
-def test_gqa7_split_prefix_ragged(seed):
-    wl = _case(GQA7_BF16, seed)
-    check(wl.cfg, run_gpu(wl), run_oracle(wl), wl.cand_len)
+@pytest.mark.parametrize("seed,split", [(0, 0), (1, 1), (2, 2)])
+def test_gqa7_split_prefix_ragged(seed, split):
+    wl = _case(GQA7_BF16, seed, split=split)
+    check(wl.cfg, run_gpu(wl, split_layers=split), run_oracle(wl), wl.cand_len)
+
+
+def test_precise_layers_track_the_oracle_closely():
+    """All layers precise: the remaining error is the fp16 LM-head input and
+    fp32 accumulation order, an order of magnitude inside the tolerance."""
+    wl = _case(GQA7_BF16, 3, split=2)
+    lp_g, sc_g, _, _ = run_gpu(wl, split_layers=2)
+    lp_o, sc_o, _ = run_oracle(wl)
+    valid = np.arange(lp_o.shape[1])[None, :] < np.asarray(wl.cand_len)[:, None]
+    err = np.abs(lp_g - lp_o)[valid]
+    _say(f"  all layers precise: max |dlp| = {err.max():.3e}")
+    assert err.max() <= 2e-3
 
 
 def test_text_only_and_visual_only_prefixes():
@@ -172,10 +190,12 @@ def test_full_1p5b_workload():
 @pytest.mark.timeout(900)
 @pytest.mark.parametrize("cfg", [W.B7, W.B7_LONG, W.B32], ids=["7B", "7B-long", "32B"])
 def test_full_width_two_layers(cfg):
+    """Layer 0 precise, layer 1 fast: both attention and GEMM variants at the
+    full widths and sizes."""
     cfg2 = cfg.replace(name=cfg.name + " (2 layers)", n_layers=2)
-    wl = _case(cfg2, 0)
+    wl = _case(cfg2, 0, split=1)
     t0 = time.time()
-    gpu = run_gpu(wl)
+    gpu = run_gpu(wl, split_layers=1)
     _say(f"  gpu done in {time.time() - t0:.1f}s, running oracle (fp32)")
     t0 = time.time()
     ora = run_oracle(wl, dtype=np.float32)
