@@ -162,8 +162,12 @@ void vsr_destroy(vsr_ctx *ctx);
 #define VSR_STAGE_KINDS 14
 #define VSR_STAGES (2 * VSR_STAGE_KINDS)
 
-/* Turns stage timing on (1) or off (0); clears what was recorded. */
-int vsr_profile_enable(vsr_ctx *ctx, int enable);
+/* Times the stage kinds whose bits are set in kinds (bit k: kind k, in both
+ * passes; VSR_PROFILE_ALL: every kind; 0: timing off) and clears what was
+ * recorded. Each timed launch adds two event records to the stream, so a
+ * benchmark that times few kinds perturbs the pass least. */
+#define VSR_PROFILE_ALL ((1 << VSR_STAGE_KINDS) - 1)
+int vsr_profile_enable(vsr_ctx *ctx, int kinds);
 
 /* Waits for the recorded launches, then writes, for every stage, the summed
  * kernel time in milliseconds (ms, HOST [VSR_STAGES]) and the number of

@@ -23,6 +23,7 @@ EXPORTS = ["vsr_workspace_size", "vsr_create", "vsr_load_weights", "vsr_prefill"
 
 VSR_STAGE_KINDS = 14
 VSR_STAGES = 2 * VSR_STAGE_KINDS
+VSR_PROFILE_ALL = (1 << VSR_STAGE_KINDS) - 1
 STAGE_KINDS = ["embed", "rmsnorm", "qkv_rope", "attention", "attn_merge", "o_proj",
                "gate_up_swiglu", "down_proj", "lm_inputs", "lm_head_lse", "lse_gather",
                "sum_argmax", "row_tables", "copy"]
@@ -185,9 +186,13 @@ class Verifier:
                                        _ptr(sc), _ptr(am)))
         return lp, sc, am
 
-    def profile(self, enable: bool):
-        """Turns per-stage kernel timing on or off (clears recorded launches)."""
-        self._check(self.lib.vsr_profile_enable(self.h, 1 if enable else 0))
+    def profile(self, enable, kinds=None):
+        """Turns per-stage kernel timing on or off (clears recorded launches).
+        `kinds`: stage-kind names (STAGE_KINDS) to time; default all."""
+        mask = 0
+        if enable:
+            mask = VSR_PROFILE_ALL if kinds is None else sum(1 << STAGE_KINDS.index(k) for k in kinds)
+        self._check(self.lib.vsr_profile_enable(self.h, mask))
 
     def profile_read(self) -> Dict[str, tuple]:
         """{stage name: (summed ms, launches)} since the last read."""

@@ -168,7 +168,7 @@ struct vsr_ctx {
     int stage;
     hipEvent_t a, b;
   };
-  bool prof = false;
+  int prof = 0;  // bitmask of the stage kinds being timed
   int phase = 0;  // 0 prefix pass, 1 candidate pass
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
@@ -225,13 +225,14 @@ static_assert(K_COPY + 1 == VSR_STAGE_KINDS, "stage kinds");
 #define STAGE(ctx, kind, name, ...)                                                     \
   do {                                                                                  \
     hipEvent_t a_ = nullptr;                                                            \
-    if ((ctx)->prof) {                                                                  \
+    const bool timed_ = ((ctx)->prof >> (kind)) & 1;                                    \
+    if (timed_) {                                                                       \
       a_ = (ctx)->event();                                                              \
       if (!a_) return (ctx)->fail(VSR_EHIP, "hipEventCreate failed");                   \
       HIPCHECK(ctx, "profile event", hipEventRecord(a_, (ctx)->stream));                \
     }                                                                                   \
     HIPCHECK(ctx, name, (__VA_ARGS__));                                                 \
-    if ((ctx)->prof) {                                                                  \
+    if (timed_) {                                                                       \
       hipEvent_t b_ = (ctx)->event();                                                   \
       if (!b_) return (ctx)->fail(VSR_EHIP, "hipEventCreate failed");                   \
       HIPCHECK(ctx, "profile event", hipEventRecord(b_, (ctx)->stream));                \
@@ -591,11 +592,12 @@ extern "C" const char *vsr_last_error(const vsr_ctx *ctx) {
 
 extern "C" void vsr_destroy(vsr_ctx *ctx) { delete ctx; }
 
-extern "C" int vsr_profile_enable(vsr_ctx *ctx, int enable) {
+extern "C" int vsr_profile_enable(vsr_ctx *ctx, int kinds) {
   if (!ctx) return VSR_EINVAL;
+  if (kinds & ~VSR_PROFILE_ALL) return ctx->fail(VSR_EINVAL, "profile_enable: unknown stage kinds");
   if (!ctx->recs.empty()) HIPCHECK(ctx, "profile sync", hipStreamSynchronize(ctx->stream));
   ctx->drop_records();
-  ctx->prof = enable != 0;
+  ctx->prof = kinds;
   return VSR_OK;
 }
 
