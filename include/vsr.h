@@ -144,8 +144,51 @@ int vsr_score(vsr_ctx *ctx, const int32_t *cand_ids, const int32_t *cand_len,
               int32_t M, int32_t Cmax, float *logprobs, float *scores,
               int32_t *argmax);
 
+/* Stage 1 of the two-stage verification (Section 3.2, Eq. 11-13): the
+ * reliability of M drafts against the current prefix. Branch m (the draft's
+ * answer, entity and reasoning tokens followed by the verification prompt)
+ * runs after the prefix at positions P.. exactly like a scored candidate;
+ * at its last token the verifier's next-token distribution gives
+ *   lp_yes_no[m] = (log p(yes_id), log p(no_id))            (Eq. 11)
+ *   rel[m]       = p_yes / (p_yes + p_no)                   (Eq. 12)
+ *   keep[m]      = rel[m] >= max_j rel[j] - delta ? 1 : 0   (Eq. 13, A_H)
+ *   branch_ids : device [M][Cmax] int32 (out-of-range ids read as id 0);
+ *   branch_len : HOST [M] int32, each in [1, Cmax] (a branch needs a last token);
+ *   yes_id, no_id in [0, vocab); delta finite and >= 0;
+ *   lp_yes_no  : device [M][2] float out; rel : device [M] float out;
+ *   keep       : device [M] int32 out.
+ * 1 <= M <= max_cands, 1 <= Cmax <= max_cand_len. Uses the same workspace
+ * buffers as vsr_score (the two calls may be interleaved freely). */
+int vsr_reliability(vsr_ctx *ctx, const int32_t *branch_ids, const int32_t *branch_len,
+                    int32_t M, int32_t Cmax, int32_t yes_id, int32_t no_id, float delta,
+                    float *lp_yes_no, float *rel, int32_t *keep);
+
+/* Stage 2 and the final choice (Section 3.2, Eq. 14-15; Algorithm 1; the
+ * strategies compared in Table 3). No context: the inputs are CLIP
+ * embeddings, not verifier state.
+ *   ent    : device [M][D] float, one entity embedding per draft;
+ *   frames : device [NF][D] float, one embedding per keyframe;
+ *   rel    : device [M] float, the drafts' reliability (Eq. 12);
+ *   align  : device [M] float out, max_f cos(ent[m], frames[f]) (Eq. 14-15);
+ *            a zero-norm row has similarity 0 with every row;
+ *   choice : device [1] int32 out, the selected draft:
+ *     VSR_SELECT_TWO_STAGE  argmax of align over A_H = {rel >= max rel - delta}
+ *     VSR_SELECT_ADDITION   argmax of rel + align over all drafts
+ *     VSR_SELECT_INVERT     argmax of rel over {align >= max align - delta}
+ *   every argmax takes the lowest index among equal maxima.
+ * 1 <= M <= VSR_MAX_CANDS, NF >= 1, 1 <= D <= 4096, delta finite and >= 0.
+ * Enqueued on hip_stream (NULL = default stream). Errors are reported by
+ * vsr_last_error(NULL). */
+#define VSR_SELECT_TWO_STAGE 0
+#define VSR_SELECT_ADDITION 1
+#define VSR_SELECT_INVERT 2
+int vsr_align_select(const float *ent, const float *frames, int32_t M, int32_t NF, int32_t D,
+                     const float *rel, float delta, int32_t strategy, float *align,
+                     int32_t *choice, void *hip_stream);
+
 /* Message of the last failed call on this context ("" if none). With
- * ctx == NULL: message of the last failed vsr_create on this thread. */
+ * ctx == NULL: message of the last failed vsr_create or vsr_align_select on
+ * this thread. */
 const char *vsr_last_error(const vsr_ctx *ctx);
 
 /* Releases the context (not the workspace or the weights). NULL is a no-op. */

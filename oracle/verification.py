@@ -32,7 +32,8 @@ index among equal maxima.
 Readings (shared with the HIP path): the branch's own tokens follow the
 prefix at positions P.. like a scored candidate; a branch has at least one
 token; delta >= 0; "invert" uses the same delta as its margin (parity of that
-reading unpinned: the paper gives no threshold for it).
+reading unpinned: the paper gives no threshold for it); a zero-norm embedding
+has cosine similarity 0 with everything (the paper's cosine is undefined there).
 """
 from __future__ import annotations
 
@@ -120,10 +121,12 @@ def reliability(cfg, weights: Dict, visual, prefix_ids, branch_ids, branch_len, 
 
 def entity_alignment(ent, frames) -> np.ndarray:
     """Eq. 14-15: for each entity row, the largest cosine similarity with any
-    frame row (float64)."""
+    frame row (float64). A zero-norm row has similarity 0 with every row."""
     e = np.asarray(ent, dtype=np.float64)
     f = np.asarray(frames, dtype=np.float64)
-    sim = (e @ f.T) / np.outer(np.linalg.norm(e, axis=1), np.linalg.norm(f, axis=1))
+    num = e @ f.T
+    den = np.outer(np.linalg.norm(e, axis=1), np.linalg.norm(f, axis=1))
+    sim = np.divide(num, den, out=np.zeros_like(num), where=den > 0)
     return sim.max(axis=1)
 
 

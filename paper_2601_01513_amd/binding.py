@@ -18,8 +18,12 @@ VSR_F32, VSR_BF16 = 0, 1
 VSR_MAX_CANDS = 256
 
 EXPORTS = ["vsr_workspace_size", "vsr_create", "vsr_load_weights", "vsr_prefill",
-           "vsr_score", "vsr_last_error", "vsr_destroy", "vsr_profile_enable",
-           "vsr_profile_read"]
+           "vsr_score", "vsr_reliability", "vsr_align_select", "vsr_last_error", "vsr_destroy",
+           "vsr_profile_enable", "vsr_profile_read"]
+
+VSR_SELECT_TWO_STAGE, VSR_SELECT_ADDITION, VSR_SELECT_INVERT = 0, 1, 2
+SELECT_STRATEGIES = {"two_stage": VSR_SELECT_TWO_STAGE, "addition": VSR_SELECT_ADDITION,
+                     "invert": VSR_SELECT_INVERT}
 
 VSR_STAGE_KINDS = 14
 VSR_STAGES = 2 * VSR_STAGE_KINDS
@@ -81,6 +85,17 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                               ctypes.POINTER(ctypes.c_int32), ctypes.c_int32, ctypes.c_int32,
                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.vsr_score.restype = ctypes.c_int
+    lib.vsr_reliability.argtypes = [ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
+                                    ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                    ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.c_void_p]
+    lib.vsr_reliability.restype = ctypes.c_int
+    lib.vsr_align_select.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                     ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                     ctypes.c_float, ctypes.c_int32, ctypes.c_void_p,
+                                     ctypes.c_void_p, ctypes.c_void_p]
+    lib.vsr_align_select.restype = ctypes.c_int
     lib.vsr_last_error.argtypes = [ctypes.c_void_p]
     lib.vsr_last_error.restype = ctypes.c_char_p
     lib.vsr_destroy.argtypes = [ctypes.c_void_p]
@@ -186,6 +201,27 @@ class Verifier:
                                        _ptr(sc), _ptr(am)))
         return lp, sc, am
 
+    def reliability(self, branch_ids, branch_len: Sequence[int], yes_id: int, no_id: int,
+                    delta: float, out=None):
+        """Stage 1 of the two-stage verification against the current prefix.
+
+        branch_ids: device int32 [M][Cmax]; branch_len: host ints [M], each >= 1.
+        Returns device tensors (lp_yes_no [M][2] f32, rel [M] f32, keep [M]
+        int32), valid once the stream is synchronised.
+        """
+        torch = self._torch
+        M, cmax = int(branch_ids.shape[0]), int(branch_ids.shape[1])
+        lens = (ctypes.c_int32 * M)(*[int(x) for x in branch_len])
+        if out is None:
+            out = (torch.empty((M, 2), dtype=torch.float32, device=self.device),
+                   torch.empty(M, dtype=torch.float32, device=self.device),
+                   torch.empty(M, dtype=torch.int32, device=self.device))
+        lp, rel, keep = out
+        self._check(self.lib.vsr_reliability(self.h, _ptr(branch_ids), lens, M, cmax,
+                                             int(yes_id), int(no_id), float(delta), _ptr(lp),
+                                             _ptr(rel), _ptr(keep)))
+        return lp, rel, keep
+
     def profile(self, enable, kinds=None):
         """Turns per-stage kernel timing on or off (clears recorded launches).
         `kinds`: stage-kind names (STAGE_KINDS) to time; default all."""
@@ -211,6 +247,34 @@ class Verifier:
             self.close()
         except Exception:
             pass
+
+
+def align_select(ent, frames, rel, delta: float, strategy: str = "two_stage", out=None,
+                 stream=None):
+    """Entity alignment (Eq. 14-15) and the final choice (Algorithm 1 or a
+    Table 3 strategy). ent: device f32 [M][D]; frames: device f32 [NF][D];
+    rel: device f32 [M]. Returns device tensors (align [M] f32, choice [1]
+    int32), valid once the stream is synchronised."""
+    import torch
+    lib = load_library()
+    M, D = int(ent.shape[0]), int(ent.shape[1])
+    NF = int(frames.shape[0])
+    if int(frames.shape[1]) != D or int(rel.shape[0]) != M:
+        raise VsrError(VSR_EINVAL, "align_select: shapes of ent, frames and rel disagree")
+    for t in (ent, frames, rel):
+        if t.dtype != torch.float32 or not t.is_contiguous():
+            raise VsrError(VSR_EINVAL, "align_select: contiguous float32 tensors expected")
+    if out is None:
+        out = (torch.empty(M, dtype=torch.float32, device=ent.device),
+               torch.empty(1, dtype=torch.int32, device=ent.device))
+    align, choice = out
+    st = stream if stream is not None else torch.cuda.current_stream(ent.device)
+    rc = lib.vsr_align_select(_ptr(ent), _ptr(frames), M, NF, D, _ptr(rel), float(delta),
+                              SELECT_STRATEGIES[strategy], _ptr(align), _ptr(choice),
+                              st.cuda_stream)
+    if rc != VSR_OK:
+        raise VsrError(rc, lib.vsr_last_error(None).decode())
+    return align, choice
 
 
 def verifier_from_workload(wl, device="cuda", **kw) -> Verifier:

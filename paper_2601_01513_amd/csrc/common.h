@@ -75,6 +75,22 @@ template <typename TW, typename TA>
 hipError_t launch_lm_inputs(const float *x, const float *h_last, const int32_t *row_lo,
                             const TW *g, int T_rows, int d, float eps, TA *y, hipStream_t s);
 
+// LM-head inputs of a reliability call (2M rows): y[b] = norm(x[last row of
+// branch b % M]); lm_tgt[b] = yes_id for b < M, no_id for b >= M.
+template <typename TW, typename TA>
+hipError_t launch_last_inputs(const float *x, const Branches &br, const TW *g, int d, float eps,
+                              int yes_id, int no_id, TA *y, int32_t *lm_tgt, hipStream_t s);
+// Reliability from the LM-head partials of those 2M rows (Eq. 11-13):
+// lp_yes_no[m] = (tgt[m] - lse[m], tgt[M + m] - lse[M + m]),
+// rel[m] = 1 / (1 + exp(lp_no - lp_yes)), keep[m] = rel[m] >= max rel - delta.
+hipError_t launch_reliability_finish(int M, const float2 *part, int nchunks,
+                                     const float *tgt_logit, float delta, float *lp_yes_no,
+                                     float *rel, int32_t *keep, hipStream_t s);
+// Entity alignment and final choice (Eq. 14-15, Algorithm 1, Table 3).
+hipError_t launch_align_select(const float *ent, const float *frames, int M, int NF, int D,
+                               const float *rel, float delta, int strategy, float *align,
+                               int32_t *choice, hipStream_t s);
+
 // Per-row merge of the LM-head partials: lse over the vocabulary chunks,
 // lp = target logit - lse, scattered to logprobs[m][j] (zeros elsewhere).
 hipError_t launch_lse_gather(const Branches &br, const float2 *part, int nchunks,

@@ -164,7 +164,155 @@ hipError_t launch_lm_inputs(const float *x, const float *h_last, const int32_t *
   return hipGetLastError();
 }
 
+// Reliability rows: block b normalises the last row of branch b % M.
+template <typename TW, typename TA>
+__global__ __launch_bounds__(256) void k_last_inputs(const float *x, Branches br, const TW *g,
+                                                     int d, float eps, int yes_id, int no_id,
+                                                     TA *y, int32_t *lm_tgt) {
+  __shared__ float red[4];
+  const int b = blockIdx.x, m = b % br.M;
+  const int t = br.cu[m + 1] - 1;  // every branch has at least one row
+  norm_row(x + (long)t * d, g, d, eps, y + (long)b * d, red);
+  if (threadIdx.x == 0) lm_tgt[b] = b < br.M ? yes_id : no_id;
+}
+
+template <typename TW, typename TA>
+hipError_t launch_last_inputs(const float *x, const Branches &br, const TW *g, int d, float eps,
+                              int yes_id, int no_id, TA *y, int32_t *lm_tgt, hipStream_t s) {
+  k_last_inputs<TW, TA><<<2 * br.M, 256, 0, s>>>(x, br, g, d, eps, yes_id, no_id, y, lm_tgt);
+  return hipGetLastError();
+}
+
 // ----------------------------------------------------- LSE merge and gather
+// Log-sum-exp of LM-head row t (T rows) over its vocabulary chunks, by one
+// wave (fixed order).
+__device__ __forceinline__ float wave_lse(const float2 *part, int nchunks, int T, int t) {
+  const int lane = threadIdx.x & 63;
+  float mx = -INFINITY;
+  for (int c = lane; c < nchunks; c += 64) mx = fmaxf(mx, part[(long)c * T + t].x);
+  mx = wave_max(mx);
+  float sum = 0.f;
+  for (int c = lane; c < nchunks; c += 64) {
+    const float2 p = part[(long)c * T + t];
+    sum += p.y * __expf(p.x - mx);
+  }
+  return mx + __logf(wave_sum(sum));
+}
+
+// One block: wave w handles branches w, w+4, ...; then thread 0 takes the
+// maximum reliability and every thread marks its branches (Eq. 13).
+__global__ __launch_bounds__(256) void k_reliability_finish(int M, const float2 *part,
+                                                            int nchunks, const float *tgt,
+                                                            float delta, float *lp_yes_no,
+                                                            float *rel, int32_t *keep) {
+  __shared__ float r[kMaxCands];
+  __shared__ float best;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int m = w; m < M; m += 4) {
+    const float ly = tgt[m] - wave_lse(part, nchunks, 2 * M, m);
+    const float ln = tgt[M + m] - wave_lse(part, nchunks, 2 * M, M + m);
+    if (lane == 0) {
+      const float v = 1.f / (1.f + expf(ln - ly));
+      lp_yes_no[2 * m] = ly;
+      lp_yes_no[2 * m + 1] = ln;
+      rel[m] = v;
+      r[m] = v;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float b = r[0];
+    for (int m = 1; m < M; ++m) b = fmaxf(b, r[m]);
+    best = b;
+  }
+  __syncthreads();
+  for (int m = threadIdx.x; m < M; m += 256) keep[m] = r[m] >= best - delta ? 1 : 0;
+}
+
+hipError_t launch_reliability_finish(int M, const float2 *part, int nchunks,
+                                     const float *tgt_logit, float delta, float *lp_yes_no,
+                                     float *rel, int32_t *keep, hipStream_t s) {
+  k_reliability_finish<<<1, 256, 0, s>>>(M, part, nchunks, tgt_logit, delta, lp_yes_no, rel,
+                                         keep);
+  return hipGetLastError();
+}
+
+// --------------------------------------------- entity alignment and choice
+// Block m (16 waves): wave w takes frames w, w+16, ...; lanes stride over the
+// D coordinates. cos = (e . f) / (|e| |f|), 0 if either norm is 0.
+__global__ __launch_bounds__(1024) void k_align(const float *ent, const float *frames, int NF,
+                                                int D, float *align) {
+  __shared__ float red[16];
+  const int m = blockIdx.x, w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const float *e = ent + (long)m * D;
+  float ee = 0.f;
+  for (int c = lane; c < D; c += 64) ee += e[c] * e[c];
+  ee = wave_sum(ee);
+  float best = -INFINITY;
+  for (int f = w; f < NF; f += 16) {
+    const float *fr = frames + (long)f * D;
+    float ef = 0.f, ff = 0.f;
+    for (int c = lane; c < D; c += 64) {
+      const float v = fr[c];
+      ef += e[c] * v;
+      ff += v * v;
+    }
+    ef = wave_sum(ef);
+    ff = wave_sum(ff);
+    const float den = sqrtf(ee) * sqrtf(ff);
+    best = fmaxf(best, den > 0.f ? ef / den : 0.f);
+  }
+  if (lane == 0) red[w] = best;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float b = red[0];
+    for (int i = 1; i < 16; ++i) b = fmaxf(b, red[i]);
+    align[m] = b;
+  }
+}
+
+// First index of the largest value among the allowed ones (-1 if none).
+__device__ __forceinline__ int argmax_where(const float *v, const bool *ok, int n) {
+  int best = -1;
+  for (int i = 0; i < n; ++i)
+    if (ok[i] && (best < 0 || v[i] > v[best])) best = i;
+  return best;
+}
+
+__global__ __launch_bounds__(64) void k_choose(const float *rel, const float *align, int M,
+                                               float delta, int strategy, int32_t *choice) {
+  __shared__ float r[kMaxCands], a[kMaxCands], sum[kMaxCands];
+  __shared__ bool ok[kMaxCands];
+  for (int m = threadIdx.x; m < M; m += 64) {
+    r[m] = rel[m];
+    a[m] = align[m];
+    sum[m] = r[m] + a[m];
+  }
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  int best;
+  if (strategy == 1) {  // addition
+    for (int m = 0; m < M; ++m) ok[m] = true;
+    best = argmax_where(sum, ok, M);
+  } else {
+    const float *filt = strategy == 0 ? r : a, *rank = strategy == 0 ? a : r;
+    float mx = filt[0];
+    for (int m = 1; m < M; ++m) mx = fmaxf(mx, filt[m]);
+    for (int m = 0; m < M; ++m) ok[m] = filt[m] >= mx - delta;
+    best = argmax_where(rank, ok, M);
+  }
+  *choice = best;
+}
+
+hipError_t launch_align_select(const float *ent, const float *frames, int M, int NF, int D,
+                               const float *rel, float delta, int strategy, float *align,
+                               int32_t *choice, hipStream_t s) {
+  k_align<<<M, 1024, 0, s>>>(ent, frames, NF, D, align);
+  k_choose<<<1, 64, 0, s>>>(rel, align, M, delta, strategy, choice);
+  return hipGetLastError();
+}
+
+
 // One wave per output slot (m, j); lanes stride over the vocabulary chunks.
 __global__ __launch_bounds__(256) void k_lse_gather(Branches br, const float2 *part,
                                                     int nchunks, const float *tgt_logit,
@@ -179,17 +327,8 @@ __global__ __launch_bounds__(256) void k_lse_gather(Branches br, const float2 *p
     return;
   }
   const int t = br.cu[m] + j;
-  const int T = br.cu[br.M];
-  float mx = -INFINITY;
-  for (int c = lane; c < nchunks; c += 64) mx = fmaxf(mx, part[(long)c * T + t].x);
-  mx = wave_max(mx);
-  float sum = 0.f;
-  for (int c = lane; c < nchunks; c += 64) {
-    const float2 p = part[(long)c * T + t];
-    sum += p.y * __expf(p.x - mx);
-  }
-  sum = wave_sum(sum);
-  if (lane == 0) logprobs[slot] = tgt_logit[t] - (mx + __logf(sum));
+  const float lse = wave_lse(part, nchunks, br.cu[br.M], t);
+  if (lane == 0) logprobs[slot] = tgt_logit[t] - lse;
 }
 
 hipError_t launch_lse_gather(const Branches &br, const float2 *part, int nchunks,
@@ -243,7 +382,10 @@ VSR_INST(bf16)
   template hipError_t launch_rmsnorm<TW, TA>(const float *, const TW *, int, int, float,      \
                                              TA *, int, hipStream_t);                         \
   template hipError_t launch_lm_inputs<TW, TA>(const float *, const float *, const int32_t *, \
-                                               const TW *, int, int, float, TA *, hipStream_t);
+                                               const TW *, int, int, float, TA *, hipStream_t); \
+  template hipError_t launch_last_inputs<TW, TA>(const float *, const Branches &, const TW *, \
+                                                 int, float, int, int, TA *, int32_t *,       \
+                                                 hipStream_t);
 VSR_INST2(float, float)
 VSR_INST2(bf16, f16)
 #undef VSR_INST2

@@ -6,6 +6,7 @@
 #include "vsr.h"
 
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -42,6 +43,7 @@ Split cascade_split(int T, int P, int n_heads, int n_kv) {
 
 struct Plan {
   int kv_npos, bk_npos, max_t, rows_max, rope_npos, lm_chunks;
+  int lm_rows;  // LM-head rows: candidate rows, or 2 per branch (reliability)
   size_t x, xn, q, q_lo, attn, h, kc, vtc, kc_lo, vtc_lo, bk, bvt, bk_lo, bvt_lo, part_acc,
       part_ml, lm_part, tgt, row_lo, row_pos, lm_tgt, rope, h_last, gemm_part, total;
 };
@@ -80,7 +82,8 @@ Plan make_plan(const vsr_config &c) {
   p.kv_npos = (int)align_up(c.max_prefix, 64);
   p.max_t = c.max_cands * c.max_cand_len;
   p.bk_npos = (int)align_up(p.max_t, 64);
-  p.rows_max = std::max(c.max_prefix, p.max_t);
+  p.lm_rows = std::max(p.max_t, 2 * c.max_cands);
+  p.rows_max = std::max(c.max_prefix, p.lm_rows);
   p.rope_npos = p.kv_npos + c.max_cand_len;
   p.lm_chunks = c.dtype == VSR_BF16 ? lmhead_chunks(c.vocab) : 1;
   // Largest partial-row count of the cascade split over every T <= max_t.
@@ -136,11 +139,11 @@ Plan make_plan(const vsr_config &c) {
   p.bvt_lo = take(nprec ? branch_cache : 0);
   p.part_acc = take(part_rows * c.n_kv_heads * hd * 4);
   p.part_ml = take(part_rows * c.n_kv_heads * 8);
-  p.lm_part = take((size_t)p.lm_chunks * p.max_t * 8);
-  p.tgt = take((size_t)p.max_t * 4);
+  p.lm_part = take((size_t)p.lm_chunks * p.lm_rows * 8);
+  p.tgt = take((size_t)p.lm_rows * 4);
   p.row_lo = take((size_t)p.max_t * 4);
   p.row_pos = take((size_t)p.max_t * 4);
-  p.lm_tgt = take((size_t)p.max_t * 4);
+  p.lm_tgt = take((size_t)p.lm_rows * 4);
   p.rope = take((size_t)p.rope_npos * (hd / 2) * 8);
   p.h_last = take(d * 4);
   p.gemm_part = take(gemm_part * 4);
@@ -479,9 +482,11 @@ int prefill_impl(vsr_ctx *c, const void *visual, int nv, const int32_t *ids, int
   return VSR_OK;
 }
 
+// The candidate rows of a score or reliability call through every layer:
+// row tables, embedding, the decoder blocks in cascade mode (residual stream
+// left in x).
 template <typename TW, typename TA>
-int score_impl(vsr_ctx *c, const Branches &br, const int32_t *cand_ids, float *logprobs,
-               float *scores, int32_t *argmax) {
+int branch_forward(vsr_ctx *c, const Branches &br, const int32_t *cand_ids) {
   constexpr bool kMfma = std::is_same<TA, f16>::value;
   const vsr_config &cf = c->cfg;
   const Plan &p = c->plan;
@@ -489,38 +494,86 @@ int score_impl(vsr_ctx *c, const Branches &br, const int32_t *cand_ids, float *l
   hipStream_t s = c->stream;
   int32_t *row_lo = c->at<int32_t>(p.row_lo), *row_pos = c->at<int32_t>(p.row_pos);
   int32_t *lm_tgt = c->at<int32_t>(p.lm_tgt);
+  STAGE(c, K_ROWS, "row tables",
+        launch_row_tables(br, c->P, cand_ids, cf.vocab, row_lo, row_pos, lm_tgt, s));
+  STAGE(c, K_EMBED, "candidate embedding",
+        launch_embed_rows<TW>(lm_tgt, T_rows, static_cast<const TW *>(c->embed), cf.d_model,
+                              c->at<float>(p.x), s));
+  const Split split =
+      kMfma ? cascade_split(T_rows, c->P, cf.n_heads, cf.n_kv_heads) : Split{1, 0};
+  return run_layers<TW, TA>(c, T_rows, 1, split);
+}
+
+// LM head over `rows` prepared input rows (xn) with targets lm_tgt: chunk
+// partials (max, sum exp) and target logits.
+template <typename TW, typename TA>
+int lm_head(vsr_ctx *c, int rows, int *chunks) {
+  constexpr bool kMfma = std::is_same<TA, f16>::value;
+  const vsr_config &cf = c->cfg;
+  const Plan &p = c->plan;
+  hipStream_t s = c->stream;
+  const TA *lm_in = c->at<TA>(p.xn);
+  int32_t *lm_tgt = c->at<int32_t>(p.lm_tgt);
   float2 *lm_part = c->at<float2>(p.lm_part);
   float *tgt = c->at<float>(p.tgt);
+  if constexpr (kMfma) {
+    *chunks = lmhead_chunks(cf.vocab);
+    STAGE(c, K_LMHEAD, "lm head",
+          gemm_lmhead(lm_in, static_cast<const bf16 *>(c->lm_head), rows, cf.vocab,
+                      cf.d_model, lm_tgt, lm_part, tgt, s));
+  } else {
+    *chunks = 1;
+    STAGE(c, K_LMHEAD, "lm head",
+          simple_lmhead<TA>(lm_in, static_cast<const TW *>(c->lm_head), rows, cf.vocab,
+                            cf.d_model, lm_tgt, lm_part, tgt, s));
+  }
+  return VSR_OK;
+}
+
+template <typename TW, typename TA>
+int score_impl(vsr_ctx *c, const Branches &br, const int32_t *cand_ids, float *logprobs,
+               float *scores, int32_t *argmax) {
+  const vsr_config &cf = c->cfg;
+  const Plan &p = c->plan;
+  const int T_rows = br.cu[br.M];
+  hipStream_t s = c->stream;
   int lm_chunks = 1;
   if (T_rows > 0) {
-    STAGE(c, K_ROWS, "row tables",
-             launch_row_tables(br, c->P, cand_ids, cf.vocab, row_lo, row_pos, lm_tgt, s));
-    float *x = c->at<float>(p.x);
-    STAGE(c, K_EMBED, "candidate embedding",
-             launch_embed_rows<TW>(lm_tgt, T_rows, static_cast<const TW *>(c->embed),
-                                   cf.d_model, x, s));
-    const Split split =
-        kMfma ? cascade_split(T_rows, c->P, cf.n_heads, cf.n_kv_heads) : Split{1, 0};
-    const int rc = run_layers<TW, TA>(c, T_rows, 1, split);
+    int rc = branch_forward<TW, TA>(c, br, cand_ids);
     if (rc) return rc;
-    TA *lm_in = c->at<TA>(p.xn);
     STAGE(c, K_LMIN, "lm inputs",
-          launch_lm_inputs<TW, TA>(x, c->at<float>(p.h_last), row_lo,
+          launch_lm_inputs<TW, TA>(c->at<float>(p.x), c->at<float>(p.h_last),
+                                   c->at<int32_t>(p.row_lo),
                                    static_cast<const TW *>(c->final_norm), T_rows, cf.d_model,
-                                   cf.rms_eps, lm_in, s));
-    if constexpr (kMfma) {
-      lm_chunks = lmhead_chunks(cf.vocab);
-      STAGE(c, K_LMHEAD, "lm head",
-            gemm_lmhead(lm_in, static_cast<const bf16 *>(c->lm_head), T_rows, cf.vocab,
-                        cf.d_model, lm_tgt, lm_part, tgt, s));
-    } else {
-      STAGE(c, K_LMHEAD, "lm head",
-            simple_lmhead<TA>(lm_in, static_cast<const TW *>(c->lm_head), T_rows, cf.vocab,
-                              cf.d_model, lm_tgt, lm_part, tgt, s));
-    }
+                                   cf.rms_eps, c->at<TA>(p.xn), s));
+    rc = lm_head<TW, TA>(c, T_rows, &lm_chunks);
+    if (rc) return rc;
   }
-  STAGE(c, K_LSE, "lse gather", launch_lse_gather(br, lm_part, lm_chunks, tgt, logprobs, s));
+  STAGE(c, K_LSE, "lse gather",
+        launch_lse_gather(br, c->at<float2>(p.lm_part), lm_chunks, c->at<float>(p.tgt),
+                          logprobs, s));
   STAGE(c, K_SELECT, "reduce/select", launch_reduce_select(br, logprobs, scores, argmax, s));
+  return VSR_OK;
+}
+
+template <typename TW, typename TA>
+int reliability_impl(vsr_ctx *c, const Branches &br, const int32_t *ids, int yes_id, int no_id,
+                     float delta, float *lp_yes_no, float *rel, int32_t *keep) {
+  const vsr_config &cf = c->cfg;
+  const Plan &p = c->plan;
+  hipStream_t s = c->stream;
+  int rc = branch_forward<TW, TA>(c, br, ids);
+  if (rc) return rc;
+  STAGE(c, K_LMIN, "last-row inputs",
+        launch_last_inputs<TW, TA>(c->at<float>(p.x), br, static_cast<const TW *>(c->final_norm),
+                                   cf.d_model, cf.rms_eps, yes_id, no_id, c->at<TA>(p.xn),
+                                   c->at<int32_t>(p.lm_tgt), s));
+  int chunks = 1;
+  rc = lm_head<TW, TA>(c, 2 * br.M, &chunks);
+  if (rc) return rc;
+  STAGE(c, K_LSE, "reliability",
+        launch_reliability_finish(br.M, c->at<float2>(p.lm_part), chunks, c->at<float>(p.tgt),
+                                  delta, lp_yes_no, rel, keep, s));
   return VSR_OK;
 }
 
@@ -584,6 +637,68 @@ extern "C" int vsr_score(vsr_ctx *ctx, const int32_t *cand_ids, const int32_t *c
   return ctx->cfg.dtype == VSR_BF16
              ? score_impl<bf16, f16>(ctx, br, cand_ids, logprobs, scores, argmax)
              : score_impl<float, float>(ctx, br, cand_ids, logprobs, scores, argmax);
+}
+
+extern "C" int vsr_reliability(vsr_ctx *ctx, const int32_t *branch_ids,
+                               const int32_t *branch_len, int32_t M, int32_t Cmax,
+                               int32_t yes_id, int32_t no_id, float delta, float *lp_yes_no,
+                               float *rel, int32_t *keep) {
+  if (!ctx) return VSR_EINVAL;
+  if (!ctx->prefilled) return ctx->fail(VSR_ESTATE, "reliability before a successful prefill");
+  if (M < 1 || Cmax < 1) return ctx->fail(VSR_EINVAL, "M and Cmax must be >= 1");
+  if (M > ctx->cfg.max_cands)
+    return ctx->fail(VSR_ERANGE, "M = %d exceeds max_cands %d", M, ctx->cfg.max_cands);
+  if (Cmax > ctx->cfg.max_cand_len)
+    return ctx->fail(VSR_ERANGE, "Cmax = %d exceeds max_cand_len %d", Cmax,
+                     ctx->cfg.max_cand_len);
+  if (!branch_ids || !branch_len || !lp_yes_no || !rel || !keep)
+    return ctx->fail(VSR_EINVAL, "reliability: NULL argument");
+  if (yes_id < 0 || yes_id >= ctx->cfg.vocab || no_id < 0 || no_id >= ctx->cfg.vocab)
+    return ctx->fail(VSR_EINVAL, "yes_id and no_id must lie in [0, vocab)");
+  if (!(delta >= 0.f) || !std::isfinite(delta))
+    return ctx->fail(VSR_EINVAL, "delta must be finite and >= 0");
+  Branches br{};
+  br.M = M;
+  br.cmax = Cmax;
+  br.cu[0] = 0;
+  for (int m = 0; m < M; ++m) {
+    if (branch_len[m] < 1 || branch_len[m] > Cmax)
+      return ctx->fail(VSR_EINVAL, "branch_len[%d] = %d outside [1, Cmax]", m, branch_len[m]);
+    br.cu[m + 1] = br.cu[m] + branch_len[m];
+  }
+  const int rc = set_device(ctx);
+  if (rc) return rc;
+  ctx->phase = 1;
+  return ctx->cfg.dtype == VSR_BF16
+             ? reliability_impl<bf16, f16>(ctx, br, branch_ids, yes_id, no_id, delta, lp_yes_no,
+                                           rel, keep)
+             : reliability_impl<float, float>(ctx, br, branch_ids, yes_id, no_id, delta,
+                                              lp_yes_no, rel, keep);
+}
+
+extern "C" int vsr_align_select(const float *ent, const float *frames, int32_t M, int32_t NF,
+                                int32_t D, const float *rel, float delta, int32_t strategy,
+                                float *align, int32_t *choice, void *hip_stream) {
+  g_create_error.clear();
+  const char *msg = nullptr;
+  if (!ent || !frames || !rel || !align || !choice) msg = "align_select: NULL argument";
+  else if (M < 1 || M > VSR_MAX_CANDS) msg = "M must lie in [1, VSR_MAX_CANDS]";
+  else if (NF < 1) msg = "NF must be >= 1";
+  else if (D < 1 || D > 4096) msg = "D must lie in [1, 4096]";
+  else if (!(delta >= 0.f) || !std::isfinite(delta)) msg = "delta must be finite and >= 0";
+  else if (strategy < VSR_SELECT_TWO_STAGE || strategy > VSR_SELECT_INVERT)
+    msg = "unknown selection strategy";
+  if (msg) {
+    g_create_error = msg;
+    return VSR_EINVAL;
+  }
+  const hipError_t e = launch_align_select(ent, frames, M, NF, D, rel, delta, strategy, align,
+                                           choice, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) {
+    g_create_error = std::string("HIP error in align_select: ") + hipGetErrorString(e);
+    return VSR_EHIP;
+  }
+  return VSR_OK;
 }
 
 extern "C" const char *vsr_last_error(const vsr_ctx *ctx) {

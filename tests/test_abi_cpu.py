@@ -99,3 +99,29 @@ def test_default_precise_layers_follow_depth():
     assert B.default_split_layers(1) == 1
     assert B.default_split_layers(28) == 1
     assert B.default_split_layers(64) == 2
+
+
+def test_align_select_rejects_bad_arguments():
+    lib = _lib()
+    ok = dict(ent=0x10000, frames=0x20000, M=4, NF=8, D=16, rel=0x30000, delta=0.05,
+              strategy=B.VSR_SELECT_TWO_STAGE, align=0x40000, choice=0x50000)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return lib.vsr_align_select(a["ent"], a["frames"], a["M"], a["NF"], a["D"], a["rel"],
+                                    a["delta"], a["strategy"], a["align"], a["choice"], None)
+    for bad, word in ((dict(ent=None), b"NULL"), (dict(choice=None), b"NULL"),
+                      (dict(M=0), b"M must"), (dict(M=B.VSR_MAX_CANDS + 1), b"M must"),
+                      (dict(NF=0), b"NF"), (dict(D=0), b"D must"), (dict(D=4097), b"D must"),
+                      (dict(delta=-0.1), b"delta"), (dict(delta=float("nan")), b"delta"),
+                      (dict(delta=float("inf")), b"delta"), (dict(strategy=3), b"strategy"),
+                      (dict(strategy=-1), b"strategy")):
+        assert call(**bad) == B.VSR_EINVAL, bad
+        assert word in lib.vsr_last_error(None), (bad, lib.vsr_last_error(None))
+
+
+def test_reliability_without_context_fails_cleanly():
+    lib = _lib()
+    lens = (ctypes.c_int32 * 1)(1)
+    assert lib.vsr_reliability(None, None, lens, 1, 1, 0, 1, 0.05, None, None, None) == \
+        B.VSR_EINVAL

@@ -117,6 +117,14 @@ def test_alignment_closed_forms():
     np.testing.assert_allclose(a, [0.8, 0.0, 0.0, 1.0], rtol=0, atol=1e-15)
 
 
+def test_zero_norm_rows_have_zero_similarity():
+    frames = np.array([[0.0, 0.0, 0.0], [-1.0, 0.0, 0.0]])
+    ent = np.array([[0.0, 0.0, 0.0], [1.0, 0.0, 0.0], [0.0, 2.0, 0.0]])
+    # row 0: zero entity -> 0 with both; row 1: 0 (zero frame) vs -1 -> 0;
+    # row 2: orthogonal to f1 -> 0.
+    np.testing.assert_array_equal(ov.entity_alignment(ent, frames), [0.0, 0.0, 0.0])
+
+
 def test_alignment_matches_torch_and_is_scale_invariant():
     rng = np.random.default_rng(7)
     ent, frames = rng.normal(size=(6, 32)), rng.normal(size=(10, 32))
