@@ -91,6 +91,41 @@ def measured_traffic(kname):
         return None
 
 
+def time_next_rows(v, cids, lens, dev, reps, log_fn):
+    """The two-stage verification on the same workload, after the timed
+    region: vsr_reliability over the same branches (against the current
+    prefix) and vsr_align_select at M drafts x 64 keyframes x 768 (CLIP
+    ViT-L/14 embedding width), timed with events on the stream."""
+    import numpy as np
+    import torch
+    from paper_2601_01513_amd.binding import align_select
+    M = len(lens)
+    st = torch.cuda.current_stream(dev)
+
+    def timed(fn, n):
+        for _ in range(2):
+            fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(st)
+        for _ in range(n):
+            fn()
+        b.record(st)
+        b.synchronize()
+        return a.elapsed_time(b) / n
+    blens = [max(1, n) for n in lens]
+    rel_ms = timed(lambda: v.reliability(cids, blens, 17, 29, 0.05), reps)
+    rng = np.random.default_rng(0)
+    ent = torch.tensor(rng.normal(size=(M, 768)).astype(np.float32), device=dev)
+    frames = torch.tensor(rng.normal(size=(64, 768)).astype(np.float32), device=dev)
+    rel = torch.rand(M, device=dev)
+    sel_ms = timed(lambda: align_select(ent, frames, rel, 0.05, "two_stage"), 100)
+    log_fn(f"reliability {rel_ms:.3f} ms/call, align_select {sel_ms * 1e3:.1f} us/call")
+    return {"reliability_ms": round(rel_ms, 3),
+            "reliability_tok_s": round(sum(blens) / (rel_ms * 1e-3), 1),
+            "align_select_us": round(sel_ms * 1e3, 2),
+            "align_select_shape": f"M={M} frames=64 D=768"}
+
+
 def cpu_baseline(wl, log_fn):
     """The oracle (float64, shared-prefix mode) on the same workload with 1 and
     2 of its layers; the per-layer cost is extrapolated to the full depth."""
@@ -244,6 +279,7 @@ def main():
                       "score_only_tok_s": round(tokens / (sco / 1e3), 1) if sco else None},
         "roofline": roofline,
     }
+    result["next_rows"] = time_next_rows(v, cids, lens, dev, max(3, args.steps // 2), log)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, log)
     print(json.dumps(result), flush=True)

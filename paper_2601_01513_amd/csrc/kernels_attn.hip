@@ -17,8 +17,10 @@
 // product is permuted to the key order the S^T accumulator leaves in each
 // lane, and the Vt cache stores positions in the matching order (within each
 // aligned group of 16 positions the middle two quarters are swapped), so a
-// lane's V^T operand is one 16-byte LDS read. Softmax runs online in the log2
-// domain in fp32; operands (queries, keys, values, probabilities) are fp16.
+// lane's V^T operand is one 16-byte LDS read. Softmax runs online in fp32:
+// the running maximum is kept on the raw scores and the scale folds into the
+// exponent, exp2(s * c - m * c) with c = log2(e) / sqrt(hd), one FMA per
+// score; operands (queries, keys, values, probabilities) are fp16.
 //
 // The candidate pass may split the prefix keys into chunks (more blocks on the
 // chip); each chunk writes (max, sum, unnormalised output) partials and
@@ -79,7 +81,8 @@ struct Seg {
 struct Lane {
   int tok;   // query token of this lane's row
   int lo;    // SEG_BRANCH: first visible key
-  float m, l;
+  float m;   // running maximum of the raw (unscaled) scores
+  float l;   // running sum of exp2(s * c - m * c)
   f32x16 o[HD / 32];
   const u32x4 *qs;  // fast: the block's query tile in LDS [QT rows][16 chunks]
   int qrow;         // fast: this lane's row in it
@@ -140,33 +143,31 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *st
       s[b] = mfma(kf, qf, s[b]);
     }
   }
-  // Scale (and mask); key of register r of block b: kb + 32b + 8(r/4) + 4h + r%4.
+  // Mask; key of register r of block b: kb + 32b + 8(r/4) + 4h + r%4.
   float mloc = -INFINITY;
 #pragma unroll
   for (int b = 0; b < 2; ++b)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      float v = s[b][r] * scale_log2;
       if constexpr (MASK) {
         const int key = kb + b * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
         bool vis = key < sg.kvalid;
         if (sg.mode == SEG_CAUSAL) vis = vis && key <= L.tok;
         if (sg.mode == SEG_BRANCH) vis = vis && key >= L.lo && key <= L.tok;
-        v = vis ? v : -INFINITY;
+        s[b][r] = vis ? s[b][r] : -INFINITY;
       }
-      s[b][r] = v;
-      mloc = fmaxf(mloc, v);
+      mloc = fmaxf(mloc, s[b][r]);
     }
   mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
   const float mnew = fmaxf(L.m, mloc);
-  const float mref = mnew == -INFINITY ? 0.f : mnew;
+  const float mref = mnew == -INFINITY ? 0.f : -mnew * scale_log2;  // exponent offset
   float psum = 0.f;
   f16x8 p[4], pl[4];
 #pragma unroll
   for (int b = 0; b < 2; ++b)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const float e = __builtin_amdgcn_exp2f(s[b][r] - mref);
+      const float e = __builtin_amdgcn_exp2f(fmaf(s[b][r], scale_log2, mref));
       psum += e;
       const f16 eh = static_cast<f16>(e);
       p[b * 2 + (r >> 3)][r & 7] = eh;
@@ -174,7 +175,7 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *st
     }
   psum += __shfl_xor(psum, 32, 64);
   if (mnew != L.m) {  // rescale only when this lane's running max moved
-    const float alpha = __builtin_amdgcn_exp2f(L.m - mref);
+    const float alpha = __builtin_amdgcn_exp2f(fmaf(L.m, scale_log2, mref));
     L.l *= alpha;
 #pragma unroll
     for (int db = 0; db < HD / 32; ++db) L.o[db] *= alpha;
@@ -332,7 +333,8 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
         for (int j = 0; j < 4; ++j) v[j] = L.o[db][g4 * 4 + j];
         *reinterpret_cast<f32x4 *>(pa + db * 32 + 8 * g4 + 4 * h) = v;
       }
-    if (h == 0) a.part_ml[prow] = make_float2(L.m, L.l);
+    // The merge works in the scaled log2 domain.
+    if (h == 0) a.part_ml[prow] = make_float2(L.m * scale_log2, L.l);
   }
 }
 
