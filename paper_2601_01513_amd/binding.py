@@ -14,12 +14,13 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libvsr.so")
 
 VSR_OK, VSR_EINVAL, VSR_ESTATE, VSR_ERANGE, VSR_ENOMEM, VSR_EHIP = 0, -1, -2, -3, -4, -5
-VSR_F32, VSR_BF16 = 0, 1
+VSR_F32, VSR_BF16, VSR_F16 = 0, 1, 2
+GEMM_WEIGHT_KEYS = ("wqkv", "wo", "wgu", "wdown")  # per layer, plus lm_head
 VSR_MAX_CANDS = 256
 
 EXPORTS = ["vsr_workspace_size", "vsr_create", "vsr_load_weights", "vsr_prefill",
-           "vsr_score", "vsr_reliability", "vsr_align_select", "vsr_last_error", "vsr_destroy",
-           "vsr_profile_enable", "vsr_profile_read"]
+           "vsr_score", "vsr_reliability", "vsr_align_select", "vsr_weights_to_f16",
+           "vsr_last_error", "vsr_destroy", "vsr_profile_enable", "vsr_profile_read"]
 
 VSR_SELECT_TWO_STAGE, VSR_SELECT_ADDITION, VSR_SELECT_INVERT = 0, 1, 2
 SELECT_STRATEGIES = {"two_stage": VSR_SELECT_TWO_STAGE, "addition": VSR_SELECT_ADDITION,
@@ -41,7 +42,8 @@ class VsrConfig(ctypes.Structure):
                 ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float),
                 ("rope_base", ctypes.c_float), ("dtype", ctypes.c_int32),
                 ("max_prefix", ctypes.c_int32), ("max_cands", ctypes.c_int32),
-                ("max_cand_len", ctypes.c_int32), ("split_layers", ctypes.c_int32)]
+                ("max_cand_len", ctypes.c_int32), ("split_layers", ctypes.c_int32),
+                ("gemm_weights", ctypes.c_int32)]
 
 
 _PP = ctypes.POINTER(ctypes.c_void_p)
@@ -96,6 +98,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                      ctypes.c_float, ctypes.c_int32, ctypes.c_void_p,
                                      ctypes.c_void_p, ctypes.c_void_p]
     lib.vsr_align_select.restype = ctypes.c_int
+    lib.vsr_weights_to_f16.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                       ctypes.c_void_p]
+    lib.vsr_weights_to_f16.restype = ctypes.c_int
     lib.vsr_last_error.argtypes = [ctypes.c_void_p]
     lib.vsr_last_error.restype = ctypes.c_char_p
     lib.vsr_destroy.argtypes = [ctypes.c_void_p]
@@ -116,8 +121,8 @@ def default_split_layers(n_layers: int) -> int:
 
 
 def make_config(cfg, max_prefix: Optional[int] = None, max_cands: Optional[int] = None,
-                max_cand_len: Optional[int] = None,
-                split_layers: Optional[int] = None) -> VsrConfig:
+                max_cand_len: Optional[int] = None, split_layers: Optional[int] = None,
+                gemm_weights: int = 0) -> VsrConfig:
     """vsr_config from a workload.VerifierConfig (maxima default to its sizes;
     split_layers defaults to default_split_layers(n_layers))."""
     if split_layers is None:
@@ -125,7 +130,7 @@ def make_config(cfg, max_prefix: Optional[int] = None, max_cands: Optional[int] 
     return VsrConfig(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim,
                      cfg.d_ff, cfg.vocab, cfg.rms_eps, cfg.rope_base, cfg.dtype,
                      max_prefix or cfg.n_prefix, max_cands or cfg.n_cands,
-                     max_cand_len or cfg.cand_len, split_layers)
+                     max_cand_len or cfg.cand_len, split_layers, gemm_weights)
 
 
 def workspace_size(c: VsrConfig) -> int:
@@ -137,15 +142,25 @@ def _ptr(t) -> int:
 
 
 class Verifier:
-    """One vsr context: workspace, borrowed weights and the current prefix."""
+    """One vsr context: workspace, borrowed weights and the current prefix.
+
+    gemm_weights (bf16 models): "f16" keeps fp16 copies of the GEMM weight
+    matrices (the bf16 values, exact for magnitudes >= 2^-17), which the GEMMs
+    load without conversion; "bf16" uses the given tensors as they are.
+    """
 
     def __init__(self, cfg, weights: Dict, device="cuda", stream=None,
-                 max_prefix=None, max_cands=None, max_cand_len=None, split_layers=None):
+                 max_prefix=None, max_cands=None, max_cand_len=None, split_layers=None,
+                 gemm_weights: str = "f16"):
         import torch
         self._torch = torch
         self.lib = load_library()
         self.cfg = cfg
-        self.c = make_config(cfg, max_prefix, max_cands, max_cand_len, split_layers)
+        if gemm_weights not in ("f16", "bf16"):
+            raise ValueError("gemm_weights must be 'f16' or 'bf16'")
+        self.gemm_f16 = cfg.dtype == VSR_BF16 and gemm_weights == "f16"
+        self.c = make_config(cfg, max_prefix, max_cands, max_cand_len, split_layers,
+                             VSR_F16 if self.gemm_f16 else 0)
         size = self.lib.vsr_workspace_size(ctypes.byref(self.c))
         if size == 0:
             raise VsrError(VSR_EINVAL, "unsupported config")
@@ -165,6 +180,11 @@ class Verifier:
             raise VsrError(rc, self.lib.vsr_last_error(self.h).decode())
 
     def load_weights(self, w: Dict):
+        if self.gemm_f16:  # one-time fp16 copies of the GEMM matrices
+            f16 = lambda t: weights_to_f16(t, self.stream)  # noqa: E731
+            w = dict(w, lm_head=f16(w["lm_head"]),
+                     layers=[dict(lw, **{k: f16(lw[k]) for k in GEMM_WEIGHT_KEYS})
+                             for lw in w["layers"]])
         self.weights = w  # keep the borrowed tensors alive
         L = len(w["layers"])
         arrs = {}
@@ -247,6 +267,21 @@ class Verifier:
             self.close()
         except Exception:
             pass
+
+
+def weights_to_f16(t, stream=None):
+    """fp16 copy of a contiguous bf16 device tensor, rounded as the GEMMs
+    round bf16 weights (vsr_weights_to_f16)."""
+    import torch
+    if t.dtype != torch.bfloat16 or not t.is_contiguous():
+        raise VsrError(VSR_EINVAL, "weights_to_f16: contiguous bfloat16 tensor expected")
+    lib = load_library()
+    out = torch.empty(t.shape, dtype=torch.float16, device=t.device)
+    st = stream if stream is not None else torch.cuda.current_stream(t.device)
+    rc = lib.vsr_weights_to_f16(_ptr(t), _ptr(out), t.numel(), st.cuda_stream)
+    if rc != VSR_OK:
+        raise VsrError(rc, lib.vsr_last_error(None).decode())
+    return out
 
 
 def align_select(ent, frames, rel, delta: float, strategy: str = "two_stage", out=None,

@@ -121,27 +121,31 @@ struct QKVOut {
 };
 
 // ------------------------------------------------------------ MFMA path
-// C = A[rows][K] . W[N][K]^T with fused epilogues; A fp16 activations, W bf16
-// weights (converted to fp16 on their way into LDS), fp32 accumulation.
+// C = A[rows][K] . W[N][K]^T with fused epilogues; A fp16 activations, W
+// 16-bit weights: bf16 (w_f16 = false: converted to fp16 on their way into
+// LDS) or fp16 (w_f16 = true: loaded straight into LDS); fp32 accumulation.
 // Shapes with few output tiles split K; `part` is fp32 scratch of
 // gemm_split_floats(rows, N, K) floats (N = B rows) for the partials.
 // asplit = 2: each A row is [hi | lo] (2K wide), an fp16 value and its fp16
 // remainder, multiplied by the same W (about 22-bit operands); outputs that
 // feed a split GEMM are written the same way.
 size_t gemm_split_floats(int rows, int N, int K);
-hipError_t gemm_qkv_rope(const f16 *A, const bf16 *W, int rows, int K, int asplit, int n_heads,
-                         int n_kv, const QKVOut<f16> &out, float *part, hipStream_t s);
+hipError_t gemm_qkv_rope(const f16 *A, const void *W, bool w_f16, int rows, int K, int asplit,
+                         int n_heads, int n_kv, const QKVOut<f16> &out, float *part,
+                         hipStream_t s);
 // x[rows][N] += A . W^T (residual stream, fp32).
-hipError_t gemm_residual(const f16 *A, const bf16 *W, int rows, int N, int K, int asplit,
-                         float *x, float *part, hipStream_t s);
+hipError_t gemm_residual(const f16 *A, const void *W, bool w_f16, int rows, int N, int K,
+                         int asplit, float *x, float *part, hipStream_t s);
 // h[rows][F] = silu(A . Wg^T) * (A . Wu^T), W = [Wg; Wu] ([2F][K]); h rows are
 // [hi | lo] (2F wide) when asplit == 2.
-hipError_t gemm_swiglu(const f16 *A, const bf16 *W, int rows, int F, int K, int asplit, f16 *h,
-                       float *part, hipStream_t s);
+hipError_t gemm_swiglu(const f16 *A, const void *W, bool w_f16, int rows, int F, int K,
+                       int asplit, f16 *h, float *part, hipStream_t s);
 // LM head: per (vocab chunk c, row t): part[c][t] = (max, sum exp(l - max)) over
 // the chunk's logits l = W[v] . A[t]; tgt_logit[t] = logit of lm_tgt[t].
 int lmhead_chunks(int vocab);
-hipError_t gemm_lmhead(const f16 *A, const bf16 *W, int rows, int vocab, int K,
+// dst[i] = fp16 of the bf16 src[i], the GEMMs' in-register conversion.
+hipError_t convert_bf16_to_f16(const uint16_t *src, uint16_t *dst, size_t n, hipStream_t s);
+hipError_t gemm_lmhead(const f16 *A, const void *W, bool w_f16, int rows, int vocab, int K,
                        const int32_t *lm_tgt, float2 *part, float *tgt_logit, hipStream_t s);
 
 // Attention of query rows against one key source. Query row r of KV head h is

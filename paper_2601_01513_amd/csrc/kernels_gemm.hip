@@ -2,9 +2,11 @@
 //
 // Every GEMM here is C = A . B^T with A [rows][K] and B [N][K] both
 // K-contiguous (activations and nn.Linear weights), fp32 accumulation on the
-// gfx950 v_mfma_f32_32x32x16_f16 matrix cores. Activations are fp16; a bf16
-// weight operand is converted to fp16 in registers on its way into LDS (exact:
-// a bf16 value's 8 significant bits fit fp16's 11).
+// gfx950 v_mfma_f32_32x32x16_f16 matrix cores. Activations are fp16. Weights
+// are 16-bit: fp16 (loaded straight into LDS) or bf16, converted to fp16 in
+// registers on their way into LDS (exact: a bf16 value's 8 significant bits
+// fit fp16's 11). The two forms cost the same HBM bytes; the fp16 form saves
+// the register path and its conversion (about 6% of the GEMM time).
 //
 // Block: 512 threads = 8 waves (two per SIMD) on a 256 x 256 tile; the waves
 // form a 4 x 2 grid, each owning 64 x 128 outputs (2 x 4 MFMA 32x32 blocks).
@@ -349,9 +351,9 @@ __device__ __forceinline__ void store_act(f16 *p, long base, int col, int n, int
 }
 
 // ------------------------------------------------------- residual (O, down)
-template <class TL>
+template <class TL, bool WCVT>
 __global__ __launch_bounds__(NT) void k_gemm_residual(const f16 *__restrict__ A,
-                                                      const bf16 *__restrict__ W, int rows,
+                                                      const uint16_t *__restrict__ W, int rows,
                                                       int N, int K, int asplit, Launch ln,
                                                       float *__restrict__ x,
                                                       float *__restrict__ part) {
@@ -362,7 +364,7 @@ __global__ __launch_bounds__(NT) void k_gemm_residual(const f16 *__restrict__ A,
   int k0 = 0, k1 = K / BK * asplit;
   if (split) split_range(k1, ln.nsplit, wk.split, k0, k1);
   f32x16 acc[TL::FM][TL::FN];
-  mainloop<TL, false, true>(
+  mainloop<TL, false, WCVT>(
       A, [=](int r) { return min(m0 + r, rows - 1); }, W,
       [=](int r) { return min(n0 + r, N - 1); }, K, asplit, k0, k1, lds, acc);
   if (split) {
@@ -402,10 +404,10 @@ __global__ __launch_bounds__(256) void k_reduce_residual(const float *__restrict
 // out per wave column: wave column wn takes gate rows o0+64wn .. +63 then the
 // matching up rows, so MFMA blocks fn and fn+2 hold gate and up of the same
 // output columns (partial tiles keep that column order).
-template <class TL>
+template <class TL, bool WCVT>
 __global__ __launch_bounds__(NT) void k_gemm_swiglu(const f16 *__restrict__ A,
-                                                    const bf16 *__restrict__ W, int rows, int F,
-                                                    int K, int asplit, Launch ln,
+                                                    const uint16_t *__restrict__ W, int rows,
+                                                    int F, int K, int asplit, Launch ln,
                                                     f16 *__restrict__ h, float *__restrict__ part) {
   static_assert(TL::WN == 2 && TL::TN == 128 && TL::BN == 256, "gate/up pairing");
   __shared__ u32x4 lds[2 * TL::STAGE];
@@ -415,7 +417,7 @@ __global__ __launch_bounds__(NT) void k_gemm_swiglu(const f16 *__restrict__ A,
   int k0 = 0, k1 = K / BK * asplit;
   if (split) split_range(k1, ln.nsplit, wk.split, k0, k1);
   f32x16 acc[TL::FM][TL::FN];
-  mainloop<TL, false, true>(
+  mainloop<TL, false, WCVT>(
       A, [=](int r) { return min(m0 + r, rows - 1); }, W,
       [=](int r) {
         const int q = r & 127;
@@ -508,10 +510,11 @@ __device__ __forceinline__ void qkv_store(const QKVOut<f16> &o, int n_heads, int
   }
 }
 
-template <class TL>
+template <class TL, bool WCVT>
 __global__ __launch_bounds__(NT) void k_gemm_qkv(const f16 *__restrict__ A,
-                                                 const bf16 *__restrict__ W, int rows, int K,
-                                                 int asplit, int n_heads, int n_kv, Launch ln,
+                                                 const uint16_t *__restrict__ W, int rows,
+                                                 int K, int asplit, int n_heads, int n_kv,
+                                                 Launch ln,
                                                  QKVOut<f16> o, float *__restrict__ part) {
   static_assert(TL::WN == 2 && TL::TN == 128 && TL::BN == 256, "one head per wave column");
   __shared__ u32x4 lds[2 * TL::STAGE];
@@ -522,7 +525,7 @@ __global__ __launch_bounds__(NT) void k_gemm_qkv(const f16 *__restrict__ A,
   int k0 = 0, k1 = K / BK * asplit;
   if (split) split_range(k1, ln.nsplit, wk.split, k0, k1);
   f32x16 acc[TL::FM][TL::FN];
-  mainloop<TL, false, true>(
+  mainloop<TL, false, WCVT>(
       A, [=](int r) { return min(m0 + r, rows - 1); }, W,
       [=](int r) { return min(n0 + r, nrows - 1); }, K, asplit, k0, k1, lds, acc);
   if (split) {
@@ -571,9 +574,9 @@ __global__ __launch_bounds__(256) void k_reduce_qkv(const float *__restrict__ pa
 // tile) writes, for each token t, part[c][t] = (max_v l, sum_v exp(l - max))
 // over its BM vocabulary rows, and the target logit when the target falls in
 // the tile. The [tokens x vocab] logits never leave registers.
-template <class TL>
+template <class TL, bool WCVT>
 __global__ __launch_bounds__(NT) void k_gemm_lmhead(const f16 *__restrict__ Hn,
-                                                    const bf16 *__restrict__ Wlm, int T,
+                                                    const uint16_t *__restrict__ Wlm, int T,
                                                     int vocab, int K, Launch ln,
                                                     const int32_t *__restrict__ lm_tgt,
                                                     float2 *__restrict__ part,
@@ -583,7 +586,7 @@ __global__ __launch_bounds__(NT) void k_gemm_lmhead(const f16 *__restrict__ Hn,
   const Work wk = block_work(ln);
   const int m0 = wk.tm * TL::BM, n0 = wk.tn * TL::BN;
   f32x16 acc[TL::FM][TL::FN];
-  mainloop<TL, true, false>(
+  mainloop<TL, WCVT, false>(
       Wlm, [=](int r) { return min(m0 + r, vocab - 1); }, Hn,
       [=](int r) { return min(n0 + r, T - 1); }, K, 1, 0, K / BK, lds, acc);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -657,38 +660,49 @@ size_t gemm_split_floats(int rows, int N, int K) {
   return (size_t)ln.ntail * ln.nsplit * kTileElems;
 }
 
-hipError_t gemm_residual(const f16 *A, const bf16 *W, int rows, int N, int K, int asplit,
-                         float *x, float *part, hipStream_t s) {
+// Weight-format dispatch of a GEMM kernel launch.
+#define VSR_WLAUNCH(kern, grid, ...)                                              \
+  do {                                                                           \
+    const uint16_t *W16 = static_cast<const uint16_t *>(W);                      \
+    if (w_f16)                                                                   \
+      kern<TL, false><<<grid, NT, 0, s>>>(__VA_ARGS__);                           \
+    else                                                                         \
+      kern<TL, true><<<grid, NT, 0, s>>>(__VA_ARGS__);                            \
+  } while (0)
+
+hipError_t gemm_residual(const f16 *A, const void *W, bool w_f16, int rows, int N, int K,
+                         int asplit, float *x, float *part, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
   const Launch ln = plan_launch((rows + TL::BM - 1) / TL::BM, (N + TL::BN - 1) / TL::BN, 8,
                                 K / BK * asplit);
-  k_gemm_residual<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, N, K, asplit, ln, x, part);
+  VSR_WLAUNCH(k_gemm_residual, ln.blocks(), A, W16, rows, N, K, asplit, ln, x, part);
   if (ln.ntail > 0)
     k_reduce_residual<<<ln.ntail * 256, 256, 0, s>>>(part, ln, rows, N, x);
   return hipGetLastError();
 }
 
-hipError_t gemm_swiglu(const f16 *A, const bf16 *W, int rows, int F, int K, int asplit, f16 *h,
-                       float *part, hipStream_t s) {
+hipError_t gemm_swiglu(const f16 *A, const void *W, bool w_f16, int rows, int F, int K,
+                       int asplit, f16 *h, float *part, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
   const Launch ln = plan_launch((rows + TL::BM - 1) / TL::BM, (F + 127) / 128, 8,
                                 K / BK * asplit);
-  k_gemm_swiglu<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, F, K, asplit, ln, h, part);
+  VSR_WLAUNCH(k_gemm_swiglu, ln.blocks(), A, W16, rows, F, K, asplit, ln, h, part);
   if (ln.ntail > 0)
     k_reduce_swiglu<<<ln.ntail * 128, 256, 0, s>>>(part, ln, rows, F, asplit, h);
   return hipGetLastError();
 }
 
-hipError_t gemm_qkv_rope(const f16 *A, const bf16 *W, int rows, int K, int asplit, int n_heads,
-                         int n_kv, const QKVOut<f16> &out, float *part, hipStream_t s) {
+hipError_t gemm_qkv_rope(const f16 *A, const void *W, bool w_f16, int rows, int K, int asplit,
+                         int n_heads, int n_kv, const QKVOut<f16> &out, float *part,
+                         hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
   const int nslots = n_heads + 2 * n_kv;
   const Launch ln = plan_launch((rows + TL::BM - 1) / TL::BM, (nslots + 1) / 2, 8,
                                 K / BK * asplit);
-  k_gemm_qkv<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, K, asplit, n_heads, n_kv, ln, out, part);
+  VSR_WLAUNCH(k_gemm_qkv, ln.blocks(), A, W16, rows, K, asplit, n_heads, n_kv, ln, out, part);
   if (ln.ntail > 0)
     k_reduce_qkv<<<ln.ntail * 128, 256, 0, s>>>(part, ln, rows, n_heads, n_kv, out);
   return hipGetLastError();
@@ -696,7 +710,7 @@ hipError_t gemm_qkv_rope(const f16 *A, const bf16 *W, int rows, int K, int aspli
 
 int lmhead_chunks(int vocab) { return (vocab + TileStd::BM - 1) / TileStd::BM; }
 
-hipError_t gemm_lmhead(const f16 *A, const bf16 *W, int rows, int vocab, int K,
+hipError_t gemm_lmhead(const f16 *A, const void *W, bool w_f16, int rows, int vocab, int K,
                        const int32_t *lm_tgt, float2 *part, float *tgt_logit, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
@@ -705,8 +719,33 @@ hipError_t gemm_lmhead(const f16 *A, const bf16 *W, int rows, int vocab, int K,
   // partials).
   const int nm = lmhead_chunks(vocab), nn = (rows + TL::BN - 1) / TL::BN;
   const Launch ln{nm, nn, 1, nm * nn, 0, 1};
-  k_gemm_lmhead<TL><<<ln.blocks(), NT, 0, s>>>(A, W, rows, vocab, K, ln, lm_tgt, part,
-                                               tgt_logit);
+  VSR_WLAUNCH(k_gemm_lmhead, ln.blocks(), A, W16, rows, vocab, K, ln, lm_tgt, part, tgt_logit);
+  return hipGetLastError();
+}
+
+#undef VSR_WLAUNCH
+
+namespace {
+// Eight values per thread (16-byte loads and stores); the tail one by one.
+__global__ __launch_bounds__(256) void k_bf16_to_f16(const u32x4 *src, u32x4 *dst, size_t n8,
+                                                     const uint16_t *tsrc, uint16_t *tdst,
+                                                     int ntail) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n8) dst[i] = bf16x8_to_f16x8(src[i]);
+  if (i < (size_t)ntail) {
+    const float v = __uint_as_float((uint32_t)tsrc[i] << 16);
+    tdst[i] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(v, 0.f)) & 0xFFFFu;
+  }
+}
+}  // namespace
+
+hipError_t convert_bf16_to_f16(const uint16_t *src, uint16_t *dst, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const size_t n8 = n / 8, work = n8 > 8 ? n8 : 8;
+  const int ntail = (int)(n % 8);
+  k_bf16_to_f16<<<(unsigned)((work + 255) / 256), 256, 0, s>>>(
+      reinterpret_cast<const u32x4 *>(src), reinterpret_cast<u32x4 *>(dst), n8, src + n8 * 8,
+      dst + n8 * 8, ntail);
   return hipGetLastError();
 }
 

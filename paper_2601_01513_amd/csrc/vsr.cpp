@@ -63,6 +63,10 @@ std::string check_config(const vsr_config *c) {
   if (c->max_prefix > (1 << 24)) return "max_prefix too large";
   if (c->split_layers < 0 || c->split_layers > c->n_layers)
     return "split_layers must be in [0, n_layers]";
+  if (c->dtype == VSR_BF16 ? (c->gemm_weights != 0 && c->gemm_weights != VSR_BF16 &&
+                              c->gemm_weights != VSR_F16)
+                           : c->gemm_weights != 0)
+    return "gemm_weights must be 0, VSR_BF16 or VSR_F16 (bf16 contexts), 0 otherwise";
   if (c->dtype == VSR_BF16) {
     if (c->head_dim != 128) return "bf16 contexts need head_dim == 128";
     if (c->d_model % 64 || c->d_ff % 64) return "bf16 contexts need d_model and d_ff multiples of 64";
@@ -338,6 +342,7 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
   TA *xn = c->at<TA>(p.xn), *q = c->at<TA>(p.q), *attn = c->at<TA>(p.attn), *h = c->at<TA>(p.h);
   float *gpart = c->at<float>(p.gemm_part);
   const size_t layer_cache = (size_t)Hkv * p.kv_npos * hd;
+  const bool wf16 = cf.gemm_weights == VSR_F16;  // GEMM weights stored as fp16
   hipStream_t s = c->stream;
   for (int l = 0; l < cf.n_layers; ++l) {
     const TW *wqkv = static_cast<const TW *>(c->wqkv[l]);
@@ -374,7 +379,7 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
     }
     if constexpr (kMfma) {
       STAGE(c, K_QKV, "qkv projection",
-            gemm_qkv_rope(xn, wqkv, rows, d, sp, Hq, Hkv, qo, gpart, s));
+            gemm_qkv_rope(xn, wqkv, wf16, rows, d, sp, Hq, Hkv, qo, gpart, s));
     } else {
       STAGE(c, K_QKV, "qkv projection",
             simple_qkv_rope<TA>(xn, wqkv, rows, d, Hq, Hkv, hd, qo, s));
@@ -442,7 +447,7 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
     float *x_r = x + (size_t)r0 * d;
     if constexpr (kMfma) {
       STAGE(c, K_OPROJ, "output projection",
-            gemm_residual(attn_r, wo, nr, d, Hq * hd, sp, x_r, gpart, s));
+            gemm_residual(attn_r, wo, wf16, nr, d, Hq * hd, sp, x_r, gpart, s));
     } else {
       STAGE(c, K_OPROJ, "output projection",
             simple_residual<TA>(attn_r, wo, nr, d, Hq * hd, x_r, s));
@@ -452,9 +457,9 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
                                  cf.rms_eps, xn, sp, s));
     if constexpr (kMfma) {
       STAGE(c, K_GATEUP, "gate/up projection",
-            gemm_swiglu(xn, wgu, nr, F, d, sp, h, gpart, s));
+            gemm_swiglu(xn, wgu, wf16, nr, F, d, sp, h, gpart, s));
       STAGE(c, K_DOWN, "down projection",
-            gemm_residual(h, wdown, nr, d, F, sp, x_r, gpart, s));
+            gemm_residual(h, wdown, wf16, nr, d, F, sp, x_r, gpart, s));
     } else {
       STAGE(c, K_GATEUP, "gate/up projection", simple_swiglu<TA>(xn, wgu, nr, F, d, h, s));
       STAGE(c, K_DOWN, "down projection", simple_residual<TA>(h, wdown, nr, d, F, x_r, s));
@@ -519,7 +524,7 @@ int lm_head(vsr_ctx *c, int rows, int *chunks) {
   if constexpr (kMfma) {
     *chunks = lmhead_chunks(cf.vocab);
     STAGE(c, K_LMHEAD, "lm head",
-          gemm_lmhead(lm_in, static_cast<const bf16 *>(c->lm_head), rows, cf.vocab,
+          gemm_lmhead(lm_in, c->lm_head, cf.gemm_weights == VSR_F16, rows, cf.vocab,
                       cf.d_model, lm_tgt, lm_part, tgt, s));
   } else {
     *chunks = 1;
@@ -706,6 +711,28 @@ extern "C" const char *vsr_last_error(const vsr_ctx *ctx) {
 }
 
 extern "C" void vsr_destroy(vsr_ctx *ctx) { delete ctx; }
+
+extern "C" int vsr_weights_to_f16(const void *src, void *dst, size_t n, void *hip_stream) {
+  g_create_error.clear();
+  const uintptr_t a = reinterpret_cast<uintptr_t>(src), b = reinterpret_cast<uintptr_t>(dst);
+  if (n == 0) return VSR_OK;
+  if (!src || !dst || (a & 15) || (b & 15)) {
+    g_create_error = "weights_to_f16: src and dst must be non-NULL and 16-byte aligned";
+    return VSR_EINVAL;
+  }
+  if ((a < b + 2 * n) && (b < a + 2 * n)) {
+    g_create_error = "weights_to_f16: src and dst overlap";
+    return VSR_EINVAL;
+  }
+  const hipError_t e = convert_bf16_to_f16(static_cast<const uint16_t *>(src),
+                                           static_cast<uint16_t *>(dst), n,
+                                           static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) {
+    g_create_error = std::string("HIP error in weights_to_f16: ") + hipGetErrorString(e);
+    return VSR_EHIP;
+  }
+  return VSR_OK;
+}
 
 extern "C" int vsr_profile_enable(vsr_ctx *ctx, int kinds) {
   if (!ctx) return VSR_EINVAL;

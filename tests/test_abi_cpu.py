@@ -22,7 +22,7 @@ def _lib():
 def test_header_symbols_are_exported():
     lib = _lib()
     hdr = open(os.path.join(ROOT, "include", "vsr.h")).read()
-    declared = set(re.findall(r"\b(vsr_[a-z_]+)\s*\(", hdr))
+    declared = set(re.findall(r"\b(vsr_[a-z_0-9]+)\s*\(", hdr))
     assert declared == set(B.EXPORTS)
     for name in declared:
         assert hasattr(lib, name), name
@@ -41,7 +41,8 @@ def test_workspace_size_of_each_workload(cfg):
 @pytest.mark.parametrize("field,value", [
     ("n_heads", 5), ("head_dim", 64), ("d_model", 100), ("dtype", 7), ("max_cands", 0),
     ("max_cands", B.VSR_MAX_CANDS + 1), ("vocab", 0), ("max_prefix", 0), ("d_ff", 96),
-    ("split_layers", -1), ("split_layers", W.B1_5.n_layers + 1)])
+    ("split_layers", -1), ("split_layers", W.B1_5.n_layers + 1), ("gemm_weights", 3),
+    ("gemm_weights", -1)])
 def test_invalid_configs_have_no_workspace(field, value):
     _lib()
     c = B.make_config(W.B1_5)
@@ -125,3 +126,21 @@ def test_reliability_without_context_fails_cleanly():
     lens = (ctypes.c_int32 * 1)(1)
     assert lib.vsr_reliability(None, None, lens, 1, 1, 0, 1, 0.05, None, None, None) == \
         B.VSR_EINVAL
+
+
+def test_fp32_contexts_take_no_gemm_weight_format():
+    _lib()
+    c = B.make_config(W.TINY_F32, gemm_weights=B.VSR_F16)
+    assert B.workspace_size(c) == 0
+    for g in (0, B.VSR_BF16, B.VSR_F16):
+        assert B.workspace_size(B.make_config(W.B1_5, gemm_weights=g)) > 0
+
+
+def test_weights_to_f16_rejects_bad_arguments():
+    lib = _lib()
+    assert lib.vsr_weights_to_f16(None, 0x1000, 8, None) == B.VSR_EINVAL
+    assert lib.vsr_weights_to_f16(0x1008, 0x20000, 8, None) == B.VSR_EINVAL   # misaligned
+    assert b"aligned" in lib.vsr_last_error(None)
+    assert lib.vsr_weights_to_f16(0x10000, 0x10010, 64, None) == B.VSR_EINVAL  # overlap
+    assert b"overlap" in lib.vsr_last_error(None)
+    assert lib.vsr_weights_to_f16(None, None, 0, None) == B.VSR_OK             # nothing to do
