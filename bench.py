@@ -172,6 +172,8 @@ def main():
                     help="index into the workload list (default: the 7B-class 4k prefix 8x64)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-next-rows", action="store_true",
+                    help="skip the two-stage verification timings (counter runs)")
     ap.add_argument("--stages", action="store_true", help="print per-stage times to stderr")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device-to-device (counter calibration) and exit")
@@ -279,7 +281,8 @@ def main():
                       "score_only_tok_s": round(tokens / (sco / 1e3), 1) if sco else None},
         "roofline": roofline,
     }
-    result["next_rows"] = time_next_rows(v, cids, lens, dev, max(3, args.steps // 2), log)
+    if not args.no_next_rows:
+        result["next_rows"] = time_next_rows(v, cids, lens, dev, max(3, args.steps // 2), log)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, log)
     print(json.dumps(result), flush=True)
