@@ -233,3 +233,72 @@ def host_weights(weights: Dict, lazy: bool = False) -> Dict:
         "final_norm": to_host_f32(weights["final_norm"]),
         "layers": layers if lazy else list(layers),
     }
+
+
+# ------------------------------------------------------- retrieval-stage inputs
+# Stand-ins for a short video and a CLIP embedding bank (the paper's videos
+# last about 22 s; CLIP ViT-L/14-336 embeds frames of 336 x 336 into 768
+# dimensions). No arithmetic of the method happens here.
+
+@dataclasses.dataclass(frozen=True)
+class RetrievalConfig:
+    name: str
+    n_frames: int      # decoded frames of the video
+    height: int
+    width: int
+    n_scenes: int      # the video cuts between this many scenes
+    n_docs: int        # document embeddings in the bank
+    dim: int           # embedding width
+    k: int             # documents retrieved per keyframe
+    K: int             # documents kept in T*
+    theta: float       # keyframe threshold on the histogram similarity
+
+
+VIDEO_SMALL = RetrievalConfig("small video 40x24x32, 5 scenes, 300 docs", 40, 24, 32, 5, 300,
+                              64, 3, 3, 0.6)
+# About 22 s at 10 frames/s, CLIP-sized frames and embeddings; the paper's
+# collection holds ~156 documents per video, the large bank is a stand-in for
+# a shared knowledge base.
+VIDEO_22S = RetrievalConfig("22 s video 220x336x336, 12 scenes, 156 docs", 220, 336, 336, 12,
+                            156, 768, 3, 3, 0.6)
+VIDEO_22S_BANK = RetrievalConfig("22 s video 220x336x336, 12 scenes, 100k docs", 220, 336, 336,
+                                 12, 100_000, 768, 3, 3, 0.6)
+
+
+def make_video(rc: RetrievalConfig, seed: int) -> np.ndarray:
+    """uint8 frames [NF][H][W][3]: each scene is a random base image with its
+    own colour range; every frame adds small noise and a slow brightness drift
+    (so consecutive frames of a scene are similar, scene cuts are not)."""
+    rng = host_rng(seed, "video")
+    cuts = np.sort(rng.choice(np.arange(1, rc.n_frames), size=rc.n_scenes - 1, replace=False))
+    scene_of = np.searchsorted(cuts, np.arange(rc.n_frames), side="right")
+    bases = []
+    for _ in range(rc.n_scenes):
+        lo = rng.integers(0, 160, size=3)
+        span = rng.integers(20, 96, size=3)
+        bases.append(lo + rng.random((rc.height, rc.width, 3)) * span)
+    out = np.empty((rc.n_frames, rc.height, rc.width, 3), dtype=np.uint8)
+    for i in range(rc.n_frames):
+        b = bases[scene_of[i]]
+        noise = rng.normal(0.0, 2.0, size=b.shape)
+        out[i] = np.clip(b + noise + 0.3 * (i % 7), 0, 255).astype(np.uint8)
+    return out
+
+
+def make_embeddings(n: int, dim: int, seed: int, name: str) -> np.ndarray:
+    """float32 rows N(0, 1) (stand-ins for CLIP embeddings)."""
+    return host_rng(seed, name).normal(size=(n, dim)).astype(np.float32)
+
+
+def make_retrieval(rc: RetrievalConfig, seed: int):
+    """(frames uint8 [NF][H][W][3], frame embeddings [NF][D], document
+    embeddings [ND][D]); a few documents are planted near some frames so
+    that retrieval has clear winners."""
+    frames = make_video(rc, seed)
+    femb = make_embeddings(rc.n_frames, rc.dim, seed, "frame_emb")
+    demb = make_embeddings(rc.n_docs, rc.dim, seed, "doc_emb")
+    rng = host_rng(seed, "planted_docs")
+    for i in range(0, rc.n_frames, max(1, rc.n_frames // 8)):
+        j = int(rng.integers(0, rc.n_docs))
+        demb[j] = femb[i] + 0.5 * rng.normal(size=rc.dim).astype(np.float32)
+    return frames, femb, demb
