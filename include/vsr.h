@@ -195,9 +195,51 @@ int vsr_align_select(const float *ent, const float *frames, int32_t M, int32_t N
                      int32_t *choice, void *hip_stream);
 
 /* Message of the last failed call on this context ("" if none). With
- * ctx == NULL: message of the last failed vsr_create or vsr_align_select on
- * this thread. */
+ * ctx == NULL: message of the last failed context-free call on this thread
+ * (vsr_create, vsr_align_select, vsr_weights_to_f16, vsr_keyframes,
+ * vsr_retrieve). */
 const char *vsr_last_error(const vsr_ctx *ctx);
+
+/* Keyframes of a video (Section 3.1, Eq. 1). Each frame is compared with the
+ * frame before it through colour histograms (64 bins per RGB channel, bin =
+ * value >> 2); the similarity is the histogram intersection
+ * S[i] = sum over channels and bins of min(count_i, count_{i-1}), divided by
+ * 3 H W. Frame 0 and every frame with S[i] < theta * 3 H W (decided in
+ * float64) are keyframes.
+ *   frames  : device uint8 [NF][H][W][3], 16-byte aligned;
+ *   hist    : device int32 [NF][3][64] out, the per-frame counts;
+ *   inter   : device int32 [NF] out, S[i] (S[0] = -1);
+ *   key_idx : device int32 [NF] out, the keyframe indices in order;
+ *   n_keys  : device int32 [1] out, their number (stays on the device).
+ * 1 <= NF <= 65536, H, W >= 1, H W <= 2^24, theta finite. Enqueued on
+ * hip_stream; errors via vsr_last_error(NULL). */
+int vsr_keyframes(const uint8_t *frames, int32_t NF, int32_t H, int32_t W, float theta,
+                  int32_t *hist, int32_t *inter, int32_t *key_idx, int32_t *n_keys,
+                  void *hip_stream);
+
+/* Bytes of device workspace vsr_retrieve needs (0 for invalid sizes). */
+size_t vsr_retrieve_workspace_size(int32_t NF, int32_t ND, int32_t k);
+
+/* Document retrieval for the keyframes (Section 3.1, Eq. 2-3). For keyframe
+ * r (frame key_idx[r], r < n_keys) the k documents with the largest cosine
+ * similarity of embeddings (Eq. 2), then T*: the K best documents of the
+ * union of those lists, each scored by the best similarity it was retrieved
+ * with (Eq. 3). Rankings break ties by the lower document index; a zero-norm
+ * embedding has similarity 0 with everything.
+ *   frame_emb : device float [NF][D] (embeddings of every frame);
+ *   key_idx, n_keys : device, as written by vsr_keyframes;
+ *   docs      : device float [ND][D];
+ *   workspace : device, >= vsr_retrieve_workspace_size(NF, ND, k) bytes,
+ *               8-byte aligned, caller-owned;
+ *   top_idx, top_sim : device [NF][k] out (rows r < n_keys written);
+ *   sel_idx, sel_sim : device [K] out (the first n_sel entries written);
+ *   n_sel     : device int32 [1] out, min(K, |T|).
+ * 1 <= NF <= 65536, 1 <= ND <= 2^24, 1 <= D <= 1024, 1 <= k <= 16,
+ * 1 <= K <= 64. Enqueued on hip_stream; errors via vsr_last_error(NULL). */
+int vsr_retrieve(const float *frame_emb, const int32_t *key_idx, const int32_t *n_keys,
+                 int32_t NF, const float *docs, int32_t ND, int32_t D, int32_t k, int32_t K,
+                 void *workspace, size_t ws_bytes, int32_t *top_idx, float *top_sim,
+                 int32_t *sel_idx, float *sel_sim, int32_t *n_sel, void *hip_stream);
 
 /* Weight preparation for gemm_weights = VSR_F16: writes the n bf16 values of
  * src (device) to dst (device, n fp16 values, not overlapping src) with the

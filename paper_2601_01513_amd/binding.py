@@ -20,7 +20,8 @@ VSR_MAX_CANDS = 256
 
 EXPORTS = ["vsr_workspace_size", "vsr_create", "vsr_load_weights", "vsr_prefill",
            "vsr_score", "vsr_reliability", "vsr_align_select", "vsr_weights_to_f16",
-           "vsr_last_error", "vsr_destroy", "vsr_profile_enable", "vsr_profile_read"]
+           "vsr_keyframes", "vsr_retrieve_workspace_size", "vsr_retrieve", "vsr_last_error",
+           "vsr_destroy", "vsr_profile_enable", "vsr_profile_read"]
 
 VSR_SELECT_TWO_STAGE, VSR_SELECT_ADDITION, VSR_SELECT_INVERT = 0, 1, 2
 SELECT_STRATEGIES = {"two_stage": VSR_SELECT_TWO_STAGE, "addition": VSR_SELECT_ADDITION,
@@ -101,6 +102,20 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vsr_weights_to_f16.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                        ctypes.c_void_p]
     lib.vsr_weights_to_f16.restype = ctypes.c_int
+    lib.vsr_keyframes.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                  ctypes.c_int32, ctypes.c_float, ctypes.c_void_p,
+                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                  ctypes.c_void_p]
+    lib.vsr_keyframes.restype = ctypes.c_int
+    lib.vsr_retrieve_workspace_size.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
+    lib.vsr_retrieve_workspace_size.restype = ctypes.c_size_t
+    lib.vsr_retrieve.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+                                 ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                 ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.c_void_p, ctypes.c_void_p]
+    lib.vsr_retrieve.restype = ctypes.c_int
     lib.vsr_last_error.argtypes = [ctypes.c_void_p]
     lib.vsr_last_error.restype = ctypes.c_char_p
     lib.vsr_destroy.argtypes = [ctypes.c_void_p]
@@ -310,6 +325,62 @@ def align_select(ent, frames, rel, delta: float, strategy: str = "two_stage", ou
     if rc != VSR_OK:
         raise VsrError(rc, lib.vsr_last_error(None).decode())
     return align, choice
+
+
+class Retriever:
+    """The retrieval stage on the device: keyframes (Eq. 1), then per-keyframe
+    top-k documents and T* (Eq. 2-3). Holds the output and workspace tensors
+    for one video size and document bank."""
+
+    def __init__(self, n_frames: int, height: int, width: int, n_docs: int, dim: int, k: int,
+                 K: int, device="cuda", stream=None):
+        import torch
+        self._torch = torch
+        self.lib = load_library()
+        self.NF, self.H, self.W, self.ND, self.D, self.k, self.K = (
+            n_frames, height, width, n_docs, dim, k, K)
+        dev = torch.device(device)
+        i32 = dict(dtype=torch.int32, device=dev)
+        f32 = dict(dtype=torch.float32, device=dev)
+        self.hist = torch.empty((n_frames, 3, 64), **i32)
+        self.inter = torch.empty(n_frames, **i32)
+        self.key_idx = torch.empty(n_frames, **i32)
+        self.n_keys = torch.empty(1, **i32)
+        size = self.lib.vsr_retrieve_workspace_size(n_frames, n_docs, k)
+        if size == 0:
+            raise VsrError(VSR_EINVAL, "unsupported retrieval sizes")
+        self.ws = torch.empty(size, dtype=torch.uint8, device=dev)
+        self.top_idx = torch.empty((n_frames, k), **i32)
+        self.top_sim = torch.empty((n_frames, k), **f32)
+        self.sel_idx = torch.empty(K, **i32)
+        self.sel_sim = torch.empty(K, **f32)
+        self.n_sel = torch.empty(1, **i32)
+        self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
+
+    def _check(self, rc):
+        if rc != VSR_OK:
+            raise VsrError(rc, self.lib.vsr_last_error(None).decode())
+
+    def keyframes(self, frames, theta: float):
+        """frames: device uint8 [NF][H][W][3] -> (key_idx, n_keys) device tensors."""
+        self._frames = frames
+        self._check(self.lib.vsr_keyframes(_ptr(frames), self.NF, self.H, self.W, float(theta),
+                                           _ptr(self.hist), _ptr(self.inter),
+                                           _ptr(self.key_idx), _ptr(self.n_keys),
+                                           self.stream.cuda_stream))
+        return self.key_idx, self.n_keys
+
+    def retrieve(self, frame_emb, docs):
+        """frame_emb: device f32 [NF][D]; docs: device f32 [ND][D]. Uses the
+        keyframes of the last keyframes() call. Returns device tensors
+        (top_idx [NF][k], top_sim, sel_idx [K], sel_sim, n_sel)."""
+        self._emb = (frame_emb, docs)
+        self._check(self.lib.vsr_retrieve(
+            _ptr(frame_emb), _ptr(self.key_idx), _ptr(self.n_keys), self.NF, _ptr(docs),
+            self.ND, self.D, self.k, self.K, _ptr(self.ws), self.ws.numel(), _ptr(self.top_idx),
+            _ptr(self.top_sim), _ptr(self.sel_idx), _ptr(self.sel_sim), _ptr(self.n_sel),
+            self.stream.cuda_stream))
+        return self.top_idx, self.top_sim, self.sel_idx, self.sel_sim, self.n_sel
 
 
 def verifier_from_workload(wl, device="cuda", **kw) -> Verifier:

@@ -36,6 +36,19 @@ template <> __device__ __forceinline__ f16 from_f32<f16>(float x) { return stati
 constexpr int kMaxCands = 256;
 
 // Packed candidate rows: candidate m owns rows [cu[m], cu[m+1]).
+// Sum / maximum over the 64 lanes of a wave (butterfly, fixed order), the
+// result in every lane.
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
 struct Branches {
   int M;
   int cmax;
@@ -90,6 +103,17 @@ hipError_t launch_reliability_finish(int M, const float2 *part, int nchunks,
 hipError_t launch_align_select(const float *ent, const float *frames, int M, int NF, int D,
                                const float *rel, float delta, int strategy, float *align,
                                int32_t *choice, hipStream_t s);
+
+// Retrieval stage (Eq. 1-3): histograms + keyframes, then per-keyframe top-k
+// and the merged top-K (kernels_retrieval.hip).
+hipError_t launch_keyframes(const uint8_t *frames, int NF, int H, int W, float theta,
+                            int32_t *hist, int32_t *inter, int32_t *key_idx, int32_t *n_keys,
+                            hipStream_t s);
+size_t retrieve_workspace_bytes(int NF, int ND, int k);
+hipError_t launch_retrieve(const float *frame_emb, const int32_t *key_idx, const int32_t *n_keys,
+                           int NF, const float *docs, int ND, int D, int k, int K, void *ws,
+                           int32_t *top_idx, float *top_sim, int32_t *sel_idx, float *sel_sim,
+                           int32_t *n_sel, hipStream_t s);
 
 // Per-row merge of the LM-head partials: lse over the vocabulary chunks,
 // lp = target logit - lse, scattered to logprobs[m][j] (zeros elsewhere).

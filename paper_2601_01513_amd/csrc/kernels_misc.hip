@@ -7,17 +7,6 @@
 
 namespace vsr {
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
-}
-
 // Sum over a 256-thread block, same value returned to every thread.
 __device__ __forceinline__ float block_sum256(float v, float *red) {
   v = wave_sum(v);

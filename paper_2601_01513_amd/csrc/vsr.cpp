@@ -712,6 +712,73 @@ extern "C" const char *vsr_last_error(const vsr_ctx *ctx) {
 
 extern "C" void vsr_destroy(vsr_ctx *ctx) { delete ctx; }
 
+extern "C" int vsr_keyframes(const uint8_t *frames, int32_t NF, int32_t H, int32_t W,
+                             float theta, int32_t *hist, int32_t *inter, int32_t *key_idx,
+                             int32_t *n_keys, void *hip_stream) {
+  g_create_error.clear();
+  const char *msg = nullptr;
+  if (!frames || !hist || !inter || !key_idx || !n_keys) msg = "keyframes: NULL argument";
+  else if (reinterpret_cast<uintptr_t>(frames) & 15) msg = "frames must be 16-byte aligned";
+  else if (NF < 1 || NF > 65536) msg = "NF must lie in [1, 65536]";
+  else if (H < 1 || W < 1 || (long long)H * W > (1LL << 24)) msg = "need H, W >= 1, H W <= 2^24";
+  else if (!std::isfinite(theta)) msg = "theta must be finite";
+  if (msg) {
+    g_create_error = msg;
+    return VSR_EINVAL;
+  }
+  const hipError_t e = launch_keyframes(frames, NF, H, W, theta, hist, inter, key_idx, n_keys,
+                                        static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) {
+    g_create_error = std::string("HIP error in keyframes: ") + hipGetErrorString(e);
+    return VSR_EHIP;
+  }
+  return VSR_OK;
+}
+
+namespace {
+const char *retrieve_sizes_error(int32_t NF, int32_t ND, int32_t k) {
+  if (NF < 1 || NF > 65536) return "NF must lie in [1, 65536]";
+  if (ND < 1 || ND > (1 << 24)) return "ND must lie in [1, 2^24]";
+  if (k < 1 || k > 16) return "k must lie in [1, 16]";
+  return nullptr;
+}
+}  // namespace
+
+extern "C" size_t vsr_retrieve_workspace_size(int32_t NF, int32_t ND, int32_t k) {
+  return retrieve_sizes_error(NF, ND, k) ? 0 : retrieve_workspace_bytes(NF, ND, k);
+}
+
+extern "C" int vsr_retrieve(const float *frame_emb, const int32_t *key_idx,
+                            const int32_t *n_keys, int32_t NF, const float *docs, int32_t ND,
+                            int32_t D, int32_t k, int32_t K, void *workspace, size_t ws_bytes,
+                            int32_t *top_idx, float *top_sim, int32_t *sel_idx, float *sel_sim,
+                            int32_t *n_sel, void *hip_stream) {
+  g_create_error.clear();
+  const char *msg = retrieve_sizes_error(NF, ND, k);
+  if (!msg) {
+    if (!frame_emb || !key_idx || !n_keys || !docs || !workspace || !top_idx || !top_sim ||
+        !sel_idx || !sel_sim || !n_sel)
+      msg = "retrieve: NULL argument";
+    else if (D < 1 || D > 1024) msg = "D must lie in [1, 1024]";
+    else if (K < 1 || K > 64) msg = "K must lie in [1, 64]";
+    else if (reinterpret_cast<uintptr_t>(workspace) & 7) msg = "workspace must be 8-byte aligned";
+    else if (ws_bytes < retrieve_workspace_bytes(NF, ND, k))
+      msg = "workspace smaller than vsr_retrieve_workspace_size";
+  }
+  if (msg) {
+    g_create_error = msg;
+    return VSR_EINVAL;
+  }
+  const hipError_t e = launch_retrieve(frame_emb, key_idx, n_keys, NF, docs, ND, D, k, K,
+                                       workspace, top_idx, top_sim, sel_idx, sel_sim, n_sel,
+                                       static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) {
+    g_create_error = std::string("HIP error in retrieve: ") + hipGetErrorString(e);
+    return VSR_EHIP;
+  }
+  return VSR_OK;
+}
+
 extern "C" int vsr_weights_to_f16(const void *src, void *dst, size_t n, void *hip_stream) {
   g_create_error.clear();
   const uintptr_t a = reinterpret_cast<uintptr_t>(src), b = reinterpret_cast<uintptr_t>(dst);

@@ -144,3 +144,34 @@ def test_weights_to_f16_rejects_bad_arguments():
     assert lib.vsr_weights_to_f16(0x10000, 0x10010, 64, None) == B.VSR_EINVAL  # overlap
     assert b"overlap" in lib.vsr_last_error(None)
     assert lib.vsr_weights_to_f16(None, None, 0, None) == B.VSR_OK             # nothing to do
+
+
+def test_retrieval_calls_reject_bad_arguments():
+    lib = _lib()
+    ok = dict(frames=0x10000, NF=8, H=4, W=4, theta=0.5, hist=0x20000, inter=0x30000,
+              key_idx=0x40000, n_keys=0x50000)
+
+    def kf(**kw):
+        a = dict(ok, **kw)
+        return lib.vsr_keyframes(a["frames"], a["NF"], a["H"], a["W"], a["theta"], a["hist"],
+                                 a["inter"], a["key_idx"], a["n_keys"], None)
+    for bad in (dict(frames=None), dict(frames=0x10008), dict(NF=0), dict(NF=65537),
+                dict(H=0), dict(W=5000, H=5000), dict(theta=float("nan")), dict(n_keys=None)):
+        assert kf(**bad) == B.VSR_EINVAL, bad
+    assert lib.vsr_retrieve_workspace_size(8, 100, 3) > 0
+    for nf, nd, k in ((0, 100, 3), (8, 0, 3), (8, 100, 0), (8, 100, 17)):
+        assert lib.vsr_retrieve_workspace_size(nf, nd, k) == 0
+    ws = lib.vsr_retrieve_workspace_size(8, 100, 3)
+    r = dict(fe=0x10000, ki=0x20000, nk=0x30000, NF=8, docs=0x40000, ND=100, D=64, k=3, K=3,
+             ws=0x50000, wsb=ws, ti=0x60000, ts=0x70000, si=0x80000, ss=0x90000, ns=0xA0000)
+
+    def rt(**kw):
+        a = dict(r, **kw)
+        return lib.vsr_retrieve(a["fe"], a["ki"], a["nk"], a["NF"], a["docs"], a["ND"], a["D"],
+                                a["k"], a["K"], a["ws"], a["wsb"], a["ti"], a["ts"], a["si"],
+                                a["ss"], a["ns"], None)
+    for bad, word in ((dict(docs=None), b"NULL"), (dict(D=0), b"D must"), (dict(D=1025), b"D must"),
+                      (dict(K=0), b"K must"), (dict(K=65), b"K must"), (dict(k=17), b"k must"),
+                      (dict(ws=0x50004), b"aligned"), (dict(wsb=ws - 1), b"smaller")):
+        assert rt(**bad) == B.VSR_EINVAL, bad
+        assert word in lib.vsr_last_error(None), (bad, lib.vsr_last_error(None))

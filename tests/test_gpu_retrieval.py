@@ -1,0 +1,175 @@
+"""GPU parity of the retrieval stage (Section 3.1, Eq. 1-3): vsr_keyframes and
+vsr_retrieve through the C ABI against oracle/retrieval.py on the same seeded
+inputs.
+
+Bars:
+* histograms, intersection sums, keyframe indices and their count are
+  integer results: bit-exact (theta is passed to the oracle as the float32
+  value the library receives);
+* cosine similarities (float32 on the GPU, float64 in the oracle): 1e-5;
+* rankings: each keyframe's top-k and T* equal the oracle's wherever the
+  similarity gap at the list boundary exceeds 1e-5; otherwise every chosen
+  document must be within 1e-5 of the oracle's k-th best (a valid top-k
+  under rounding).
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import retrieval as R
+from paper_2601_01513_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-5
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _say(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def run_keyframes(frames, theta):
+    torch = _torch()
+    from paper_2601_01513_amd.binding import Retriever
+    nf, h, w, _ = frames.shape
+    r = Retriever(nf, h, w, 1, 1, 1, 1)
+    key_idx, n_keys = r.keyframes(torch.tensor(frames, device="cuda"), theta)
+    torch.cuda.synchronize()
+    n = int(n_keys.cpu()[0])
+    return (r.hist.cpu().numpy(), r.inter.cpu().numpy(), key_idx.cpu().numpy()[:n])
+
+
+def check_keyframes(frames, theta):
+    hist, inter, keys = run_keyframes(frames, theta)
+    t32 = float(np.float32(theta))
+    keys_o, s_o = R.keyframes(frames, t32)
+    np.testing.assert_array_equal(hist, R.frame_histograms(frames).reshape(hist.shape))
+    np.testing.assert_array_equal(inter, s_o)
+    np.testing.assert_array_equal(keys, keys_o)
+    return keys
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_keyframes_small_video(seed):
+    rc = W.VIDEO_SMALL
+    _say(f"case: {rc.name} seed {seed}")
+    keys = check_keyframes(W.make_video(rc, seed), rc.theta)
+    assert len(keys) == rc.n_scenes
+
+
+@pytest.mark.parametrize("shape", [(1, 4, 4), (7, 5, 7), (3, 1, 1), (9, 13, 11), (5, 64, 48)])
+@pytest.mark.parametrize("theta", [0.0, 0.5, 0.9, 1.0001])
+def test_keyframes_odd_shapes_and_thresholds(shape, theta):
+    """Frame sizes that are not multiples of 16 bytes take the byte path."""
+    nf, h, w = shape
+    rng = np.random.default_rng(nf * 1000 + h)
+    base = rng.integers(0, 256, size=(h, w, 3))
+    frames = np.stack([np.clip(base + rng.integers(-40, 41, size=(h, w, 3)) * (i % 3), 0, 255)
+                       for i in range(nf)]).astype(np.uint8)
+    check_keyframes(frames, theta)
+
+
+def test_keyframes_flat_and_wipe_videos():
+    flat = np.zeros((6, 8, 8, 3), dtype=np.uint8)
+    assert check_keyframes(flat, 0.99).tolist() == [0]
+    wipe = np.zeros((40, 2, 40, 3), dtype=np.uint8)
+    for i in range(40):
+        wipe[i, :, :i] = 200
+    assert check_keyframes(wipe, 0.5).tolist() == [0]
+
+
+def test_keyframes_22s_video():
+    rc = W.VIDEO_22S
+    _say(f"case: {rc.name}")
+    keys = check_keyframes(W.make_video(rc, 0), rc.theta)
+    assert len(keys) == rc.n_scenes
+
+
+def _check_topk(gpu_idx, gpu_sim, sims_o, k):
+    """One ranked list against the oracle's similarities of all candidates."""
+    order = R.top_indices(sims_o, k)
+    kk = len(order)
+    gpu_idx = np.asarray(gpu_idx[:kk])
+    np.testing.assert_allclose(gpu_sim[:kk], sims_o[gpu_idx], rtol=0, atol=TOL)
+    boundary = sims_o[order[-1]]
+    rest = np.delete(sims_o, order)
+    gaps = np.diff(-sims_o[order])
+    clear = (len(rest) == 0 or boundary - rest.max() > TOL) and np.all(gaps > TOL)
+    if clear:
+        np.testing.assert_array_equal(gpu_idx, order)
+    else:
+        assert len(set(gpu_idx.tolist())) == kk
+        assert np.all(sims_o[gpu_idx] >= boundary - TOL)
+
+
+def run_retrieval(rc, frames, femb, demb):
+    torch = _torch()
+    from paper_2601_01513_amd.binding import Retriever
+    r = Retriever(rc.n_frames, rc.height, rc.width, rc.n_docs, rc.dim, rc.k, rc.K)
+    t = lambda a: torch.tensor(a, device="cuda")  # noqa: E731
+    r.keyframes(t(frames), rc.theta)
+    top_idx, top_sim, sel_idx, sel_sim, n_sel = r.retrieve(t(femb), t(demb))
+    torch.cuda.synchronize()
+    n = int(r.n_keys.cpu()[0])
+    ns = int(n_sel.cpu()[0])
+    return (r.key_idx.cpu().numpy()[:n], top_idx.cpu().numpy()[:n], top_sim.cpu().numpy()[:n],
+            sel_idx.cpu().numpy()[:ns], sel_sim.cpu().numpy()[:ns])
+
+
+def check_retrieval(rc, frames, femb, demb):
+    keys, top_idx, top_sim, sel_idx, sel_sim = run_retrieval(rc, frames, femb, demb)
+    keys_o, _ = R.keyframes(frames, float(np.float32(rc.theta)))
+    np.testing.assert_array_equal(keys, keys_o)
+    sims = R.cosine_matrix(femb[keys_o], demb)
+    for r in range(len(keys_o)):
+        _check_topk(top_idx[r], top_sim[r], sims[r], rc.k)
+    # T*: scores of the retrieved set, from the GPU's own lists (a document
+    # retrieved on the GPU but not by the oracle differs only within TOL).
+    best = {}
+    for r in range(len(keys)):
+        for j in top_idx[r][:min(rc.k, rc.n_docs)]:
+            best[int(j)] = max(best.get(int(j), -np.inf), float(sims[r, j]))
+    docs = np.array(sorted(best))
+    scores = np.array([best[j] for j in docs])
+    _check_topk(np.searchsorted(docs, sel_idx), sel_sim, scores, rc.K)
+    _, _, T_o, Ts_o = R.retrieve(femb, keys_o, demb, rc.k, rc.K)
+    _say(f"  keyframes {keys.tolist()} T* gpu {sel_idx.tolist()} oracle {T_o.tolist()}")
+    return sel_idx, T_o
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_retrieval_small(seed):
+    rc = W.VIDEO_SMALL
+    _say(f"case: {rc.name} seed {seed}")
+    check_retrieval(rc, *W.make_retrieval(rc, seed))
+
+
+@pytest.mark.parametrize("nd,dim,k,K", [(1, 8, 1, 1), (5, 3, 16, 64), (257, 1024, 16, 64),
+                                        (5000, 768, 7, 20)])
+def test_retrieval_sizes(nd, dim, k, K):
+    rc = W.RetrievalConfig(f"sizes nd {nd} dim {dim}", 30, 16, 16, 4, nd, dim, k, K, 0.6)
+    _say(f"case: {rc.name} k {k} K {K}")
+    check_retrieval(rc, *W.make_retrieval(rc, 3))
+
+
+def test_retrieval_ties_take_lower_index():
+    torch = _torch()
+    rc = W.RetrievalConfig("ties", 10, 8, 8, 2, 40, 16, 4, 6, 0.6)
+    frames, femb, demb = W.make_retrieval(rc, 5)
+    demb[:] = demb[7]           # every document the same: all similarities tie
+    keys, top_idx, _, sel_idx, _ = run_retrieval(rc, frames, femb, demb)
+    assert all(row.tolist() == [0, 1, 2, 3] for row in top_idx)
+    assert sel_idx.tolist() == [0, 1, 2, 3]
+
+
+def test_retrieval_22s_video_large_bank():
+    rc = W.VIDEO_22S_BANK
+    _say(f"case: {rc.name}")
+    check_retrieval(rc, *W.make_retrieval(rc, 0))
