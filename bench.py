@@ -120,10 +120,30 @@ def time_next_rows(v, cids, lens, dev, reps, log_fn):
     rel = torch.rand(M, device=dev)
     sel_ms = timed(lambda: align_select(ent, frames, rel, 0.05, "two_stage"), 100)
     log_fn(f"reliability {rel_ms:.3f} ms/call, align_select {sel_ms * 1e3:.1f} us/call")
-    return {"reliability_ms": round(rel_ms, 3),
-            "reliability_tok_s": round(sum(blens) / (rel_ms * 1e-3), 1),
-            "align_select_us": round(sel_ms * 1e3, 2),
-            "align_select_shape": f"M={M} frames=64 D=768"}
+    out = {"reliability_ms": round(rel_ms, 3),
+           "reliability_tok_s": round(sum(blens) / (rel_ms * 1e-3), 1),
+           "align_select_us": round(sel_ms * 1e3, 2),
+           "align_select_shape": f"M={M} frames=64 D=768"}
+    # Retrieval stage: keyframes of a 22 s video (220 frames of 336 x 336) and
+    # top-k over a 100k-document bank.
+    from paper_2601_01513_amd.binding import Retriever
+    rc = W.VIDEO_22S_BANK
+    frames, femb, demb = W.make_retrieval(rc, 0)
+    r = Retriever(rc.n_frames, rc.height, rc.width, rc.n_docs, rc.dim, rc.k, rc.K, device=dev)
+    fr, fe, de = (torch.tensor(a, device=dev) for a in (frames, femb, demb))
+    kf_us = timed(lambda: r.keyframes(fr, rc.theta), 20) * 1e3
+    rt_us = timed(lambda: r.retrieve(fe, de), 20) * 1e3
+    nk = int(r.n_keys.cpu()[0])
+    log_fn(f"keyframes {kf_us:.1f} us/call, retrieve {rt_us:.1f} us/call ({nk} keyframes)")
+    frame_bytes = frames.nbytes
+    bank_bytes = demb.nbytes * ((nk + 7) // 8)   # the bank is read once per 8 keyframes
+    out.update({"keyframes_us": round(kf_us, 1),
+                "keyframes_GBs": round(frame_bytes / (kf_us * 1e-6) / 1e9, 1),
+                "retrieve_us": round(rt_us, 1),
+                "retrieve_GBs": round(bank_bytes / (rt_us * 1e-6) / 1e9, 1),
+                "retrieval_shape": f"{rc.n_frames} frames {rc.height}x{rc.width}, "
+                                   f"{nk} keyframes, {rc.n_docs} docs x {rc.dim}, k={rc.k}"})
+    return out
 
 
 def cpu_baseline(wl, log_fn):

@@ -228,7 +228,7 @@ size_t vsr_retrieve_workspace_size(int32_t NF, int32_t ND, int32_t k);
  * embedding has similarity 0 with everything.
  *   frame_emb : device float [NF][D] (embeddings of every frame);
  *   key_idx, n_keys : device, as written by vsr_keyframes;
- *   docs      : device float [ND][D];
+ *   docs      : device float [ND][D], 16-byte aligned;
  *   workspace : device, >= vsr_retrieve_workspace_size(NF, ND, k) bytes,
  *               8-byte aligned, caller-owned;
  *   top_idx, top_sim : device [NF][k] out (rows r < n_keys written);

@@ -92,9 +92,8 @@ __global__ __launch_bounds__(1024) void k_keyframes(const int32_t *hist, int NF,
   if (t == 1023) *n_keys = cnt[1023];
 }
 
-constexpr int RG = 8;        // keyframes per retrieval block
-constexpr int RCH = 256;     // documents per retrieval block
-constexpr int RT = 256;      // threads of a retrieval block
+constexpr int RG = 16;       // keyframes per retrieval block
+constexpr int RT = 256;      // threads of a retrieval block = documents per block
 constexpr int RW = RT / 64;
 
 struct SimIdx {
@@ -107,16 +106,36 @@ __device__ __forceinline__ bool before(float sa, int ia, float sb, int ib) {
   return sa > sb || (sa == sb && ia < ib);
 }
 
-// Block (document chunk, keyframe group): cosines of RG keyframes with RCH
-// documents, then each keyframe's top-k of the chunk -> part[key][chunk][k].
+// The better of two (similarity, index) candidates; index -1 is no candidate.
+__device__ __forceinline__ void keep_better(float &s, int &i, float s2, int i2) {
+  if (i2 >= 0 && (i < 0 || before(s2, i2, s, i))) {
+    s = s2;
+    i = i2;
+  }
+}
+
+// Best candidate of the wave (fixed butterfly order), in every lane.
+__device__ __forceinline__ void wave_best(float &s, int &i) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float s2 = __shfl_xor(s, o, 64);
+    const int i2 = __shfl_xor(i, o, 64);
+    keep_better(s, i, s2, i2);
+  }
+}
+
+// Block (document chunk, keyframe group): thread t scores document
+// d0 + t against up to RG keyframes held in LDS (every lane reads the same
+// keyframe value: an LDS broadcast), then wave w picks the top-k of the chunk
+// for keyframes w, w + RW, ... -> part[key][chunk][k].
 __global__ __launch_bounds__(RT) void k_retrieve_chunk(const float *frame_emb,
                                                        const int32_t *key_idx,
                                                        const int32_t *n_keys,
                                                        const float *docs, int ND, int D, int k,
                                                        int nchunks, SimIdx *part) {
-  __shared__ float q[RG][1024];
+  __shared__ __align__(16) float q[RG][1024];
   __shared__ float qn[RG];
-  __shared__ float sims[RG][RCH];
+  __shared__ float sims[RG][RT];
   const int nk = *n_keys;
   const int g0 = blockIdx.y * RG;
   if (g0 >= nk) return;  // uniform per block
@@ -127,95 +146,90 @@ __global__ __launch_bounds__(RT) void k_retrieve_chunk(const float *frame_emb,
     for (int c = t; c < D; c += RT) q[r][c] = src[c];
   }
   __syncthreads();
-  if (w < ng) {  // wave r: norm of keyframe r (waves 0..RG-1 cover RG <= 2 RW)
+  for (int r = w; r < ng; r += RW) {
     float s = 0.f;
-    for (int c = lane; c < D; c += 64) s += q[w][c] * q[w][c];
+    for (int c = lane; c < D; c += 64) s += q[r][c] * q[r][c];
     s = wave_sum(s);
-    if (lane == 0) qn[w] = sqrtf(s);
-  }
-  if (w + RW < ng) {
-    float s = 0.f;
-    for (int c = lane; c < D; c += 64) s += q[w + RW][c] * q[w + RW][c];
-    s = wave_sum(s);
-    if (lane == 0) qn[w + RW] = sqrtf(s);
+    if (lane == 0) qn[r] = sqrtf(s);
   }
   __syncthreads();
-  const int d0 = blockIdx.x * RCH;
-  for (int j = w; j < RCH; j += RW) {
-    const int doc = d0 + j;
-    float dot[RG], dd = 0.f;
+  const int d0 = blockIdx.x * RT, doc = d0 + t;
+  float dot[RG], dd = 0.f;
 #pragma unroll
-    for (int r = 0; r < RG; ++r) dot[r] = 0.f;
-    if (doc < ND) {
-      const float *src = docs + (long)doc * D;
-      for (int c = lane; c < D; c += 64) {
+  for (int r = 0; r < RG; ++r) dot[r] = 0.f;
+  if (doc < ND) {
+    const float *src = docs + (long)doc * D;
+    if ((D & 3) == 0) {  // rows 16-byte aligned (the base is, by contract)
+      for (int c = 0; c < D; c += 4) {
+        const float4 v = *reinterpret_cast<const float4 *>(src + c);
+        dd += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+#pragma unroll
+        for (int r = 0; r < RG; ++r) {
+          const float4 e = *reinterpret_cast<const float4 *>(&q[r][c]);
+          dot[r] += e.x * v.x + e.y * v.y + e.z * v.z + e.w * v.w;
+        }
+      }
+    } else {
+      for (int c = 0; c < D; ++c) {
         const float v = src[c];
         dd += v * v;
 #pragma unroll
         for (int r = 0; r < RG; ++r) dot[r] += q[r][c] * v;
       }
     }
-    dd = wave_sum(dd);
+  }
+  const float dn = sqrtf(dd);
 #pragma unroll
-    for (int r = 0; r < RG; ++r) dot[r] = wave_sum(dot[r]);
-    if (lane == 0) {
-      const float dn = sqrtf(dd);
-#pragma unroll
-      for (int r = 0; r < RG; ++r) {
-        const float den = qn[r] * dn;
-        sims[r][j] = doc >= ND ? -INFINITY : (den > 0.f ? dot[r] / den : 0.f);
-      }
+  for (int r = 0; r < RG; ++r) {
+    if (r < ng) {
+      const float den = qn[r] * dn;
+      sims[r][t] = den > 0.f ? dot[r] / den : 0.f;
     }
   }
   __syncthreads();
-  // Thread r < ng: k selection passes over the chunk (ties: lower index).
-  if (t < ng) {
-    SimIdx *out = part + ((long)(g0 + t) * nchunks + blockIdx.x) * k;
+  const int nvalid = min(RT, ND - d0);
+  for (int r = w; r < ng; r += RW) {
+    SimIdx *out = part + ((long)(g0 + r) * nchunks + blockIdx.x) * k;
     float last_s = INFINITY;
     int last_i = -1;
     for (int p = 0; p < k; ++p) {
       float bs = -INFINITY;
       int bi = -1;
-      for (int j = 0; j < RCH; ++j) {
-        const int doc = d0 + j;
-        if (doc >= ND) break;
-        const float s = sims[t][j];
-        if (!before(last_s, last_i, s, doc)) continue;  // already taken
-        if (bi < 0 || before(s, doc, bs, bi)) {
-          bs = s;
-          bi = doc;
-        }
+      for (int j = lane; j < nvalid; j += 64) {
+        const float sj = sims[r][j];
+        if (before(last_s, last_i, sj, d0 + j)) keep_better(bs, bi, sj, d0 + j);
       }
-      out[p] = SimIdx{bs, bi};  // bi = -1: the chunk has fewer than k documents
-      last_s = bs;
+      wave_best(bs, bi);
+      if (lane == 0) out[p] = SimIdx{bs, bi};  // -1: fewer than k documents left
+      last_s = bi < 0 ? -INFINITY : bs;
       last_i = bi;
-      if (bi < 0) last_s = -INFINITY;
     }
   }
 }
 
-// Block r < n_keys: the top-k of keyframe r over every chunk's top-k.
+// Block r < n_keys (one wave): the top-k of keyframe r over every chunk's
+// top-k, k passes of a wave-wide best.
 __global__ __launch_bounds__(64) void k_retrieve_merge(const SimIdx *part, const int32_t *n_keys,
                                                        int nchunks, int k, int32_t *top_idx,
                                                        float *top_sim) {
-  const int r = blockIdx.x;
-  if (r >= *n_keys || threadIdx.x != 0) return;
+  const int r = blockIdx.x, lane = threadIdx.x;
+  if (r >= *n_keys) return;
   const SimIdx *p = part + (long)r * nchunks * k;
+  const int n = nchunks * k;
   float last_s = INFINITY;
   int last_i = -1;
   for (int q = 0; q < k; ++q) {
     float bs = -INFINITY;
     int bi = -1;
-    for (int e = 0; e < nchunks * k; ++e) {
+    for (int e = lane; e < n; e += 64) {
       const SimIdx c = p[e];
-      if (c.i < 0 || !before(last_s, last_i, c.s, c.i)) continue;
-      if (bi < 0 || before(c.s, c.i, bs, bi)) {
-        bs = c.s;
-        bi = c.i;
-      }
+      if (c.i >= 0 && before(last_s, last_i, c.s, c.i)) keep_better(bs, bi, c.s, c.i);
     }
-    top_idx[(long)r * k + q] = bi;
-    top_sim[(long)r * k + q] = bi < 0 ? 0.f : bs;
+    wave_best(bs, bi);
+    if (lane == 0) {
+      top_idx[(long)r * k + q] = bi;
+      top_sim[(long)r * k + q] = bi < 0 ? 0.f : bs;
+    }
     last_s = bi < 0 ? -INFINITY : bs;
     last_i = bi;
   }
@@ -290,7 +304,7 @@ hipError_t launch_keyframes(const uint8_t *frames, int NF, int H, int W, float t
 }
 
 size_t retrieve_workspace_bytes(int NF, int ND, int k) {
-  const size_t nchunks = ((size_t)ND + RCH - 1) / RCH;
+  const size_t nchunks = ((size_t)ND + RT - 1) / RT;
   return (size_t)NF * nchunks * (size_t)k * sizeof(SimIdx);
 }
 
@@ -298,7 +312,7 @@ hipError_t launch_retrieve(const float *frame_emb, const int32_t *key_idx, const
                            int NF, const float *docs, int ND, int D, int k, int K, void *ws,
                            int32_t *top_idx, float *top_sim, int32_t *sel_idx, float *sel_sim,
                            int32_t *n_sel, hipStream_t s) {
-  const int nchunks = (ND + RCH - 1) / RCH;
+  const int nchunks = (ND + RT - 1) / RT;
   SimIdx *part = static_cast<SimIdx *>(ws);
   k_retrieve_chunk<<<dim3(nchunks, (NF + RG - 1) / RG), RT, 0, s>>>(
       frame_emb, key_idx, n_keys, docs, ND, D, k, nchunks, part);

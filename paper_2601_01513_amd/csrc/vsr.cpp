@@ -762,6 +762,7 @@ extern "C" int vsr_retrieve(const float *frame_emb, const int32_t *key_idx,
     else if (D < 1 || D > 1024) msg = "D must lie in [1, 1024]";
     else if (K < 1 || K > 64) msg = "K must lie in [1, 64]";
     else if (reinterpret_cast<uintptr_t>(workspace) & 7) msg = "workspace must be 8-byte aligned";
+    else if (reinterpret_cast<uintptr_t>(docs) & 15) msg = "docs must be 16-byte aligned";
     else if (ws_bytes < retrieve_workspace_bytes(NF, ND, k))
       msg = "workspace smaller than vsr_retrieve_workspace_size";
   }
