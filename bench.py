@@ -146,6 +146,54 @@ def time_next_rows(v, cids, lens, dev, reps, log_fn):
     return out
 
 
+def time_draft(dev, log_fn, reps=3):
+    """Parallel drafting (Eq. 5, 8-10) with the 3B-class drafter: one
+    vsr_draft call = the branch prompts through every layer, then 64 decode
+    steps of one row per branch. A decode step streams every GEMM weight
+    (fp16) and the LM head once: its HBM roofline."""
+    import torch
+    from paper_2601_01513_amd.binding import Verifier
+    cfg, n_new = W.DRAFT_3B, W.DRAFT_NEW
+    wl = W.make_workload(cfg, 0, device=dev)
+    v = Verifier(cfg, wl.weights, device=dev, max_new=n_new)
+    ids = torch.tensor(wl.prefix_ids, dtype=torch.int32, device=dev)
+    v.prefill(wl.visual, ids)
+    pids = torch.tensor(wl.cand_ids, dtype=torch.int32, device=dev)
+    lens = [int(x) for x in wl.cand_len]
+    M = len(lens)
+    st = torch.cuda.current_stream(dev)
+
+    def timed(n):
+        out = torch.empty((M, n), dtype=torch.int32, device=dev)
+        v.draft(pids, lens, n, out=out)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(st)
+        for _ in range(reps):
+            v.draft(pids, lens, n, out=out)
+        b.record(st)
+        b.synchronize()
+        return a.elapsed_time(b) / reps
+    one = timed(1)
+    full = timed(n_new)
+    step_ms = (full - one) / (n_new - 1)
+    d, F, L = cfg.d_model, cfg.d_ff, cfg.n_layers
+    weight_bytes = 2 * (L * d * (cfg.qkv_rows + cfg.n_heads * cfg.head_dim + 3 * F)
+                        + cfg.vocab * d)
+    gbs = weight_bytes / (step_ms * 1e-3) / 1e9
+    log_fn(f"draft: {full:.2f} ms per call ({M} branches x {n_new} new tokens), prompt pass "
+           f"{one:.2f} ms, decode step {step_ms:.3f} ms = {gbs:.0f} GB/s of weights")
+    res = {"draft_ms": round(full, 2), "draft_tok_s": round(M * n_new / (full * 1e-3), 1),
+           "draft_prompt_pass_ms": round(one, 2), "draft_step_ms": round(step_ms, 3),
+           "draft_step_weight_GBs": round(gbs, 1),
+           "draft_step_hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
+           "draft_shape": f"{cfg.name}: prefix {cfg.n_prefix}, {M} branches x "
+                          f"{cfg.cand_len} prompt tokens, {n_new} new"}
+    v.close()
+    del v, wl
+    torch.cuda.empty_cache()
+    return res
+
+
 def cpu_baseline(wl, log_fn):
     """The oracle (float64, shared-prefix mode) on the same workload with 1 and
     2 of its layers; the per-layer cost is extrapolated to the full depth."""
@@ -303,6 +351,7 @@ def main():
     }
     if not args.no_next_rows:
         result["next_rows"] = time_next_rows(v, cids, lens, dev, max(3, args.steps // 2), log)
+        result["next_rows"].update(time_draft(dev, log))
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, log)
     print(json.dumps(result), flush=True)

@@ -87,6 +87,11 @@ typedef struct vsr_config {
    * magnitudes >= 2^-17; loaded without conversion, about 6% faster GEMMs).
    * Embedding, norm gains and visual rows stay bf16. VSR_F32 contexts: 0. */
   int32_t gemm_weights;
+  /* Largest number of tokens vsr_draft may generate per branch (0: no draft
+   * cache in the workspace; vsr_draft then fails with VSR_ESTATE). The draft
+   * cache holds every layer's keys/values of max_cands branches of
+   * max_cand_len + max_new positions. 0 <= max_new <= 4096. */
+  int32_t max_new;
 } vsr_config;
 
 #define VSR_MAX_CANDS 256
@@ -171,6 +176,25 @@ int vsr_reliability(vsr_ctx *ctx, const int32_t *branch_ids, const int32_t *bran
                     int32_t M, int32_t Cmax, int32_t yes_id, int32_t no_id, float delta,
                     float *lp_yes_no, float *rel, int32_t *keep);
 
+/* Parallel draft generation over the shared prefix (Section 3.1, Eq. 5;
+ * Section 3.2, Eq. 8-10): the context's model, used as the drafter, extends
+ * every branch greedily. Branch m is the prefix followed by its prompt
+ * (the retrieved document and the generation prompt, prompt_len[m] tokens at
+ * positions P..); step s appends
+ *   tokens[m][s] = argmax_v logits(last row of branch m)[v]
+ * (lowest id among equal maxima) at the next position. Branches see the
+ * prefix and their own tokens only; all of them advance together, one batched
+ * pass per step, and the next step's inputs never leave the device.
+ *   prompt_ids : device [M][Cmax] int32 (out-of-range ids read as id 0);
+ *   prompt_len : HOST [M] int32, each in [1, Cmax];
+ *   tokens     : device [M][n_new] int32 out.
+ * 1 <= M <= max_cands, 1 <= Cmax <= max_cand_len, 1 <= n_new <= max_new;
+ * needs a prefill. Keeps the branches' keys/values in the draft cache of the
+ * workspace (overwritten by the next vsr_draft); vsr_score and
+ * vsr_reliability may be called before or after it against the same prefix. */
+int vsr_draft(vsr_ctx *ctx, const int32_t *prompt_ids, const int32_t *prompt_len, int32_t M,
+              int32_t Cmax, int32_t n_new, int32_t *tokens);
+
 /* Stage 2 and the final choice (Section 3.2, Eq. 14-15; Algorithm 1; the
  * strategies compared in Table 3). No context: the inputs are CLIP
  * embeddings, not verifier state.
@@ -254,16 +278,19 @@ void vsr_destroy(vsr_ctx *ctx);
 
 /* ---- measurement (not part of the method) ----------------------------------
  * Per-stage kernel timing for benchmarks: while enabled, every stage launch of
- * vsr_prefill / vsr_score is bracketed by HIP events on the context's stream.
- * Stage s of the prefix pass is s, of the candidate pass VSR_STAGE_KINDS + s;
+ * vsr_prefill / vsr_score / vsr_reliability / vsr_draft is bracketed by HIP
+ * events on the context's stream. Stage s of the prefix pass is s, of the
+ * candidate pass (score, reliability) VSR_STAGE_KINDS + s, of the draft
+ * pass 2 VSR_STAGE_KINDS + s (there kind 9 is the LM head + chunk argmax and
+ * kind 11 the greedy pick);
  * kinds: 0 embedding, 1 RMSNorm, 2 QKV projection + rotary + cache write,
  * 3 attention, 4 attention merge, 5 output projection, 6 gate/up + SwiGLU,
  * 7 down projection, 8 LM-head inputs, 9 LM head + chunk LSE,
  * 10 LSE merge + target gather, 11 sum + argmax, 12 row tables, 13 copy. */
 #define VSR_STAGE_KINDS 14
-#define VSR_STAGES (2 * VSR_STAGE_KINDS)
+#define VSR_STAGES (3 * VSR_STAGE_KINDS)
 
-/* Times the stage kinds whose bits are set in kinds (bit k: kind k, in both
+/* Times the stage kinds whose bits are set in kinds (bit k: kind k, in all
  * passes; VSR_PROFILE_ALL: every kind; 0: timing off) and clears what was
  * recorded. Each timed launch adds two event records to the stream, so a
  * benchmark that times few kinds perturbs the pass least. */

@@ -22,7 +22,7 @@ no end-of-sequence behaviour worth modelling).
 """
 from __future__ import annotations
 
-from typing import Dict
+from typing import Dict, List, Optional
 
 import numpy as np
 
@@ -125,12 +125,55 @@ def teacher_forced(cfg, weights: Dict, visual, prefix_ids, prompt_ids, prompt_le
         x = np.concatenate([x_pre, e[toks]], axis=0)
         h = forward_hidden(x, weights, np.arange(P + len(toks)), cfg, dtype)
         lg = next_token_logits(h[P + pl - 1:P + pl - 1 + n], weights, cfg, dtype)
-        for s in range(n):
-            row = lg[s]
-            a = greedy(row)
-            srt = np.partition(row, -2)[-2:]
-            got[m, s] = row[int(tokens[m][s])]
-            top[m, s] = row[a]
-            arg[m, s] = a
-            gap[m, s] = srt[1] - srt[0]
+        got[m], top[m], arg[m], gap[m] = _report(lg, tokens[m], dtype)
+    return got, top, arg, gap
+
+
+def _report(lg: np.ndarray, tokens, dtype):
+    """Per row of logits lg [n][V] and the chosen tokens [n]: (logit of the
+    token, largest logit, argmax, gap between the two largest logits)."""
+    n = lg.shape[0]
+    got, top, gap = (np.zeros(n, dtype=dtype) for _ in range(3))
+    arg = np.zeros(n, dtype=np.int64)
+    for s in range(n):
+        row = lg[s]
+        a = greedy(row)
+        srt = np.partition(row, -2)[-2:]
+        got[s], top[s], arg[s], gap[s] = row[int(tokens[s])], row[a], a, srt[1] - srt[0]
+    return got, top, arg, gap
+
+
+def teacher_forced_shared(cfg, weights: Dict, visual, prefix_ids, prompt_ids, prompt_len,
+                          tokens, dtype=np.float64, branches: Optional[List[int]] = None,
+                          progress=None):
+    """teacher_forced with the prefix run once per layer and its keys/values
+    reused by every branch (the same result re-associated), restricted to
+    `branches` (the other rows are nan / -1); progress(layer) after each
+    layer. Branch m runs prompt_m (+) tokens[m][:n-1]: the rows that predict
+    tokens[m][0..n-1]."""
+    P = cfg.n_visual + len(prefix_ids)
+    tokens = np.asarray(tokens)
+    M, n = tokens.shape
+    todo = list(range(M)) if branches is None else list(branches)
+    e = _c(weights["embed"], dtype)
+    x_pre = embed_prefix(weights, visual, prefix_ids, dtype)
+    pos_pre = np.arange(P)
+    xs = {}
+    for m in todo:
+        pl = int(prompt_len[m])
+        xs[m] = e[np.concatenate([np.asarray(prompt_ids[m, :pl]), tokens[m, :n - 1]])]
+    for li, lw in enumerate(weights["layers"]):
+        x_next, kp, vp = decoder_layer(x_pre, lw, pos_pre, cfg, dtype)
+        for m in todo:
+            xs[m], _, _ = decoder_layer(xs[m], lw, P + np.arange(xs[m].shape[0]), cfg, dtype,
+                                        kp, vp, pos_pre)
+        x_pre = x_next
+        if progress is not None:
+            progress(li)
+    got, top, gap = (np.full((M, n), np.nan, dtype=dtype) for _ in range(3))
+    arg = np.full((M, n), -1, dtype=np.int64)
+    for m in todo:
+        pl = int(prompt_len[m])
+        lg = next_token_logits(xs[m][pl - 1:pl - 1 + n], weights, cfg, dtype)
+        got[m], top[m], arg[m], gap[m] = _report(lg, tokens[m], dtype)
     return got, top, arg, gap

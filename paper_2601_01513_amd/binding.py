@@ -19,7 +19,7 @@ GEMM_WEIGHT_KEYS = ("wqkv", "wo", "wgu", "wdown")  # per layer, plus lm_head
 VSR_MAX_CANDS = 256
 
 EXPORTS = ["vsr_workspace_size", "vsr_create", "vsr_load_weights", "vsr_prefill",
-           "vsr_score", "vsr_reliability", "vsr_align_select", "vsr_weights_to_f16",
+           "vsr_score", "vsr_reliability", "vsr_draft", "vsr_align_select", "vsr_weights_to_f16",
            "vsr_keyframes", "vsr_retrieve_workspace_size", "vsr_retrieve", "vsr_last_error",
            "vsr_destroy", "vsr_profile_enable", "vsr_profile_read"]
 
@@ -28,12 +28,13 @@ SELECT_STRATEGIES = {"two_stage": VSR_SELECT_TWO_STAGE, "addition": VSR_SELECT_A
                      "invert": VSR_SELECT_INVERT}
 
 VSR_STAGE_KINDS = 14
-VSR_STAGES = 2 * VSR_STAGE_KINDS
+VSR_STAGES = 3 * VSR_STAGE_KINDS
 VSR_PROFILE_ALL = (1 << VSR_STAGE_KINDS) - 1
 STAGE_KINDS = ["embed", "rmsnorm", "qkv_rope", "attention", "attn_merge", "o_proj",
                "gate_up_swiglu", "down_proj", "lm_inputs", "lm_head_lse", "lse_gather",
                "sum_argmax", "row_tables", "copy"]
-STAGE_NAMES = [f"prefill.{k}" for k in STAGE_KINDS] + [f"score.{k}" for k in STAGE_KINDS]
+STAGE_NAMES = ([f"prefill.{k}" for k in STAGE_KINDS] + [f"score.{k}" for k in STAGE_KINDS]
+               + [f"draft.{k}" for k in STAGE_KINDS])
 
 
 class VsrConfig(ctypes.Structure):
@@ -44,7 +45,7 @@ class VsrConfig(ctypes.Structure):
                 ("rope_base", ctypes.c_float), ("dtype", ctypes.c_int32),
                 ("max_prefix", ctypes.c_int32), ("max_cands", ctypes.c_int32),
                 ("max_cand_len", ctypes.c_int32), ("split_layers", ctypes.c_int32),
-                ("gemm_weights", ctypes.c_int32)]
+                ("gemm_weights", ctypes.c_int32), ("max_new", ctypes.c_int32)]
 
 
 _PP = ctypes.POINTER(ctypes.c_void_p)
@@ -94,6 +95,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                     ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p,
                                     ctypes.c_void_p]
     lib.vsr_reliability.restype = ctypes.c_int
+    lib.vsr_draft.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32),
+                              ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p]
+    lib.vsr_draft.restype = ctypes.c_int
     lib.vsr_align_select.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                                      ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                      ctypes.c_float, ctypes.c_int32, ctypes.c_void_p,
@@ -137,15 +141,16 @@ def default_split_layers(n_layers: int) -> int:
 
 def make_config(cfg, max_prefix: Optional[int] = None, max_cands: Optional[int] = None,
                 max_cand_len: Optional[int] = None, split_layers: Optional[int] = None,
-                gemm_weights: int = 0) -> VsrConfig:
+                gemm_weights: int = 0, max_new: int = 0) -> VsrConfig:
     """vsr_config from a workload.VerifierConfig (maxima default to its sizes;
-    split_layers defaults to default_split_layers(n_layers))."""
+    split_layers defaults to default_split_layers(n_layers); max_new = 0
+    reserves no draft cache)."""
     if split_layers is None:
         split_layers = default_split_layers(cfg.n_layers)
     return VsrConfig(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim,
                      cfg.d_ff, cfg.vocab, cfg.rms_eps, cfg.rope_base, cfg.dtype,
                      max_prefix or cfg.n_prefix, max_cands or cfg.n_cands,
-                     max_cand_len or cfg.cand_len, split_layers, gemm_weights)
+                     max_cand_len or cfg.cand_len, split_layers, gemm_weights, max_new)
 
 
 def workspace_size(c: VsrConfig) -> int:
@@ -162,11 +167,12 @@ class Verifier:
     gemm_weights (bf16 models): "f16" keeps fp16 copies of the GEMM weight
     matrices (the bf16 values, exact for magnitudes >= 2^-17), which the GEMMs
     load without conversion; "bf16" uses the given tensors as they are.
+    max_new: the most tokens draft() may generate per branch (0: no drafting).
     """
 
     def __init__(self, cfg, weights: Dict, device="cuda", stream=None,
                  max_prefix=None, max_cands=None, max_cand_len=None, split_layers=None,
-                 gemm_weights: str = "f16"):
+                 gemm_weights: str = "f16", max_new: int = 0):
         import torch
         self._torch = torch
         self.lib = load_library()
@@ -175,7 +181,7 @@ class Verifier:
             raise ValueError("gemm_weights must be 'f16' or 'bf16'")
         self.gemm_f16 = cfg.dtype == VSR_BF16 and gemm_weights == "f16"
         self.c = make_config(cfg, max_prefix, max_cands, max_cand_len, split_layers,
-                             VSR_F16 if self.gemm_f16 else 0)
+                             VSR_F16 if self.gemm_f16 else 0, max_new)
         size = self.lib.vsr_workspace_size(ctypes.byref(self.c))
         if size == 0:
             raise VsrError(VSR_EINVAL, "unsupported config")
@@ -256,6 +262,22 @@ class Verifier:
                                              int(yes_id), int(no_id), float(delta), _ptr(lp),
                                              _ptr(rel), _ptr(keep)))
         return lp, rel, keep
+
+    def draft(self, prompt_ids, prompt_len: Sequence[int], n_new: int, out=None):
+        """Greedy parallel drafts (Eq. 5, 8-10) after the current prefix.
+
+        prompt_ids: device int32 [M][Cmax]; prompt_len: host ints [M], each >= 1.
+        Returns a device int32 tensor [M][n_new] of generated token ids, valid
+        once the stream is synchronised.
+        """
+        torch = self._torch
+        M, cmax = int(prompt_ids.shape[0]), int(prompt_ids.shape[1])
+        lens = (ctypes.c_int32 * M)(*[int(x) for x in prompt_len])
+        if out is None:
+            out = torch.empty((M, int(n_new)), dtype=torch.int32, device=self.device)
+        self._check(self.lib.vsr_draft(self.h, _ptr(prompt_ids), lens, M, cmax, int(n_new),
+                                       _ptr(out)))
+        return out
 
     def profile(self, enable, kinds=None):
         """Turns per-stage kernel timing on or off (clears recorded launches).

@@ -88,6 +88,20 @@ template <typename TW, typename TA>
 hipError_t launch_lm_inputs(const float *x, const float *h_last, const int32_t *row_lo,
                             const TW *g, int T_rows, int d, float eps, TA *y, hipStream_t s);
 
+// Draft calls (decode cache with a fixed stride S per branch): prompt row
+// tables, per-step tables, the last prompt row's norm per branch and the
+// greedy pick from the LM-head argmax partials.
+hipError_t launch_draft_rows(const Branches &br, int P, int S, const int32_t *ids, int vocab,
+                             int32_t *row_lo, int32_t *row_pos, int32_t *cache_row,
+                             int32_t *lm_tgt, hipStream_t s);
+hipError_t launch_draft_step(const Branches &br, int P, int S, int step, int32_t *row_lo,
+                             int32_t *row_pos, int32_t *cache_row, hipStream_t s);
+template <typename TW, typename TA>
+hipError_t launch_branch_last_norm(const float *x, const Branches &br, const TW *g, int d,
+                                   float eps, TA *y, hipStream_t s);
+hipError_t launch_argmax_merge(const float2 *part, int nchunks, int M, int n_new, int step,
+                               int32_t *tokens, int32_t *next_ids, hipStream_t s);
+
 // LM-head inputs of a reliability call (2M rows): y[b] = norm(x[last row of
 // branch b % M]); lm_tgt[b] = yes_id for b < M, no_id for b >= M.
 template <typename TW, typename TA>
@@ -142,6 +156,8 @@ struct QKVOut {
   // Precise layers (MFMA path): the fp16 remainders x - fp16(x) of q, k, v in
   // planes laid out like q, k, vt (NULL: not written).
   T *q_lo = nullptr, *k_lo = nullptr, *vt_lo = nullptr;
+  // Cache position of each row's key / value (NULL: the row index).
+  const int32_t *cache_row = nullptr;
 };
 
 // ------------------------------------------------------------ MFMA path
@@ -167,6 +183,10 @@ hipError_t gemm_swiglu(const f16 *A, const void *W, bool w_f16, int rows, int F,
 // LM head: per (vocab chunk c, row t): part[c][t] = (max, sum exp(l - max)) over
 // the chunk's logits l = W[v] . A[t]; tgt_logit[t] = logit of lm_tgt[t].
 int lmhead_chunks(int vocab);
+// Greedy LM head: part[c][t] = (largest logit of vocab chunk c for row t,
+// its vocabulary index as int bits; the lowest index on ties).
+hipError_t gemm_lmargmax(const f16 *A, const void *W, bool w_f16, int rows, int vocab, int K,
+                         float2 *part, hipStream_t s);
 // dst[i] = fp16 of the bf16 src[i], the GEMMs' in-register conversion.
 hipError_t convert_bf16_to_f16(const uint16_t *src, uint16_t *dst, size_t n, hipStream_t s);
 hipError_t gemm_lmhead(const f16 *A, const void *W, bool w_f16, int rows, int vocab, int K,
@@ -199,6 +219,12 @@ struct AttnArgs {
   float2 *part_ml;      // [nchunks][n_kv][T*G]
   // Precise layers: remainder planes of q, k, vt (and bk, bvt), same layouts.
   const f16 *q_lo, *k_lo, *vt_lo, *bk_lo, *bvt_lo;
+  // Mode 1: branch-cache position of each query token (its key limit; NULL:
+  // the token index, keys packed by token) and the number of branch-cache
+  // positions that hold data or zeros (0: T). q_pos and row_lo must be
+  // non-decreasing in token order.
+  const int32_t *q_pos;
+  int bk_valid;
 };
 int attn_query_tile();  // stacked query rows per attention block
 // precise = true: q/k/v and the probabilities are carried as fp16 value +
@@ -227,11 +253,16 @@ struct SimpleAttnArgs {
   const void *q, *k, *vt, *bk, *bvt;
   int kv_npos, bk_npos;
   const int32_t *row_lo;
+  const int32_t *q_pos;  // mode 1: branch-cache position of each query (NULL: token)
   int T, t0, P, n_heads, n_kv, hd;  // query tokens t0 .. T-1
   int mode;
   void *out;
 };
 template <typename T>
 hipError_t simple_attn(const SimpleAttnArgs &a, hipStream_t s);
+// Greedy LM head of the plain path: part[t] = (largest logit, index bits).
+template <typename T>
+hipError_t simple_lmargmax(const T *A, const T *W, int rows, int vocab, int K, float2 *part,
+                           hipStream_t s);
 
 }  // namespace vsr

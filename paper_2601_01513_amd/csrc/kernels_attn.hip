@@ -80,6 +80,7 @@ struct Seg {
 
 struct Lane {
   int tok;   // query token of this lane's row
+  int qp;    // SEG_BRANCH: last visible key (the query's own cache position)
   int lo;    // SEG_BRANCH: first visible key
   float m;   // running maximum of the raw (unscaled) scores
   float l;   // running sum of exp2(s * c - m * c)
@@ -153,7 +154,7 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *st
         const int key = kb + b * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
         bool vis = key < sg.kvalid;
         if (sg.mode == SEG_CAUSAL) vis = vis && key <= L.tok;
-        if (sg.mode == SEG_BRANCH) vis = vis && key >= L.lo && key <= L.tok;
+        if (sg.mode == SEG_BRANCH) vis = vis && key >= L.lo && key <= L.qp;
         s[b][r] = vis ? s[b][r] : -INFINITY;
       }
       mloc = fmaxf(mloc, s[b][r]);
@@ -249,6 +250,7 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
   L.tok = a.t0 + rowc / G;
   const int head = kvh * G + rowc % G;
   L.lo = MODE == 1 ? a.row_lo[L.tok] : 0;
+  L.qp = MODE == 1 && a.q_pos ? a.q_pos[L.tok] : L.tok;
   L.m = -INFINITY;
   L.l = 0.f;
 #pragma unroll
@@ -293,10 +295,13 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
            PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.P, kb, ke, SEG_ALL, tok_first};
     walk_segment<PREC>(sp, lds, L, scale_log2);
     if (chunk == a.nchunks - 1) {
+      // Branch keys from the block's first query's segment start to its last
+      // query's position (both non-decreasing in token order).
       const int lo = a.row_lo[tok_first] & ~(KT - 1);
+      const int hi = a.q_pos ? a.q_pos[tok_last] : tok_last;
       Seg sb{a.bk + boff, a.bvt + boff, PREC ? a.bk_lo + boff : nullptr,
-             PREC ? a.bvt_lo + boff : nullptr, a.bk_npos, a.T, lo, tok_last + 1, SEG_BRANCH,
-             tok_first};
+             PREC ? a.bvt_lo + boff : nullptr, a.bk_npos, a.bk_valid ? a.bk_valid : a.T, lo,
+             hi + 1, SEG_BRANCH, tok_first};
       walk_segment<PREC>(sb, lds, L, scale_log2);
     }
   }

@@ -488,7 +488,8 @@ __device__ __forceinline__ void qkv_store(const QKVOut<f16> &o, int n_heads, int
       o.q_lo[off + d + 64] = l2;
     }
   } else if (slot < n_heads + n_kv) {
-    const long off = ((long)(slot - n_heads) * o.kv_npos + row) * 128;
+    const int crow = o.cache_row ? o.cache_row[row] : row;
+    const long off = ((long)(slot - n_heads) * o.kv_npos + crow) * 128;
     o.k[off + d] = h1;
     o.k[off + d + 64] = h2;
     if (o.k_lo) {
@@ -499,7 +500,8 @@ __device__ __forceinline__ void qkv_store(const QKVOut<f16> &o, int n_heads, int
     // Values go to the Vt cache at the attention kernel's interleaved
     // position: within each aligned group of 16, quarters 1 and 2 swap.
     const long base = (long)(slot - n_heads - n_kv) * 128 * o.kv_npos;
-    const int pp = (row & ~12) | ((row & 4) << 1) | ((row & 8) >> 1);
+    const int crow = o.cache_row ? o.cache_row[row] : row;
+    const int pp = (crow & ~12) | ((crow & 4) << 1) | ((crow & 8) >> 1);
     const long o1 = base + (long)d * o.kv_npos + pp, o2 = base + (long)(d + 64) * o.kv_npos + pp;
     o.vt[o1] = h1;
     o.vt[o2] = h2;
@@ -653,6 +655,73 @@ __global__ __launch_bounds__(NT) void k_gemm_lmhead(const f16 *__restrict__ Hn,
   }
 }
 
+// Greedy variant of the LM head: per (vocab tile, token) the largest logit and
+// its vocabulary index (the lowest on ties), part[c][t] = (max, index bits).
+template <class TL, bool WCVT>
+__global__ __launch_bounds__(NT) void k_gemm_lmargmax(const f16 *__restrict__ Hn,
+                                                      const uint16_t *__restrict__ Wlm, int T,
+                                                      int vocab, int K, Launch ln,
+                                                      float2 *__restrict__ part) {
+  __shared__ u32x4 lds[2 * TL::STAGE];
+  __shared__ float redv[TL::WM][TL::BN];
+  __shared__ int redi[TL::WM][TL::BN];
+  const Work wk = block_work(ln);
+  const int m0 = wk.tm * TL::BM, n0 = wk.tn * TL::BN;
+  f32x16 acc[TL::FM][TL::FN];
+  mainloop<TL, WCVT, false>(
+      Wlm, [=](int r) { return min(m0 + r, vocab - 1); }, Hn,
+      [=](int r) { return min(n0 + r, T - 1); }, K, 1, 0, K / BK, lds, acc);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int wm = w / TL::WN, wn = w % TL::WN;
+#pragma unroll
+  for (int fn = 0; fn < TL::FN; ++fn) {
+    float v = -INFINITY;
+    int vi = -1;
+    // Rows increase with (fm, r) in a lane, so a strict > keeps the lowest.
+#pragma unroll
+    for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + acc_row<TL>(wm, fm, r, lane);
+        if (row < vocab && (vi < 0 || acc[fm][fn][r] > v)) {
+          v = acc[fm][fn][r];
+          vi = row;
+        }
+      }
+    const float v2 = __shfl_xor(v, 32, 64);
+    const int i2 = __shfl_xor(vi, 32, 64);
+    if (i2 >= 0 && (vi < 0 || v2 > v || (v2 == v && i2 < vi))) {
+      v = v2;
+      vi = i2;
+    }
+    if (lane < 32) {
+      redv[wm][acc_col<TL>(wn, fn, lane)] = v;
+      redi[wm][acc_col<TL>(wn, fn, lane)] = vi;
+    }
+  }
+  __syncthreads();
+  if (wm == 0 && lane < 32) {
+#pragma unroll
+    for (int fn = 0; fn < TL::FN; ++fn) {
+      const int c = acc_col<TL>(wn, fn, lane);
+      const int t = n0 + c;
+      if (t >= T) continue;
+      float v = redv[0][c];
+      int vi = redi[0][c];
+#pragma unroll
+      for (int i = 1; i < TL::WM; ++i) {
+        const float v2 = redv[i][c];
+        const int i2 = redi[i][c];
+        if (i2 >= 0 && (vi < 0 || v2 > v || (v2 == v && i2 < vi))) {
+          v = v2;
+          vi = i2;
+        }
+      }
+      part[(long)wk.tm * T + t] = make_float2(v, __int_as_float(vi));
+    }
+  }
+}
+
 }  // namespace
 
 size_t gemm_split_floats(int rows, int N, int K) {
@@ -720,6 +789,16 @@ hipError_t gemm_lmhead(const f16 *A, const void *W, bool w_f16, int rows, int vo
   const int nm = lmhead_chunks(vocab), nn = (rows + TL::BN - 1) / TL::BN;
   const Launch ln{nm, nn, 1, nm * nn, 0, 1};
   VSR_WLAUNCH(k_gemm_lmhead, ln.blocks(), A, W16, rows, vocab, K, ln, lm_tgt, part, tgt_logit);
+  return hipGetLastError();
+}
+
+hipError_t gemm_lmargmax(const f16 *A, const void *W, bool w_f16, int rows, int vocab, int K,
+                         float2 *part, hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  typedef TileStd TL;
+  const int nm = lmhead_chunks(vocab), nn = (rows + TL::BN - 1) / TL::BN;
+  const Launch ln{nm, nn, 1, nm * nn, 0, 1};
+  VSR_WLAUNCH(k_gemm_lmargmax, ln.blocks(), A, W16, rows, vocab, K, ln, part);
   return hipGetLastError();
 }
 

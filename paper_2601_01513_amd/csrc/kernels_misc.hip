@@ -58,6 +58,78 @@ hipError_t launch_row_tables(const Branches &br, int P, const int32_t *cand_ids,
   return hipGetLastError();
 }
 
+// Row tables of a draft call. Prompt row t of branch m at offset j sits at
+// decode-cache position m S + j (a fixed stride S per branch, room for the
+// prompt and the new tokens): row_lo = m S, row_pos = P + j (rotary),
+// cache_row = m S + j, lm_tgt = the prompt id (clamped).
+__global__ void k_draft_rows(Branches br, int P, int S, const int32_t *ids, int vocab,
+                             int32_t *row_lo, int32_t *row_pos, int32_t *cache_row,
+                             int32_t *lm_tgt) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= br.cu[br.M]) return;
+  int m = 0;
+  while (br.cu[m + 1] <= t) ++m;
+  const int j = t - br.cu[m];
+  int id = ids[(long)m * br.cmax + j];
+  if (id < 0 || id >= vocab) id = 0;
+  row_lo[t] = m * S;
+  row_pos[t] = P + j;
+  cache_row[t] = m * S + j;
+  lm_tgt[t] = id;
+}
+
+hipError_t launch_draft_rows(const Branches &br, int P, int S, const int32_t *ids, int vocab,
+                             int32_t *row_lo, int32_t *row_pos, int32_t *cache_row,
+                             int32_t *lm_tgt, hipStream_t s) {
+  const int T = br.cu[br.M];
+  k_draft_rows<<<(T + 255) / 256, 256, 0, s>>>(br, P, S, ids, vocab, row_lo, row_pos,
+                                               cache_row, lm_tgt);
+  return hipGetLastError();
+}
+
+// Decode step s >= 1: row m is new token s - 1 of branch m, at branch offset
+// n_m + s - 1.
+__global__ void k_draft_step(Branches br, int P, int S, int step, int32_t *row_lo,
+                             int32_t *row_pos, int32_t *cache_row) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= br.M) return;
+  const int j = br.cu[m + 1] - br.cu[m] + step - 1;
+  row_lo[m] = m * S;
+  row_pos[m] = P + j;
+  cache_row[m] = m * S + j;
+}
+
+hipError_t launch_draft_step(const Branches &br, int P, int S, int step, int32_t *row_lo,
+                             int32_t *row_pos, int32_t *cache_row, hipStream_t s) {
+  k_draft_step<<<(br.M + 63) / 64, 64, 0, s>>>(br, P, S, step, row_lo, row_pos, cache_row);
+  return hipGetLastError();
+}
+
+// Greedy pick per row from the LM-head partials (chunks in vocabulary order,
+// each holding its lowest best index): tokens[m][step] and the next inputs.
+__global__ void k_argmax_merge(const float2 *part, int nchunks, int M, int n_new, int step,
+                               int32_t *tokens, int32_t *next_ids) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= M) return;
+  float best = part[m].x;
+  int bi = __float_as_int(part[m].y);
+  for (int c = 1; c < nchunks; ++c) {
+    const float2 p = part[(long)c * M + m];
+    if (p.x > best) {
+      best = p.x;
+      bi = __float_as_int(p.y);
+    }
+  }
+  tokens[(long)m * n_new + step] = bi;
+  next_ids[m] = bi;
+}
+
+hipError_t launch_argmax_merge(const float2 *part, int nchunks, int M, int n_new, int step,
+                               int32_t *tokens, int32_t *next_ids, hipStream_t s) {
+  k_argmax_merge<<<(M + 63) / 64, 64, 0, s>>>(part, nchunks, M, n_new, step, tokens, next_ids);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------- embedding
 template <typename T>
 __global__ void k_embed_prefix(const T *visual, int n_visual, const int32_t *ids,
@@ -150,6 +222,23 @@ hipError_t launch_lm_inputs(const float *x, const float *h_last, const int32_t *
                             const TW *g, int T_rows, int d, float eps, TA *y, hipStream_t s) {
   if (T_rows == 0) return hipSuccess;
   k_lm_inputs<TW, TA><<<T_rows, 256, 0, s>>>(x, h_last, row_lo, g, d, eps, y);
+  return hipGetLastError();
+}
+
+// Draft prompt stage: block m normalises the last prompt row of branch m.
+template <typename TW, typename TA>
+__global__ __launch_bounds__(256) void k_branch_last_norm(const float *x, Branches br,
+                                                          const TW *g, int d, float eps,
+                                                          TA *y) {
+  __shared__ float red[4];
+  const int m = blockIdx.x;
+  norm_row(x + (long)(br.cu[m + 1] - 1) * d, g, d, eps, y + (long)m * d, red);
+}
+
+template <typename TW, typename TA>
+hipError_t launch_branch_last_norm(const float *x, const Branches &br, const TW *g, int d,
+                                   float eps, TA *y, hipStream_t s) {
+  k_branch_last_norm<TW, TA><<<br.M, 256, 0, s>>>(x, br, g, d, eps, y);
   return hipGetLastError();
 }
 
@@ -374,7 +463,10 @@ VSR_INST(bf16)
                                                const TW *, int, int, float, TA *, hipStream_t); \
   template hipError_t launch_last_inputs<TW, TA>(const float *, const Branches &, const TW *, \
                                                  int, float, int, int, TA *, int32_t *,       \
-                                                 hipStream_t);
+                                                 hipStream_t);                                \
+  template hipError_t launch_branch_last_norm<TW, TA>(const float *, const Branches &,        \
+                                                      const TW *, int, float, TA *,           \
+                                                      hipStream_t);
 VSR_INST2(float, float)
 VSR_INST2(bf16, f16)
 #undef VSR_INST2

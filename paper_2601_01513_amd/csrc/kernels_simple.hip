@@ -37,13 +37,15 @@ __global__ void k_simple_qkv(const T *A, const T *W, int K, int n_heads, int n_k
     q[i] = from_f32<T>(x1);
     q[i + half] = from_f32<T>(x2);
   } else if (slot < n_heads + n_kv) {
-    T *k = o.k + ((long)(slot - n_heads) * o.kv_npos + row) * hd;
+    const int crow = o.cache_row ? o.cache_row[row] : row;
+    T *k = o.k + ((long)(slot - n_heads) * o.kv_npos + crow) * hd;
     k[i] = from_f32<T>(x1);
     k[i + half] = from_f32<T>(x2);
   } else {
+    const int crow = o.cache_row ? o.cache_row[row] : row;
     T *vt = o.vt + (long)(slot - n_heads - n_kv) * hd * o.kv_npos;
-    vt[(long)i * o.kv_npos + row] = from_f32<T>(x1);
-    vt[(long)(i + half) * o.kv_npos + row] = from_f32<T>(x2);
+    vt[(long)i * o.kv_npos + crow] = from_f32<T>(x1);
+    vt[(long)(i + half) * o.kv_npos + crow] = from_f32<T>(x2);
   }
 }
 
@@ -138,6 +140,50 @@ hipError_t simple_lmhead(const T *A, const T *W, int rows, int vocab, int K,
   return hipGetLastError();
 }
 
+// Greedy variant: one block per row; each thread keeps the first best of its
+// strided vocabulary subset, then a tree reduction prefers the lower index.
+template <typename T>
+__global__ __launch_bounds__(256) void k_simple_lmargmax(const T *A, const T *W, int vocab,
+                                                         int K, float2 *part) {
+  __shared__ float sv[256];
+  __shared__ int si[256];
+  const int t = blockIdx.x;
+  const T *a = A + (long)t * K;
+  float best = -INFINITY;
+  int bi = -1;
+  for (int v = threadIdx.x; v < vocab; v += 256) {
+    const float l = dot_row(a, W + (long)v * K, K);
+    if (bi < 0 || l > best) {
+      best = l;
+      bi = v;
+    }
+  }
+  sv[threadIdx.x] = best;
+  si[threadIdx.x] = bi;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) {
+      const float v2 = sv[threadIdx.x + w];
+      const int i2 = si[threadIdx.x + w];
+      if (i2 >= 0 && (si[threadIdx.x] < 0 || v2 > sv[threadIdx.x] ||
+                      (v2 == sv[threadIdx.x] && i2 < si[threadIdx.x]))) {
+        sv[threadIdx.x] = v2;
+        si[threadIdx.x] = i2;
+      }
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) part[t] = make_float2(sv[0], __int_as_float(si[0]));
+}
+
+template <typename T>
+hipError_t simple_lmargmax(const T *A, const T *W, int rows, int vocab, int K, float2 *part,
+                           hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  k_simple_lmargmax<T><<<rows, 256, 0, s>>>(A, W, vocab, K, part);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------- attention
 // One wave per (token, query head); online softmax over the visible keys in
 // position order. Lane l owns dims l, l+64, ... of the head.
@@ -178,7 +224,7 @@ __global__ __launch_bounds__(64) void k_simple_attn(SimpleAttnArgs a) {
     attend_keys(kc, vtc, a.kv_npos, 0, a.P - 1, hd, qr, m, l, acc);
     const T *bk = (const T *)a.bk + (long)kv * a.bk_npos * hd;
     const T *bvt = (const T *)a.bvt + (long)kv * hd * a.bk_npos;
-    attend_keys(bk, bvt, a.bk_npos, a.row_lo[t], t, hd, qr, m, l, acc);
+    attend_keys(bk, bvt, a.bk_npos, a.row_lo[t], a.q_pos ? a.q_pos[t] : t, hd, qr, m, l, acc);
   }
   T *o = (T *)a.out + ((long)t * a.n_heads + h) * hd;
   const float inv = 1.f / l;
@@ -200,7 +246,9 @@ hipError_t simple_attn(const SimpleAttnArgs &a, hipStream_t s) {
   template hipError_t simple_swiglu<T>(const T *, const T *, int, int, int, T *, hipStream_t); \
   template hipError_t simple_lmhead<T>(const T *, const T *, int, int, int, const int32_t *,  \
                                        float2 *, float *, hipStream_t);                       \
-  template hipError_t simple_attn<T>(const SimpleAttnArgs &, hipStream_t);
+  template hipError_t simple_attn<T>(const SimpleAttnArgs &, hipStream_t);                    \
+  template hipError_t simple_lmargmax<T>(const T *, const T *, int, int, int, float2 *,       \
+                                         hipStream_t);
 VSR_INST(float)
 VSR_INST(bf16)
 #undef VSR_INST

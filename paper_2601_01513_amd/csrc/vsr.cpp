@@ -43,9 +43,11 @@ Split cascade_split(int T, int P, int n_heads, int n_kv) {
 
 struct Plan {
   int kv_npos, bk_npos, max_t, rows_max, rope_npos, lm_chunks;
+  int dec_S, dec_npos;  // draft cache: positions per branch, capacity (0: none)
   int lm_rows;  // LM-head rows: candidate rows, or 2 per branch (reliability)
-  size_t x, xn, q, q_lo, attn, h, kc, vtc, kc_lo, vtc_lo, bk, bvt, bk_lo, bvt_lo, part_acc,
-      part_ml, lm_part, tgt, row_lo, row_pos, lm_tgt, rope, h_last, gemm_part, total;
+  size_t x, xn, q, q_lo, attn, h, kc, vtc, kc_lo, vtc_lo, bk, bvt, bk_lo, bvt_lo, kd, vtd,
+      kd_lo, vtd_lo, part_acc, part_ml, lm_part, tgt, row_lo, row_pos, cache_row, dec_ids,
+      lm_tgt, rope, h_last, gemm_part, total;
 };
 
 // Returns an empty message if cfg is supported.
@@ -63,6 +65,7 @@ std::string check_config(const vsr_config *c) {
   if (c->max_prefix > (1 << 24)) return "max_prefix too large";
   if (c->split_layers < 0 || c->split_layers > c->n_layers)
     return "split_layers must be in [0, n_layers]";
+  if (c->max_new < 0 || c->max_new > 4096) return "max_new must be in [0, 4096]";
   if (c->dtype == VSR_BF16 ? (c->gemm_weights != 0 && c->gemm_weights != VSR_BF16 &&
                               c->gemm_weights != VSR_F16)
                            : c->gemm_weights != 0)
@@ -88,7 +91,9 @@ Plan make_plan(const vsr_config &c) {
   p.bk_npos = (int)align_up(p.max_t, 64);
   p.lm_rows = std::max(p.max_t, 2 * c.max_cands);
   p.rows_max = std::max(c.max_prefix, p.lm_rows);
-  p.rope_npos = p.kv_npos + c.max_cand_len;
+  p.dec_S = c.max_new > 0 ? c.max_cand_len + c.max_new : 0;
+  p.dec_npos = c.max_new > 0 ? (int)align_up((size_t)c.max_cands * p.dec_S, 64) : 0;
+  p.rope_npos = p.kv_npos + c.max_cand_len + c.max_new;
   p.lm_chunks = c.dtype == VSR_BF16 ? lmhead_chunks(c.vocab) : 1;
   // Largest partial-row count of the cascade split over every T <= max_t.
   size_t part_rows = 0;
@@ -141,12 +146,20 @@ Plan make_plan(const vsr_config &c) {
   p.bvt = take(branch_cache);
   p.bk_lo = take(nprec ? branch_cache : 0);
   p.bvt_lo = take(nprec ? branch_cache : 0);
+  // Draft cache: every layer's keys / values of the branches being decoded.
+  const size_t dec_cache = (size_t)c.n_kv_heads * p.dec_npos * hd * E;
+  p.kd = take(c.n_layers * dec_cache);
+  p.vtd = take(c.n_layers * dec_cache);
+  p.kd_lo = take(nprec * dec_cache);
+  p.vtd_lo = take(nprec * dec_cache);
   p.part_acc = take(part_rows * c.n_kv_heads * hd * 4);
   p.part_ml = take(part_rows * c.n_kv_heads * 8);
   p.lm_part = take((size_t)p.lm_chunks * p.lm_rows * 8);
   p.tgt = take((size_t)p.lm_rows * 4);
   p.row_lo = take((size_t)p.max_t * 4);
   p.row_pos = take((size_t)p.max_t * 4);
+  p.cache_row = take((size_t)p.max_t * 4);
+  p.dec_ids = take((size_t)c.max_cands * 4);
   p.lm_tgt = take((size_t)p.lm_rows * 4);
   p.rope = take((size_t)p.rope_npos * (hd / 2) * 8);
   p.h_last = take(d * 4);
@@ -176,7 +189,7 @@ struct vsr_ctx {
     hipEvent_t a, b;
   };
   int prof = 0;  // bitmask of the stage kinds being timed
-  int phase = 0;  // 0 prefix pass, 1 candidate pass
+  int phase = 0;  // 0 prefix pass, 1 candidate pass, 2 draft pass
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
   hipEvent_t event() {
@@ -342,7 +355,13 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
   TA *xn = c->at<TA>(p.xn), *q = c->at<TA>(p.q), *attn = c->at<TA>(p.attn), *h = c->at<TA>(p.h);
   float *gpart = c->at<float>(p.gemm_part);
   const size_t layer_cache = (size_t)Hkv * p.kv_npos * hd;
+  const size_t layer_dec = (size_t)Hkv * p.dec_npos * hd;
   const bool wf16 = cf.gemm_weights == VSR_F16;  // GEMM weights stored as fp16
+  // mode 2 (draft): branch keys/values go to the persistent draft cache at
+  // the rows' cache positions; queries see the prefix and their branch up to
+  // their own position.
+  const bool draft = mode == 2;
+  const int32_t *cache_row = draft ? c->at<int32_t>(p.cache_row) : nullptr;
   hipStream_t s = c->stream;
   for (int l = 0; l < cf.n_layers; ++l) {
     const TW *wqkv = static_cast<const TW *>(c->wqkv[l]);
@@ -366,16 +385,27 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       qo.vt = vtc;
       qo.kv_npos = p.kv_npos;
       qo.row_pos = nullptr;
-    } else {
+    } else if (!draft) {
       qo.k = c->at<TA>(p.bk);
       qo.vt = c->at<TA>(p.bvt);
       qo.kv_npos = p.bk_npos;
       qo.row_pos = c->at<int32_t>(p.row_pos);
+    } else {
+      qo.k = c->at<TA>(p.kd) + l * layer_dec;
+      qo.vt = c->at<TA>(p.vtd) + l * layer_dec;
+      qo.kv_npos = p.dec_npos;
+      qo.row_pos = c->at<int32_t>(p.row_pos);
+      qo.cache_row = cache_row;
     }
+    TA *bk = draft ? c->at<TA>(p.kd) + l * layer_dec : c->at<TA>(p.bk);
+    TA *bvt = draft ? c->at<TA>(p.vtd) + l * layer_dec : c->at<TA>(p.bvt);
+    TA *bk_lo = draft ? c->at<TA>(p.kd_lo) + l * layer_dec : c->at<TA>(p.bk_lo);
+    TA *bvt_lo = draft ? c->at<TA>(p.vtd_lo) + l * layer_dec : c->at<TA>(p.bvt_lo);
+    const int bk_npos = draft ? p.dec_npos : p.bk_npos;
     if (precise) {
       qo.q_lo = c->at<TA>(p.q_lo);
-      qo.k_lo = mode == 0 ? c->at<TA>(p.kc_lo) + l * layer_cache : c->at<TA>(p.bk_lo);
-      qo.vt_lo = mode == 0 ? c->at<TA>(p.vtc_lo) + l * layer_cache : c->at<TA>(p.bvt_lo);
+      qo.k_lo = mode == 0 ? c->at<TA>(p.kc_lo) + l * layer_cache : bk_lo;
+      qo.vt_lo = mode == 0 ? c->at<TA>(p.vtc_lo) + l * layer_cache : bvt_lo;
     }
     if constexpr (kMfma) {
       STAGE(c, K_QKV, "qkv projection",
@@ -396,9 +426,11 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       a.k = kc;
       a.vt = vtc;
       a.kv_npos = p.kv_npos;
-      a.bk = c->at<f16>(p.bk);
-      a.bvt = c->at<f16>(p.bvt);
-      a.bk_npos = p.bk_npos;
+      a.bk = bk;
+      a.bvt = bvt;
+      a.bk_npos = bk_npos;
+      a.q_pos = cache_row;
+      a.bk_valid = draft ? p.dec_npos : 0;
       a.row_lo = c->at<int32_t>(p.row_lo);
       a.T = rows;
       a.P = c->P;
@@ -414,8 +446,8 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
         a.q_lo = c->at<f16>(p.q_lo);
         a.k_lo = c->at<f16>(p.kc_lo) + l * layer_cache;
         a.vt_lo = c->at<f16>(p.vtc_lo) + l * layer_cache;
-        a.bk_lo = c->at<f16>(p.bk_lo);
-        a.bvt_lo = c->at<f16>(p.bvt_lo);
+        a.bk_lo = bk_lo;
+        a.bvt_lo = bvt_lo;
       }
       if (mode == 0) {
         STAGE(c, K_ATTN, "prefill attention", attn_prefill(a, precise, s));
@@ -429,17 +461,18 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       a.k = kc;
       a.vt = vtc;
       a.kv_npos = p.kv_npos;
-      a.bk = c->at<TA>(p.bk);
-      a.bvt = c->at<TA>(p.bvt);
-      a.bk_npos = p.bk_npos;
+      a.bk = bk;
+      a.bvt = bvt;
+      a.bk_npos = bk_npos;
       a.row_lo = c->at<int32_t>(p.row_lo);
+      a.q_pos = cache_row;
       a.T = rows;
       a.P = c->P;
       a.n_heads = Hq;
       a.n_kv = Hkv;
       a.hd = hd;
       a.t0 = r0;
-      a.mode = mode;
+      a.mode = mode == 0 ? 0 : 1;
       a.out = attn;
       STAGE(c, K_ATTN, "attention", simple_attn<TA>(a, s));
     }
@@ -582,6 +615,70 @@ int reliability_impl(vsr_ctx *c, const Branches &br, const int32_t *ids, int yes
   return VSR_OK;
 }
 
+// Greedy drafts: the prompt rows of every branch through all layers (keys /
+// values kept in the draft cache), then n_new steps of one row per branch.
+// Each step's LM head picks the next token on the device and feeds it to the
+// next step's embedding, so the loop never waits for the host.
+template <typename TW, typename TA>
+int draft_impl(vsr_ctx *c, const Branches &br, const int32_t *ids, int n_new, int32_t *tokens) {
+  constexpr bool kMfma = std::is_same<TA, f16>::value;
+  const vsr_config &cf = c->cfg;
+  const Plan &p = c->plan;
+  hipStream_t s = c->stream;
+  const int M = br.M, T_rows = br.cu[M];
+  int32_t *row_lo = c->at<int32_t>(p.row_lo), *row_pos = c->at<int32_t>(p.row_pos);
+  int32_t *cache_row = c->at<int32_t>(p.cache_row), *lm_tgt = c->at<int32_t>(p.lm_tgt);
+  int32_t *next_ids = c->at<int32_t>(p.dec_ids);
+  float *x = c->at<float>(p.x);
+  TA *lm_in = c->at<TA>(p.xn);
+  float2 *part = c->at<float2>(p.lm_part);
+  const TW *g = static_cast<const TW *>(c->final_norm);
+  const bool wf16 = cf.gemm_weights == VSR_F16;
+  const int chunks = kMfma ? lmhead_chunks(cf.vocab) : 1;
+  auto pick = [&](int step) -> int {
+    if constexpr (kMfma) {
+      STAGE(c, K_LMHEAD, "draft lm head",
+            gemm_lmargmax(lm_in, c->lm_head, wf16, M, cf.vocab, cf.d_model, part, s));
+    } else {
+      STAGE(c, K_LMHEAD, "draft lm head",
+            simple_lmargmax<TA>(lm_in, static_cast<const TW *>(c->lm_head), M, cf.vocab,
+                                cf.d_model, part, s));
+    }
+    STAGE(c, K_SELECT, "draft pick",
+          launch_argmax_merge(part, chunks, M, n_new, step, tokens, next_ids, s));
+    return VSR_OK;
+  };
+  STAGE(c, K_ROWS, "draft rows",
+        launch_draft_rows(br, c->P, p.dec_S, ids, cf.vocab, row_lo, row_pos, cache_row, lm_tgt,
+                          s));
+  STAGE(c, K_EMBED, "draft embedding",
+        launch_embed_rows<TW>(lm_tgt, T_rows, static_cast<const TW *>(c->embed), cf.d_model,
+                              x, s));
+  const Split split0 =
+      kMfma ? cascade_split(T_rows, c->P, cf.n_heads, cf.n_kv_heads) : Split{1, 0};
+  int rc = run_layers<TW, TA>(c, T_rows, 2, split0);
+  if (rc) return rc;
+  STAGE(c, K_LMIN, "draft inputs",
+        launch_branch_last_norm<TW, TA>(x, br, g, cf.d_model, cf.rms_eps, lm_in, s));
+  rc = pick(0);
+  if (rc) return rc;
+  const Split split1 = kMfma ? cascade_split(M, c->P, cf.n_heads, cf.n_kv_heads) : Split{1, 0};
+  for (int step = 1; step < n_new; ++step) {
+    STAGE(c, K_ROWS, "draft step rows",
+          launch_draft_step(br, c->P, p.dec_S, step, row_lo, row_pos, cache_row, s));
+    STAGE(c, K_EMBED, "draft step embedding",
+          launch_embed_rows<TW>(next_ids, M, static_cast<const TW *>(c->embed), cf.d_model, x,
+                                s));
+    rc = run_layers<TW, TA>(c, M, 2, split1);
+    if (rc) return rc;
+    STAGE(c, K_LMIN, "draft step inputs",
+          launch_rmsnorm<TW, TA>(x, g, M, cf.d_model, cf.rms_eps, lm_in, 1, s));
+    rc = pick(step);
+    if (rc) return rc;
+  }
+  return VSR_OK;
+}
+
 int set_device(vsr_ctx *c) {
   int cur = -1;
   if (hipGetDevice(&cur) == hipSuccess && cur == c->device) return VSR_OK;
@@ -679,6 +776,38 @@ extern "C" int vsr_reliability(vsr_ctx *ctx, const int32_t *branch_ids,
                                            rel, keep)
              : reliability_impl<float, float>(ctx, br, branch_ids, yes_id, no_id, delta,
                                               lp_yes_no, rel, keep);
+}
+
+extern "C" int vsr_draft(vsr_ctx *ctx, const int32_t *prompt_ids, const int32_t *prompt_len,
+                         int32_t M, int32_t Cmax, int32_t n_new, int32_t *tokens) {
+  if (!ctx) return VSR_EINVAL;
+  if (!ctx->prefilled) return ctx->fail(VSR_ESTATE, "draft before a successful prefill");
+  if (ctx->cfg.max_new < 1) return ctx->fail(VSR_ESTATE, "context created with max_new = 0");
+  if (M < 1 || Cmax < 1) return ctx->fail(VSR_EINVAL, "M and Cmax must be >= 1");
+  if (M > ctx->cfg.max_cands)
+    return ctx->fail(VSR_ERANGE, "M = %d exceeds max_cands %d", M, ctx->cfg.max_cands);
+  if (Cmax > ctx->cfg.max_cand_len)
+    return ctx->fail(VSR_ERANGE, "Cmax = %d exceeds max_cand_len %d", Cmax,
+                     ctx->cfg.max_cand_len);
+  if (n_new < 1 || n_new > ctx->cfg.max_new)
+    return ctx->fail(VSR_ERANGE, "n_new = %d outside [1, max_new = %d]", n_new,
+                     ctx->cfg.max_new);
+  if (!prompt_ids || !prompt_len || !tokens) return ctx->fail(VSR_EINVAL, "draft: NULL argument");
+  Branches br{};
+  br.M = M;
+  br.cmax = Cmax;
+  br.cu[0] = 0;
+  for (int m = 0; m < M; ++m) {
+    if (prompt_len[m] < 1 || prompt_len[m] > Cmax)
+      return ctx->fail(VSR_EINVAL, "prompt_len[%d] = %d outside [1, Cmax]", m, prompt_len[m]);
+    br.cu[m + 1] = br.cu[m] + prompt_len[m];
+  }
+  const int rc = set_device(ctx);
+  if (rc) return rc;
+  ctx->phase = 2;
+  return ctx->cfg.dtype == VSR_BF16
+             ? draft_impl<bf16, f16>(ctx, br, prompt_ids, n_new, tokens)
+             : draft_impl<float, float>(ctx, br, prompt_ids, n_new, tokens);
 }
 
 extern "C" int vsr_align_select(const float *ent, const float *frames, int32_t M, int32_t NF,

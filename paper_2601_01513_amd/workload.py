@@ -100,6 +100,17 @@ B32 = VerifierConfig(
     cand_len=128)
 
 CONFIGS: List[VerifierConfig] = [TINY_F32, B1_5, B7, B7_LONG, B32]
+
+# Drafting (Eq. 5, 8-10): a 3B-class drafter (36 layers, d 2048, 16/2 heads,
+# d_ff 11008) continues k = 3 branches, one per retrieved document, after the
+# shared (visual, question) prefix: 2048 visual rows + 128 question tokens,
+# each branch prompt a 512-token document plus its generation prompt, 64 new
+# tokens per branch (the entity, reasoning and answer generations together).
+DRAFT_3B = VerifierConfig(
+    name="3B-class drafter bf16 P2176 3 branches x 512 + 64 new", n_layers=36, d_model=2048,
+    n_heads=16, n_kv_heads=2, head_dim=128, d_ff=11008, vocab=151936, rope_base=1e6,
+    dtype=BF16, n_prefix=2176, n_visual=2048, n_cands=3, cand_len=512)
+DRAFT_NEW = 64
 HEADLINE = B7
 
 

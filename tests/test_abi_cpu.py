@@ -42,7 +42,7 @@ def test_workspace_size_of_each_workload(cfg):
     ("n_heads", 5), ("head_dim", 64), ("d_model", 100), ("dtype", 7), ("max_cands", 0),
     ("max_cands", B.VSR_MAX_CANDS + 1), ("vocab", 0), ("max_prefix", 0), ("d_ff", 96),
     ("split_layers", -1), ("split_layers", W.B1_5.n_layers + 1), ("gemm_weights", 3),
-    ("gemm_weights", -1)])
+    ("gemm_weights", -1), ("max_new", -1), ("max_new", 4097)])
 def test_invalid_configs_have_no_workspace(field, value):
     _lib()
     c = B.make_config(W.B1_5)
@@ -126,6 +126,27 @@ def test_reliability_without_context_fails_cleanly():
     lens = (ctypes.c_int32 * 1)(1)
     assert lib.vsr_reliability(None, None, lens, 1, 1, 0, 1, 0.05, None, None, None) == \
         B.VSR_EINVAL
+
+
+def test_draft_without_context_fails_cleanly():
+    lib = _lib()
+    lens = (ctypes.c_int32 * 1)(1)
+    assert lib.vsr_draft(None, None, lens, 1, 1, 1, None) == B.VSR_EINVAL
+
+
+def test_draft_cache_is_sized_by_max_new():
+    """The draft cache holds L layers of keys and values for max_cands
+    branches of max_cand_len + max_new positions (64-aligned) in the
+    activation type; the rotary table gains max_new positions."""
+    _lib()
+    cfg = W.B1_5
+    base = B.workspace_size(B.make_config(cfg, split_layers=0))
+    for n in (1, 64, 4096):
+        grown = B.workspace_size(B.make_config(cfg, split_layers=0, max_new=n))
+        npos = -(-cfg.n_cands * (cfg.cand_len + n) // 64) * 64
+        cache = 2 * cfg.n_layers * cfg.n_kv_heads * npos * cfg.head_dim * 2
+        rope = n * cfg.head_dim * 4      # (cos, sin) float pairs of the extra positions
+        assert 0 <= grown - base - cache - rope <= 4 * 256, (n, grown - base, cache + rope)
 
 
 def test_fp32_contexts_take_no_gemm_weight_format():

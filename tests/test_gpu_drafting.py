@@ -1,0 +1,224 @@
+"""GPU parity of the parallel draft generation (Section 3.1, Eq. 5; Section
+3.2, Eq. 8-10): vsr_draft through the C ABI against the CPU oracle
+(oracle/drafting.py) on the same seeded inputs.
+
+Greedy tokens are integers decided by floating point, so the check teacher-
+forces the GPU's own tokens through the oracle and asks, at every step, that
+the GPU's token be a valid greedy choice under the per-token bound of the
+scoring pass (2e-2 for bf16 contexts, 1e-4 for fp32): each of the two logits
+compared may be off by that much, so the oracle's logit of the GPU token must
+be within twice the bound of the oracle's largest logit, and wherever the
+oracle's top-2 gap exceeds twice the bound the token must be the oracle's
+argmax exactly. Along a path where every gap is that clear, this is equality
+with the oracle's own greedy decode, which is also checked directly.
+"""
+import sys
+import time
+
+import numpy as np
+import pytest
+
+from oracle import drafting as D
+from paper_2601_01513_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _say(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+SMALL_BF16 = W.VerifierConfig(
+    name="small bf16 L2 d256 G2 F320 V1000", n_layers=2, d_model=256, n_heads=4,
+    n_kv_heads=2, head_dim=128, d_ff=320, vocab=1000, rope_base=1e6, dtype=W.BF16,
+    n_prefix=300, n_visual=100, n_cands=5, cand_len=40)
+GQA7_BF16 = W.VerifierConfig(
+    name="small bf16 L2 d896 G7 P700 M8x64", n_layers=2, d_model=896, n_heads=7,
+    n_kv_heads=1, head_dim=128, d_ff=1152, vocab=3001, rope_base=1e6, dtype=W.BF16,
+    n_prefix=700, n_visual=300, n_cands=8, cand_len=64)
+
+
+def _prompts(wl, seed):
+    """Prompt lengths in [1, Cmax] (the longest and the shortest present)."""
+    rng = np.random.default_rng(seed + 200)
+    cfg = wl.cfg
+    lens = rng.integers(1, cfg.cand_len + 1, size=cfg.n_cands).astype(np.int32)
+    lens[0] = cfg.cand_len
+    lens[-1] = 1
+    ids = wl.cand_ids.copy()
+    for m in range(cfg.n_cands):
+        ids[m, lens[m]:] = 0
+    return ids, lens
+
+
+def _case(cfg, seed):
+    _torch()
+    _say(f"case: {cfg.name} seed {seed}")
+    wl = W.make_workload(cfg, seed, device="cuda")
+    return wl, *_prompts(wl, seed)
+
+
+def make_verifier(wl, max_new, split_layers=None, prefill=True):
+    torch = _torch()
+    from paper_2601_01513_amd.binding import Verifier
+    cfg = wl.cfg
+    v = Verifier(cfg, wl.weights, device="cuda", split_layers=split_layers, max_new=max_new)
+    if prefill:
+        ids = torch.tensor(wl.prefix_ids, dtype=torch.int32, device="cuda") if cfg.n_text else None
+        v.prefill(wl.visual if cfg.n_visual else None, ids)
+    return v
+
+
+def run_draft(v, ids, lens, n_new):
+    torch = _torch()
+    out = v.draft(torch.tensor(ids, dtype=torch.int32, device="cuda"), lens, n_new)
+    torch.cuda.synchronize()
+    return out.cpu().numpy().astype(np.int64)
+
+
+def run_oracle(wl, ids, lens, toks, dtype=np.float64, branches=None):
+    hw = W.host_weights(wl.weights, lazy=True)
+    vis = W.to_host_f32(wl.visual)
+    t0 = time.time()
+    every = max(1, wl.cfg.n_layers // 7)
+
+    def progress(layer):
+        if (layer + 1) % every == 0:
+            _say(f"  oracle layer {layer + 1}/{wl.cfg.n_layers} at {time.time() - t0:.0f}s")
+    return D.teacher_forced_shared(wl.cfg, hw, vis, wl.prefix_ids, ids, lens, toks, dtype=dtype,
+                                   branches=branches, progress=progress)
+
+
+def check_draft(cfg, toks, ora, branches=None):
+    got, top, arg, gap = ora
+    tol = 1e-4 if cfg.dtype == W.F32 else 2e-2
+    rows = list(range(toks.shape[0])) if branches is None else list(branches)
+    assert np.all((toks >= 0) & (toks < cfg.vocab))
+    g, t, a, gp, tk = got[rows], top[rows], arg[rows], gap[rows], toks[rows]
+    short = t - g
+    clear = gp > 2 * tol
+    _say(f"  max (top - got) = {short.max():.3e} (bound {2 * tol}), clear steps "
+         f"{int(clear.sum())}/{clear.size}, equal to oracle argmax {int((tk == a).sum())}")
+    assert np.all(short <= 2 * tol)
+    np.testing.assert_array_equal(tk[clear], a[clear])
+
+
+def check_against_decode(wl, ids, lens, toks, n_new):
+    """Where every step of the oracle's own greedy path is clear, the tokens
+    are that path."""
+    hw = W.host_weights(wl.weights, lazy=True)
+    ref = D.decode_shared(wl.cfg, hw, W.to_host_f32(wl.visual), wl.prefix_ids, ids, lens, n_new)
+    same = (ref == toks).all(axis=1)
+    _say(f"  branches equal to the oracle's greedy decode: {int(same.sum())}/{len(same)}")
+    return ref, same
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_draft_tiny_fp32(seed):
+    wl, ids, lens = _case(W.TINY_F32, seed)
+    v = make_verifier(wl, max_new=8)
+    toks = run_draft(v, ids, lens, 6)
+    ora = run_oracle(wl, ids, lens, toks)
+    check_draft(wl.cfg, toks, ora)
+    ref, same = check_against_decode(wl, ids, lens, toks, 6)
+    _, _, _, gap_ref = D.teacher_forced(wl.cfg, W.host_weights(wl.weights, lazy=True),
+                                        W.to_host_f32(wl.visual), wl.prefix_ids, ids, lens, ref)
+    for m in range(len(same)):
+        if np.all(gap_ref[m] > 2e-4):
+            assert same[m], m
+
+
+@pytest.mark.parametrize("seed,split", [(0, 0), (1, 1), (2, 2)])
+def test_draft_small_bf16(seed, split):
+    wl, ids, lens = _case(SMALL_BF16, seed)
+    v = make_verifier(wl, max_new=12, split_layers=split)
+    toks = run_draft(v, ids, lens, 12)
+    check_draft(wl.cfg, toks, run_oracle(wl, ids, lens, toks))
+
+
+@pytest.mark.parametrize("seed,split", [(0, 0), (1, 1)])
+def test_draft_gqa7_eight_branches(seed, split):
+    """Seven query heads per KV head: decode-step query tiles hold rows of
+    several branches, each masked to its own cache segment."""
+    wl, ids, lens = _case(GQA7_BF16, seed)
+    v = make_verifier(wl, max_new=20, split_layers=split)
+    toks = run_draft(v, ids, lens, 17)
+    check_draft(wl.cfg, toks, run_oracle(wl, ids, lens, toks))
+
+
+def test_draft_is_repeatable_and_leaves_scoring_alone():
+    """A second draft overwrites the draft cache and gives the same tokens;
+    scoring before and after a draft gives the same log-probs (separate
+    buffers); smaller draft calls after a larger one are unaffected by it."""
+    torch = _torch()
+    wl, ids, lens = _case(SMALL_BF16, 3)
+    v = make_verifier(wl, max_new=10, split_layers=1)
+    cids = torch.tensor(wl.cand_ids, dtype=torch.int32, device="cuda")
+    lp0 = v.score(cids, wl.cand_len)[0].cpu().numpy()
+    a = run_draft(v, ids, lens, 10)
+    lp1 = v.score(cids, wl.cand_len)[0].cpu().numpy()
+    b = run_draft(v, ids, lens, 10)
+    np.testing.assert_array_equal(a, b)
+    np.testing.assert_array_equal(lp0, lp1)
+    # Fewer branches and steps after a larger call, and one branch alone.
+    for sub, n in ((slice(0, 2), 3), (slice(3, 4), 10)):
+        c = run_draft(v, ids[sub], lens[sub], n)
+        check_draft(wl.cfg, c, run_oracle(wl, ids[sub], lens[sub], c))
+
+
+def test_draft_errors():
+    torch = _torch()
+    from paper_2601_01513_amd.binding import VSR_EINVAL, VSR_ERANGE, VSR_ESTATE, VsrError
+    wl, ids, lens = _case(W.TINY_F32, 4)
+    dev = torch.tensor(ids, dtype=torch.int32, device="cuda")
+    v = make_verifier(wl, max_new=4, prefill=False)
+    with pytest.raises(VsrError) as e:
+        v.draft(dev, lens, 2)
+    assert e.value.code == VSR_ESTATE
+    v = make_verifier(wl, max_new=0)
+    with pytest.raises(VsrError) as e:
+        v.draft(dev, lens, 2)
+    assert e.value.code == VSR_ESTATE
+    v = make_verifier(wl, max_new=4)
+    for bad_lens, n_new, code in ((lens, 5, VSR_ERANGE), (lens, 0, VSR_ERANGE),
+                                  (np.where(np.arange(len(lens)) == 1, 0, lens), 2, VSR_EINVAL),
+                                  (np.where(np.arange(len(lens)) == 1, ids.shape[1] + 1, lens),
+                                   2, VSR_EINVAL)):
+        with pytest.raises(VsrError) as e:
+            v.draft(dev, bad_lens, n_new)
+        assert e.value.code == code, (bad_lens, n_new)
+    # the context still works after rejected calls
+    toks = run_draft(v, ids, lens, 4)
+    check_draft(wl.cfg, toks, run_oracle(wl, ids, lens, toks))
+
+
+@pytest.mark.timeout(900)
+def test_draft_full_1p5b_sampled():
+    """The 1.5B-class model as the drafter at its full prefix: four branches
+    of up to 64 prompt tokens, 32 new tokens each; the oracle (float32)
+    teacher-forces two of them."""
+    wl, ids, lens = _case(W.B1_5, 0)
+    v = make_verifier(wl, max_new=32)
+    t0 = time.time()
+    toks = run_draft(v, ids, lens, 32)
+    _say(f"  gpu done in {time.time() - t0:.1f}s")
+    branches = [0, len(lens) - 1]
+    ora = run_oracle(wl, ids, lens, toks, dtype=np.float32, branches=branches)
+    check_draft(wl.cfg, toks, ora, branches)
+
+
+@pytest.mark.timeout(900)
+def test_draft_full_width_7b_two_layers():
+    """Full 7B widths and prefix, eight branches, two layers (one precise)."""
+    cfg = W.B7.replace(name=W.B7.name + " (2 layers)", n_layers=2)
+    wl, ids, lens = _case(cfg, 1)
+    v = make_verifier(wl, max_new=8, split_layers=1)
+    toks = run_draft(v, ids, lens, 8)
+    check_draft(cfg, toks, run_oracle(wl, ids, lens, toks, dtype=np.float32))

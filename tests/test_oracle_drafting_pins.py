@@ -85,6 +85,20 @@ def test_teacher_forced_report_is_consistent():
     assert got2[0, 1] < top2[0, 1]
 
 
+def test_shared_teacher_forcing_equals_per_branch_sequences():
+    w, vis, pre, ids, lens = _prompt(8, lens=(3, 6, 1))
+    toks = D.decode_bruteforce(PIN, w, vis, pre, ids, lens, 4)
+    toks[1, 2] = (toks[1, 2] + 5) % PIN.vocab       # not the greedy path: still reported
+    full = D.teacher_forced(PIN, w, vis, pre, ids, lens, toks)
+    shared = D.teacher_forced_shared(PIN, w, vis, pre, ids, lens, toks)
+    for a, b in zip(full, shared):
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-10)
+    part = D.teacher_forced_shared(PIN, w, vis, pre, ids, lens, toks, branches=[2])
+    np.testing.assert_allclose(part[1][2], full[1][2], rtol=0, atol=1e-10)
+    assert np.all(np.isnan(part[1][:2])) and np.all(part[2][:2] == -1)
+    assert full[0][1, 2] < full[1][1, 2]
+
+
 def test_no_layers_closed_form():
     cfg = PIN.replace(n_layers=0)
     w, vis, pre, ids, lens = sharp_inputs(cfg, 5, lens=[2, 3, 1])
