@@ -211,8 +211,7 @@ struct AttnArgs {
   int t0;               // first query token
   int P;                // mode 1: prefix length
   int n_heads, n_kv;
-  int nchunks;          // mode 1: prefix split (partials when > 1)
-  int chunk;            // prefix keys per split
+  int nchunks;          // mode 1: key split of each block (partials when > 1)
   f16 *out;             // [T][out_split][n_heads][hd] when nchunks == 1 (or merged)
   int out_split;        // 2: [hi | lo] rows for a split output projection
   float *part_acc;      // [nchunks][n_kv][T*G][hd]

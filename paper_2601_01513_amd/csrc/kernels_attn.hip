@@ -22,9 +22,9 @@
 // exponent, exp2(s * c - m * c) with c = log2(e) / sqrt(hd), one FMA per
 // score; operands (queries, keys, values, probabilities) are fp16.
 //
-// The candidate pass may split the prefix keys into chunks (more blocks on the
-// chip); each chunk writes (max, sum, unnormalised output) partials and
-// attn_merge combines them.
+// The candidate pass may split a block's keys (its prefix tiles, then its
+// branch tiles) into chunks (more blocks on the chip); each chunk writes (max,
+// sum, unnormalised output) partials and attn_merge combines them.
 //
 // Precise variant (the leading layers of a deep model, where rounding is
 // amplified most): queries, keys and values arrive as fp16 value + fp16
@@ -230,8 +230,8 @@ __device__ __forceinline__ void walk_segment(const Seg &sg, u32x4 *lds, Lane &L,
 }
 
 // mode 0: prefill (causal over the prefix cache, one chunk, direct output);
-// mode 1: candidate pass (prefix chunk blockIdx.z; the last chunk also walks
-//         the candidate's own keys).
+// mode 1: candidate pass (chunk blockIdx.z of the block's prefix + branch
+//         key tiles).
 template <int MODE, bool PREC>
 __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
   constexpr int QT = Shape<PREC>::QT;
@@ -290,20 +290,26 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
            tok_first};
     walk_segment<PREC>(sg, lds, L, scale_log2);
   } else {
-    const int kb = chunk * a.chunk, ke = min(a.P, kb + a.chunk);
+    // The block's key tiles: the prefix tiles, then the branch tiles from its
+    // first query's segment start to its last query's position (both
+    // non-decreasing in token order; in a decode step one tile holds rows of
+    // several branches, whose segments lie between those bounds). Chunk z of
+    // nchunks walks an even share of them.
+    const int pre_t = (a.P + KT - 1) / KT;
+    const int lo = a.row_lo[tok_first] & ~(KT - 1);
+    const int hi = a.q_pos ? a.q_pos[tok_last] : tok_last;
+    const int tot = pre_t + (hi - lo) / KT + 1;
+    const int c0 = (int)((long)tot * chunk / a.nchunks);
+    const int c1 = (int)((long)tot * (chunk + 1) / a.nchunks);
     Seg sp{a.k + koff, a.vt + koff, PREC ? a.k_lo + koff : nullptr,
-           PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.P, kb, ke, SEG_ALL, tok_first};
+           PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.P, min(c0, pre_t) * KT,
+           min(a.P, min(c1, pre_t) * KT), SEG_ALL, tok_first};
     walk_segment<PREC>(sp, lds, L, scale_log2);
-    if (chunk == a.nchunks - 1) {
-      // Branch keys from the block's first query's segment start to its last
-      // query's position (both non-decreasing in token order).
-      const int lo = a.row_lo[tok_first] & ~(KT - 1);
-      const int hi = a.q_pos ? a.q_pos[tok_last] : tok_last;
-      Seg sb{a.bk + boff, a.bvt + boff, PREC ? a.bk_lo + boff : nullptr,
-             PREC ? a.bvt_lo + boff : nullptr, a.bk_npos, a.bk_valid ? a.bk_valid : a.T, lo,
-             hi + 1, SEG_BRANCH, tok_first};
-      walk_segment<PREC>(sb, lds, L, scale_log2);
-    }
+    Seg sb{a.bk + boff, a.bvt + boff, PREC ? a.bk_lo + boff : nullptr,
+           PREC ? a.bvt_lo + boff : nullptr, a.bk_npos, a.bk_valid ? a.bk_valid : a.T,
+           lo + (max(c0, pre_t) - pre_t) * KT, min(hi + 1, lo + (max(c1, pre_t) - pre_t) * KT),
+           SEG_BRANCH, tok_first};
+    walk_segment<PREC>(sb, lds, L, scale_log2);
   }
 
   if (row >= TG) return;

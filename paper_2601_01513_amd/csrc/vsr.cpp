@@ -24,21 +24,18 @@ thread_local std::string g_create_error;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Prefix split of the candidate pass: enough blocks to cover the chip, chunks
-// of at least 256 keys, a multiple of the 64-key tile.
+// Key split of the candidate pass: enough blocks to cover the chip, at least
+// 256 of a block's `keys` (prefix + branch keys it walks) per chunk.
 struct Split {
-  int nchunks, chunk;
+  int nchunks;
 };
-Split cascade_split(int T, int P, int n_heads, int n_kv) {
+Split cascade_split(int T, int keys, int n_heads, int n_kv) {
   const int G = n_heads / n_kv;
   const int qt = attn_query_tile();
   const int qtiles = (T * G + qt - 1) / qt * n_kv;
   int n = std::max(1, (512 + qtiles - 1) / qtiles);
-  n = std::min(n, std::max(1, P / 256));
-  n = std::min(n, 32);
-  int chunk = (int)align_up((size_t)((P + n - 1) / n), 64);
-  n = (P + chunk - 1) / chunk;
-  return {n, chunk};
+  n = std::min(n, std::max(1, keys / 256));
+  return {std::min(n, 32)};
 }
 
 struct Plan {
@@ -95,11 +92,14 @@ Plan make_plan(const vsr_config &c) {
   p.dec_npos = c.max_new > 0 ? (int)align_up((size_t)c.max_cands * p.dec_S, 64) : 0;
   p.rope_npos = p.kv_npos + c.max_cand_len + c.max_new;
   p.lm_chunks = c.dtype == VSR_BF16 ? lmhead_chunks(c.vocab) : 1;
-  // Largest partial-row count of the cascade split over every T <= max_t.
+  // Largest partial-row count of the cascade split over every T <= max_t
+  // (the split grows with the keys a block walks, at most the whole prefix
+  // plus the largest branch span: a candidate, or every draft branch).
   size_t part_rows = 0;
   if (c.dtype == VSR_BF16) {
+    const int keys_max = c.max_prefix + std::max(c.max_cand_len, p.dec_npos);
     for (int T = 1; T <= p.max_t; ++T) {
-      const Split s = cascade_split(T, c.max_prefix, c.n_heads, c.n_kv_heads);
+      const Split s = cascade_split(T, keys_max, c.n_heads, c.n_kv_heads);
       if (s.nchunks > 1) part_rows = std::max(part_rows, (size_t)s.nchunks * T * G);
     }
   }
@@ -437,7 +437,6 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       a.n_heads = Hq;
       a.n_kv = Hkv;
       a.nchunks = split.nchunks;
-      a.chunk = split.chunk;
       a.out = attn;
       a.out_split = sp;
       a.part_acc = c->at<float>(p.part_acc);
@@ -512,7 +511,7 @@ int prefill_impl(vsr_ctx *c, const void *visual, int nv, const int32_t *ids, int
                                    static_cast<const TW *>(c->embed), cf.vocab, cf.d_model, x,
                                    c->stream));
   c->P = P;
-  const int rc = run_layers<TW, TA>(c, P, 0, Split{1, 0});
+  const int rc = run_layers<TW, TA>(c, P, 0, Split{1});
   if (rc) return rc;
   STAGE(c, K_COPY, "last prefix row",
            hipMemcpyAsync(c->at<float>(p.h_last), x + (size_t)(P - 1) * cf.d_model,
@@ -538,7 +537,7 @@ int branch_forward(vsr_ctx *c, const Branches &br, const int32_t *cand_ids) {
         launch_embed_rows<TW>(lm_tgt, T_rows, static_cast<const TW *>(c->embed), cf.d_model,
                               c->at<float>(p.x), s));
   const Split split =
-      kMfma ? cascade_split(T_rows, c->P, cf.n_heads, cf.n_kv_heads) : Split{1, 0};
+      kMfma ? cascade_split(T_rows, c->P + br.cmax, cf.n_heads, cf.n_kv_heads) : Split{1};
   return run_layers<TW, TA>(c, T_rows, 1, split);
 }
 
@@ -654,15 +653,18 @@ int draft_impl(vsr_ctx *c, const Branches &br, const int32_t *ids, int n_new, in
   STAGE(c, K_EMBED, "draft embedding",
         launch_embed_rows<TW>(lm_tgt, T_rows, static_cast<const TW *>(c->embed), cf.d_model,
                               x, s));
+  // A prompt-pass block spans about one branch; a decode-step block spans
+  // the cache segments of all of them.
   const Split split0 =
-      kMfma ? cascade_split(T_rows, c->P, cf.n_heads, cf.n_kv_heads) : Split{1, 0};
+      kMfma ? cascade_split(T_rows, c->P + p.dec_S, cf.n_heads, cf.n_kv_heads) : Split{1};
   int rc = run_layers<TW, TA>(c, T_rows, 2, split0);
   if (rc) return rc;
   STAGE(c, K_LMIN, "draft inputs",
         launch_branch_last_norm<TW, TA>(x, br, g, cf.d_model, cf.rms_eps, lm_in, s));
   rc = pick(0);
   if (rc) return rc;
-  const Split split1 = kMfma ? cascade_split(M, c->P, cf.n_heads, cf.n_kv_heads) : Split{1, 0};
+  const Split split1 =
+      kMfma ? cascade_split(M, c->P + M * p.dec_S, cf.n_heads, cf.n_kv_heads) : Split{1};
   for (int step = 1; step < n_new; ++step) {
     STAGE(c, K_ROWS, "draft step rows",
           launch_draft_step(br, c->P, p.dec_S, step, row_lo, row_pos, cache_row, s));
