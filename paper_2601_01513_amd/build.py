@@ -19,7 +19,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libvsr.so")
 
 SOURCES = ["vsr.cpp", "kernels_misc.hip", "kernels_simple.hip", "kernels_gemm.hip",
-           "kernels_attn.hip", "kernels_retrieval.hip"]
+           "kernels_attn.hip", "kernels_retrieval.hip", "kernels_skinny.hip"]
 
 # -packed-fp32-ops: keep hipcc from emitting packed fp32 VALU instructions.
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-x", "hip",

@@ -160,6 +160,57 @@ struct QKVOut {
   const int32_t *cache_row = nullptr;
 };
 
+// Stores one rotate-half pair (dims d and d + 64 of head slot `slot` of the
+// stacked q | k | v projection) of row `row`: rotary on q and k at the row's
+// position, then q to its rows, k to the key cache and v to the Vt cache (at
+// the attention kernel's interleaved position), each with its fp16 remainder
+// where the remainder planes are given. head_dim 128.
+__device__ __forceinline__ void qkv_store(const QKVOut<f16> &o, int n_heads, int n_kv, int slot,
+                                          int row, int d, float x1, float x2) {
+  if (slot < n_heads + n_kv) {
+    const int pos = o.row_pos ? o.row_pos[row] : row;
+    const float2 cs = o.rope[(long)pos * 64 + d];
+    const float y1 = x1 * cs.x - x2 * cs.y, y2 = x2 * cs.x + x1 * cs.y;
+    x1 = y1;
+    x2 = y2;
+  }
+  const f16 h1 = static_cast<f16>(x1), h2 = static_cast<f16>(x2);
+  const f16 l1 = static_cast<f16>(x1 - static_cast<float>(h1));
+  const f16 l2 = static_cast<f16>(x2 - static_cast<float>(h2));
+  if (slot < n_heads) {
+    const long off = ((long)row * n_heads + slot) * 128;
+    o.q[off + d] = h1;
+    o.q[off + d + 64] = h2;
+    if (o.q_lo) {
+      o.q_lo[off + d] = l1;
+      o.q_lo[off + d + 64] = l2;
+    }
+  } else if (slot < n_heads + n_kv) {
+    const int crow = o.cache_row ? o.cache_row[row] : row;
+    const long off = ((long)(slot - n_heads) * o.kv_npos + crow) * 128;
+    o.k[off + d] = h1;
+    o.k[off + d + 64] = h2;
+    if (o.k_lo) {
+      o.k_lo[off + d] = l1;
+      o.k_lo[off + d + 64] = l2;
+    }
+  } else {
+    // Values go to the Vt cache at the attention kernel's interleaved
+    // position: within each aligned group of 16, quarters 1 and 2 swap.
+    const long base = (long)(slot - n_heads - n_kv) * 128 * o.kv_npos;
+    const int crow = o.cache_row ? o.cache_row[row] : row;
+    const int pp = (crow & ~12) | ((crow & 4) << 1) | ((crow & 8) >> 1);
+    const long o1 = base + (long)d * o.kv_npos + pp, o2 = base + (long)(d + 64) * o.kv_npos + pp;
+    o.vt[o1] = h1;
+    o.vt[o2] = h2;
+    if (o.vt_lo) {
+      o.vt_lo[o1] = l1;
+      o.vt_lo[o2] = l2;
+    }
+  }
+}
+
+
 // ------------------------------------------------------------ MFMA path
 // C = A[rows][K] . W[N][K]^T with fused epilogues; A fp16 activations, W
 // 16-bit weights: bf16 (w_f16 = false: converted to fp16 on their way into
@@ -187,6 +238,30 @@ int lmhead_chunks(int vocab);
 // its vocabulary index as int bits; the lowest index on ties).
 hipError_t gemm_lmargmax(const f16 *A, const void *W, bool w_f16, int rows, int vocab, int K,
                          float2 *part, hipStream_t s);
+// Few-row products (rows <= kSkinnyMaxRows; N a multiple of 64, K of 32): the
+// same operands and epilogues as the GEMMs above, computed as a weight stream
+// (K split over up to kSkinnyMaxSplit slices, fp32 partials of
+// skinny_part_floats(rows, N, K) floats in `part`, summed in slice order).
+// skinny_residual also writes the RMSNorm (gain g, NULL: none) of the updated
+// rows to y, [hi | lo] when ysplit == 2.
+constexpr int kSkinnyMaxRows = 32;
+constexpr int kSkinnyMaxSplit = 16;
+int skinny_split(int N, int K);
+size_t skinny_part_floats(int rows, int N, int K);
+hipError_t skinny_residual(const f16 *A, int rows, int asplit, const void *W, bool w_f16, int N,
+                           int K, float *x, const bf16 *g, float eps, f16 *y, int ysplit,
+                           float *part, hipStream_t s);
+hipError_t skinny_swiglu(const f16 *A, int rows, int asplit, const void *W, bool w_f16, int F,
+                         int K, f16 *h, float *part, hipStream_t s);
+hipError_t skinny_qkv_rope(const f16 *A, int rows, int asplit, const void *W, bool w_f16, int K,
+                           int n_heads, int n_kv, const QKVOut<f16> &out, float *part,
+                           hipStream_t s);
+// Greedy LM head of few rows: part[c][t] = (largest logit among vocabulary
+// entries 64c .. 64c+63 for row t, its lowest index as int bits), c <
+// skinny_lm_chunks(vocab) (0: vocab not a multiple of 64, not supported).
+int skinny_lm_chunks(int vocab);
+hipError_t skinny_lmargmax(const f16 *A, int rows, const void *W, bool w_f16, int vocab, int K,
+                           float2 *part, hipStream_t s);
 // dst[i] = fp16 of the bf16 src[i], the GEMMs' in-register conversion.
 hipError_t convert_bf16_to_f16(const uint16_t *src, uint16_t *dst, size_t n, hipStream_t s);
 hipError_t gemm_lmhead(const f16 *A, const void *W, bool w_f16, int rows, int vocab, int K,

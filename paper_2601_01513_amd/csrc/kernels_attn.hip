@@ -349,23 +349,45 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
   }
 }
 
-// One wave per (token, query head): combine the chunk partials.
-__global__ __launch_bounds__(64) void k_attn_merge(AttnArgs a) {
-  const int t = blockIdx.x, head = blockIdx.y, lane = threadIdx.x;
+// Block per (token, query head): combine the chunk partials (nchunks <= 64).
+// Lane c of every wave reads chunk c's (max, sum); wave w sums the outputs of
+// chunks w, w + 4, ... (all its loads in flight at once), then wave 0 adds
+// the four partial sums in order.
+__global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a) {
+  __shared__ float po[4][HD];
+  const int t = blockIdx.x, head = blockIdx.y;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int G = a.n_heads / a.n_kv, TG = a.T * G;
   const int kvh = head / G, row = t * G + head % G;
-  float M = -INFINITY;
-  for (int c = 0; c < a.nchunks; ++c)
-    M = fmaxf(M, a.part_ml[((long)c * a.n_kv + kvh) * TG + row].x);
-  float Lsum = 0.f, o0 = 0.f, o1 = 0.f;
-  for (int c = 0; c < a.nchunks; ++c) {
-    const long prow = ((long)c * a.n_kv + kvh) * TG + row;
-    const float2 ml = a.part_ml[prow];
-    const float wgt = ml.x == -INFINITY ? 0.f : exp2f(ml.x - M);
-    Lsum += ml.y * wgt;
-    o0 += a.part_acc[prow * HD + lane] * wgt;
-    o1 += a.part_acc[prow * HD + 64 + lane] * wgt;
+  const long r0 = (long)kvh * TG + row, cstride = (long)a.n_kv * TG;
+  const float2 ml = lane < a.nchunks ? a.part_ml[lane * cstride + r0]
+                                     : make_float2(-INFINITY, 0.f);
+  const float M = wave_max(ml.x);
+  const float wl = ml.x == -INFINITY ? 0.f : exp2f(ml.x - M);
+  const float Lsum = wave_sum(ml.y * wl);
+  float v0[16], v1[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const long prow = min(w + 4 * i, a.nchunks - 1) * cstride + r0;
+    v0[i] = a.part_acc[prow * HD + lane];
+    v1[i] = a.part_acc[prow * HD + 64 + lane];
   }
+  float o0 = 0.f, o1 = 0.f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int c = w + 4 * i;
+    const float wgt = __shfl(wl, min(c, 63), 64);
+    if (c < a.nchunks) {
+      o0 += v0[i] * wgt;
+      o1 += v1[i] * wgt;
+    }
+  }
+  po[w][lane] = o0;
+  po[w][64 + lane] = o1;
+  __syncthreads();
+  if (w) return;
+  o0 = ((po[0][lane] + po[1][lane]) + po[2][lane]) + po[3][lane];
+  o1 = ((po[0][64 + lane] + po[1][64 + lane]) + po[2][64 + lane]) + po[3][64 + lane];
   const float inv = 1.f / Lsum;
   f16 *op = a.out + ((long)t * a.out_split * a.n_heads + head) * HD;
   const float x0 = o0 * inv, x1 = o1 * inv;
@@ -407,7 +429,8 @@ hipError_t attn_cascade(const AttnArgs &a, bool precise, hipStream_t s) {
 
 hipError_t attn_merge(const AttnArgs &a, hipStream_t s) {
   if (a.T == 0 || a.nchunks == 1) return hipSuccess;
-  k_attn_merge<<<dim3(a.T, a.n_heads), 64, 0, s>>>(a);
+  if (a.nchunks > 64) return hipErrorInvalidValue;
+  k_attn_merge<<<dim3(a.T, a.n_heads), 256, 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -467,51 +467,6 @@ __global__ __launch_bounds__(256) void k_reduce_swiglu(const float *__restrict__
 // Column tile = two heads of the stacked q|k|v projection; wave column wn owns
 // head slot 2 tn + wn. MFMA blocks fn and fn+2 hold head dims d and d + 64,
 // the rotate-half pair.
-__device__ __forceinline__ void qkv_store(const QKVOut<f16> &o, int n_heads, int n_kv, int slot,
-                                          int row, int d, float x1, float x2) {
-  if (slot < n_heads + n_kv) {
-    const int pos = o.row_pos ? o.row_pos[row] : row;
-    const float2 cs = o.rope[(long)pos * 64 + d];
-    const float y1 = x1 * cs.x - x2 * cs.y, y2 = x2 * cs.x + x1 * cs.y;
-    x1 = y1;
-    x2 = y2;
-  }
-  const f16 h1 = static_cast<f16>(x1), h2 = static_cast<f16>(x2);
-  const f16 l1 = static_cast<f16>(x1 - static_cast<float>(h1));
-  const f16 l2 = static_cast<f16>(x2 - static_cast<float>(h2));
-  if (slot < n_heads) {
-    const long off = ((long)row * n_heads + slot) * 128;
-    o.q[off + d] = h1;
-    o.q[off + d + 64] = h2;
-    if (o.q_lo) {
-      o.q_lo[off + d] = l1;
-      o.q_lo[off + d + 64] = l2;
-    }
-  } else if (slot < n_heads + n_kv) {
-    const int crow = o.cache_row ? o.cache_row[row] : row;
-    const long off = ((long)(slot - n_heads) * o.kv_npos + crow) * 128;
-    o.k[off + d] = h1;
-    o.k[off + d + 64] = h2;
-    if (o.k_lo) {
-      o.k_lo[off + d] = l1;
-      o.k_lo[off + d + 64] = l2;
-    }
-  } else {
-    // Values go to the Vt cache at the attention kernel's interleaved
-    // position: within each aligned group of 16, quarters 1 and 2 swap.
-    const long base = (long)(slot - n_heads - n_kv) * 128 * o.kv_npos;
-    const int crow = o.cache_row ? o.cache_row[row] : row;
-    const int pp = (crow & ~12) | ((crow & 4) << 1) | ((crow & 8) >> 1);
-    const long o1 = base + (long)d * o.kv_npos + pp, o2 = base + (long)(d + 64) * o.kv_npos + pp;
-    o.vt[o1] = h1;
-    o.vt[o2] = h2;
-    if (o.vt_lo) {
-      o.vt_lo[o1] = l1;
-      o.vt_lo[o2] = l2;
-    }
-  }
-}
-
 template <class TL, bool WCVT>
 __global__ __launch_bounds__(NT) void k_gemm_qkv(const f16 *__restrict__ A,
                                                  const uint16_t *__restrict__ W, int rows,

@@ -107,26 +107,45 @@ hipError_t launch_draft_step(const Branches &br, int P, int S, int step, int32_t
 
 // Greedy pick per row from the LM-head partials (chunks in vocabulary order,
 // each holding its lowest best index): tokens[m][step] and the next inputs.
-__global__ void k_argmax_merge(const float2 *part, int nchunks, int M, int n_new, int step,
-                               int32_t *tokens, int32_t *next_ids) {
-  const int m = blockIdx.x * blockDim.x + threadIdx.x;
-  if (m >= M) return;
-  float best = part[m].x;
-  int bi = __float_as_int(part[m].y);
-  for (int c = 1; c < nchunks; ++c) {
-    const float2 p = part[(long)c * M + m];
-    if (p.x > best) {
-      best = p.x;
-      bi = __float_as_int(p.y);
-    }
+// Block per row: threads stride over the chunks, then waves and blocks keep
+// the largest value and, among equal values, the lowest index.
+__device__ __forceinline__ void keep_best(float &v, int &i, float v2, int i2) {
+  if (i2 >= 0 && (i < 0 || v2 > v || (v2 == v && i2 < i))) {
+    v = v2;
+    i = i2;
   }
-  tokens[(long)m * n_new + step] = bi;
-  next_ids[m] = bi;
+}
+
+__global__ __launch_bounds__(1024) void k_argmax_merge(const float2 *part, int nchunks, int M,
+                                                       int n_new, int step, int32_t *tokens,
+                                                       int32_t *next_ids) {
+  __shared__ float sv[16];
+  __shared__ int si[16];
+  const int m = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  float best = -INFINITY;
+  int bi = -1;
+  for (int c = threadIdx.x; c < nchunks; c += 1024) {
+    const float2 p = part[(long)c * M + m];
+    keep_best(best, bi, p.x, __float_as_int(p.y));
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1)
+    keep_best(best, bi, __shfl_xor(best, o, 64), __shfl_xor(bi, o, 64));
+  if (lane == 0) {
+    sv[w] = best;
+    si[w] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int i = 1; i < 16; ++i) keep_best(best, bi, sv[i], si[i]);
+    tokens[(long)m * n_new + step] = bi;
+    next_ids[m] = bi;
+  }
 }
 
 hipError_t launch_argmax_merge(const float2 *part, int nchunks, int M, int n_new, int step,
                                int32_t *tokens, int32_t *next_ids, hipStream_t s) {
-  k_argmax_merge<<<(M + 63) / 64, 64, 0, s>>>(part, nchunks, M, n_new, step, tokens, next_ids);
+  k_argmax_merge<<<M, 1024, 0, s>>>(part, nchunks, M, n_new, step, tokens, next_ids);
   return hipGetLastError();
 }
 

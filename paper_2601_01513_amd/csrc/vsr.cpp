@@ -25,7 +25,9 @@ thread_local std::string g_create_error;
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Key split of the candidate pass: enough blocks to cover the chip, at least
-// 256 of a block's `keys` (prefix + branch keys it walks) per chunk.
+// 256 of a block's `keys` (prefix + branch keys it walks) per chunk; a pass
+// with one query tile per KV head (decode steps) is latency-bound and takes
+// chunks of one 64-key tile. At most 64 chunks (the merge's limit).
 struct Split {
   int nchunks;
 };
@@ -34,8 +36,8 @@ Split cascade_split(int T, int keys, int n_heads, int n_kv) {
   const int qt = attn_query_tile();
   const int qtiles = (T * G + qt - 1) / qt * n_kv;
   int n = std::max(1, (512 + qtiles - 1) / qtiles);
-  n = std::min(n, std::max(1, keys / 256));
-  return {std::min(n, 32)};
+  n = std::min(n, std::max(1, keys / (qtiles == n_kv ? 64 : 256)));
+  return {std::min(n, 64)};
 }
 
 struct Plan {
@@ -117,6 +119,12 @@ Plan make_plan(const vsr_config &c) {
                               gemm_split_floats(rows, c.d_model, s * c.d_ff)});
       if (rows == p.rows_max) break;
     }
+    // Few-row products (at most kSkinnyMaxRows rows).
+    const int sr = std::min(p.rows_max, kSkinnyMaxRows);
+    gemm_part = std::max({gemm_part, skinny_part_floats(sr, qkv_n, c.d_model),
+                          skinny_part_floats(sr, c.d_model, c.n_heads * c.head_dim),
+                          skinny_part_floats(sr, 2 * c.d_ff, c.d_model),
+                          skinny_part_floats(sr, c.d_model, c.d_ff)});
   }
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -154,7 +162,13 @@ Plan make_plan(const vsr_config &c) {
   p.vtd_lo = take(nprec * dec_cache);
   p.part_acc = take(part_rows * c.n_kv_heads * hd * 4);
   p.part_ml = take(part_rows * c.n_kv_heads * 8);
-  p.lm_part = take((size_t)p.lm_chunks * p.lm_rows * 8);
+  // LM-head partials: vocabulary tiles x rows, or (greedy drafts of few
+  // branches) 64-entry chunks x branches.
+  p.lm_part = take(std::max((size_t)p.lm_chunks * p.lm_rows,
+                            c.dtype == VSR_BF16 ? (size_t)skinny_lm_chunks(c.vocab) *
+                                                      std::min(c.max_cands, kSkinnyMaxRows)
+                                                : 0) *
+                   8);
   p.tgt = take((size_t)p.lm_rows * 4);
   p.row_lo = take((size_t)p.max_t * 4);
   p.row_pos = take((size_t)p.max_t * 4);
@@ -363,6 +377,10 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
   const bool draft = mode == 2;
   const int32_t *cache_row = draft ? c->at<int32_t>(p.cache_row) : nullptr;
   hipStream_t s = c->stream;
+  // Few-row products stream their weights (skinny kernels); their residual
+  // reduces also apply the RMSNorm that follows (the FFN norm of the layer,
+  // the next layer's attention norm), which then needs no launch of its own.
+  bool xn_ready = false;
   for (int l = 0; l < cf.n_layers; ++l) {
     const TW *wqkv = static_cast<const TW *>(c->wqkv[l]);
     const TW *wo = static_cast<const TW *>(c->wo[l]);
@@ -374,9 +392,11 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
     // remainder.
     const bool precise = kMfma && l < cf.split_layers;
     const int sp = precise ? 2 : 1;
-    STAGE(c, K_NORM, "attention norm",
-             launch_rmsnorm<TW, TA>(x, static_cast<const TW *>(c->attn_norm[l]), rows, d,
-                                    cf.rms_eps, xn, sp, s));
+    if (!xn_ready)
+      STAGE(c, K_NORM, "attention norm",
+            launch_rmsnorm<TW, TA>(x, static_cast<const TW *>(c->attn_norm[l]), rows, d,
+                                   cf.rms_eps, xn, sp, s));
+    xn_ready = false;
     QKVOut<TA> qo;
     qo.q = q;
     qo.rope = c->at<float2>(p.rope);
@@ -408,8 +428,12 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
       qo.vt_lo = mode == 0 ? c->at<TA>(p.vtc_lo) + l * layer_cache : bvt_lo;
     }
     if constexpr (kMfma) {
-      STAGE(c, K_QKV, "qkv projection",
-            gemm_qkv_rope(xn, wqkv, wf16, rows, d, sp, Hq, Hkv, qo, gpart, s));
+      if (rows <= kSkinnyMaxRows)
+        STAGE(c, K_QKV, "qkv projection",
+              skinny_qkv_rope(xn, rows, sp, wqkv, wf16, d, Hq, Hkv, qo, gpart, s));
+      else
+        STAGE(c, K_QKV, "qkv projection",
+              gemm_qkv_rope(xn, wqkv, wf16, rows, d, sp, Hq, Hkv, qo, gpart, s));
     } else {
       STAGE(c, K_QKV, "qkv projection",
             simple_qkv_rope<TA>(xn, wqkv, rows, d, Hq, Hkv, hd, qo, s));
@@ -477,7 +501,25 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
     }
     const TA *attn_r = attn + (size_t)r0 * Hq * hd * sp;
     float *x_r = x + (size_t)r0 * d;
+    const TW *ffn_g = static_cast<const TW *>(c->ffn_norm[l]);
     if constexpr (kMfma) {
+      if (nr <= kSkinnyMaxRows) {
+        // Output projection + residual + FFN norm; gate/up + SwiGLU; down
+        // projection + residual (+ the next layer's attention norm).
+        STAGE(c, K_OPROJ, "output projection",
+              skinny_residual(attn_r, nr, sp, wo, wf16, d, Hq * hd, x_r, ffn_g, cf.rms_eps, xn,
+                              sp, gpart, s));
+        STAGE(c, K_GATEUP, "gate/up projection",
+              skinny_swiglu(xn, nr, sp, wgu, wf16, F, d, h, gpart, s));
+        const bool next = l + 1 < cf.n_layers;
+        const int sp_next = kMfma && l + 1 < cf.split_layers ? 2 : 1;
+        STAGE(c, K_DOWN, "down projection",
+              skinny_residual(h, nr, sp, wdown, wf16, d, F, x_r,
+                              next ? static_cast<const TW *>(c->attn_norm[l + 1]) : nullptr,
+                              cf.rms_eps, xn, sp_next, gpart, s));
+        xn_ready = next;
+        continue;
+      }
       STAGE(c, K_OPROJ, "output projection",
             gemm_residual(attn_r, wo, wf16, nr, d, Hq * hd, sp, x_r, gpart, s));
     } else {
@@ -485,8 +527,7 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
             simple_residual<TA>(attn_r, wo, nr, d, Hq * hd, x_r, s));
     }
     STAGE(c, K_NORM, "ffn norm",
-          launch_rmsnorm<TW, TA>(x_r, static_cast<const TW *>(c->ffn_norm[l]), nr, d,
-                                 cf.rms_eps, xn, sp, s));
+          launch_rmsnorm<TW, TA>(x_r, ffn_g, nr, d, cf.rms_eps, xn, sp, s));
     if constexpr (kMfma) {
       STAGE(c, K_GATEUP, "gate/up projection",
             gemm_swiglu(xn, wgu, wf16, nr, F, d, sp, h, gpart, s));
@@ -633,11 +674,16 @@ int draft_impl(vsr_ctx *c, const Branches &br, const int32_t *ids, int n_new, in
   float2 *part = c->at<float2>(p.lm_part);
   const TW *g = static_cast<const TW *>(c->final_norm);
   const bool wf16 = cf.gemm_weights == VSR_F16;
-  const int chunks = kMfma ? lmhead_chunks(cf.vocab) : 1;
+  const bool skinny_lm = kMfma && M <= kSkinnyMaxRows && skinny_lm_chunks(cf.vocab) > 0;
+  const int chunks = !kMfma ? 1 : skinny_lm ? skinny_lm_chunks(cf.vocab) : lmhead_chunks(cf.vocab);
   auto pick = [&](int step) -> int {
     if constexpr (kMfma) {
-      STAGE(c, K_LMHEAD, "draft lm head",
-            gemm_lmargmax(lm_in, c->lm_head, wf16, M, cf.vocab, cf.d_model, part, s));
+      if (skinny_lm)
+        STAGE(c, K_LMHEAD, "draft lm head",
+              skinny_lmargmax(lm_in, M, c->lm_head, wf16, cf.vocab, cf.d_model, part, s));
+      else
+        STAGE(c, K_LMHEAD, "draft lm head",
+              gemm_lmargmax(lm_in, c->lm_head, wf16, M, cf.vocab, cf.d_model, part, s));
     } else {
       STAGE(c, K_LMHEAD, "draft lm head",
             simple_lmargmax<TA>(lm_in, static_cast<const TW *>(c->lm_head), M, cf.vocab,

@@ -147,9 +147,9 @@ def test_draft_cache_is_sized_by_max_new():
         cache = 2 * cfg.n_layers * cfg.n_kv_heads * npos * cfg.head_dim * 2
         rope = n * cfg.head_dim * 4      # (cos, sin) float pairs of the extra positions
         # attention partials may grow too (a decode block walks every branch's
-        # keys, so the key split may take more chunks), at most to 32 chunks
+        # keys, so the key split may take more chunks), at most to 64 chunks
         T = cfg.n_cands * cfg.cand_len
-        parts = 32 * T * cfg.n_heads * (cfg.head_dim * 4 + 8)
+        parts = 64 * T * cfg.n_heads * (cfg.head_dim * 4 + 8)
         extra = grown - base - cache - rope
         assert 0 <= extra <= parts + 4 * 256, (n, grown - base, cache + rope)
 
