@@ -54,18 +54,20 @@ def stage_flops(cfg, P, lens):
 
     The prefix pass's last layer needs keys/values for every prefix row but
     attention, projections and FFN only for the last row (the one predicting
-    candidate token 0), which is all the library computes there.
+    candidate token 0), which is all the library computes there; those
+    one-row projections run the few-row kernels and are timed as a stage of
+    their own (prefill.tail_proj).
     """
     d, hq, hd, F, V = cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ff, cfg.vocab
     L = cfg.n_layers
     T = int(sum(lens))
     f = {}
-    for ph, rows, rows_tail in (("prefill", P, 1), ("score", T, T)):
-        body = rows * (L - 1) + rows_tail if L else 0
+    for ph, rows, body in (("prefill", P, P * max(L - 1, 0)), ("score", T, T * L)):
         f[f"{ph}.qkv_rope"] = 2.0 * rows * cfg.qkv_rows * d * L
         f[f"{ph}.o_proj"] = 2.0 * body * d * hq * hd
         f[f"{ph}.gate_up_swiglu"] = 2.0 * body * 2 * F * d
         f[f"{ph}.down_proj"] = 2.0 * body * d * F
+    f["prefill.tail_proj"] = 2.0 * (d * hq * hd + 3 * F * d) if L else 0.0
     # QK^T and PV over the visible keys of every query (causal / cascade).
     f["prefill.attention"] = 4.0 * hd * hq * ((P * (P + 1) / 2) * (L - 1) + P) if L else 0.0
     f["score.attention"] = 4.0 * hd * hq * sum(n * P + n * (n + 1) / 2 for n in lens) * L
@@ -243,6 +245,8 @@ def main():
     ap.add_argument("--no-next-rows", action="store_true",
                     help="skip the two-stage verification timings (counter runs)")
     ap.add_argument("--stages", action="store_true", help="print per-stage times to stderr")
+    ap.add_argument("--only-draft", action="store_true",
+                    help="only time the drafter (vsr_draft, 3B-class) and print its figures")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device-to-device (counter calibration) and exit")
     args = ap.parse_args()
@@ -264,6 +268,12 @@ def main():
             torch.mul(src, 1.0, out=dst)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": n, "copies": 3}))
+        return
+
+    if args.only_draft:
+        dev = torch.device("cuda:0")
+        torch.cuda.set_device(dev)
+        print(json.dumps(time_draft(dev, log)), flush=True)
         return
 
     cfg = W.CONFIGS[args.workload]

@@ -286,8 +286,9 @@ void vsr_destroy(vsr_ctx *ctx);
  * kinds: 0 embedding, 1 RMSNorm, 2 QKV projection + rotary + cache write,
  * 3 attention, 4 attention merge, 5 output projection, 6 gate/up + SwiGLU,
  * 7 down projection, 8 LM-head inputs, 9 LM head + chunk LSE,
- * 10 LSE merge + target gather, 11 sum + argmax, 12 row tables, 13 copy. */
-#define VSR_STAGE_KINDS 14
+ * 10 LSE merge + target gather, 11 sum + argmax, 12 row tables, 13 copy,
+ * 14 the prefix pass's last-row layer projections (O, gate/up, down). */
+#define VSR_STAGE_KINDS 15
 #define VSR_STAGES (3 * VSR_STAGE_KINDS)
 
 /* Times the stage kinds whose bits are set in kinds (bit k: kind k, in all

@@ -27,12 +27,12 @@ VSR_SELECT_TWO_STAGE, VSR_SELECT_ADDITION, VSR_SELECT_INVERT = 0, 1, 2
 SELECT_STRATEGIES = {"two_stage": VSR_SELECT_TWO_STAGE, "addition": VSR_SELECT_ADDITION,
                      "invert": VSR_SELECT_INVERT}
 
-VSR_STAGE_KINDS = 14
+VSR_STAGE_KINDS = 15
 VSR_STAGES = 3 * VSR_STAGE_KINDS
 VSR_PROFILE_ALL = (1 << VSR_STAGE_KINDS) - 1
 STAGE_KINDS = ["embed", "rmsnorm", "qkv_rope", "attention", "attn_merge", "o_proj",
                "gate_up_swiglu", "down_proj", "lm_inputs", "lm_head_lse", "lse_gather",
-               "sum_argmax", "row_tables", "copy"]
+               "sum_argmax", "row_tables", "copy", "tail_proj"]
 STAGE_NAMES = ([f"prefill.{k}" for k in STAGE_KINDS] + [f"score.{k}" for k in STAGE_KINDS]
                + [f"draft.{k}" for k in STAGE_KINDS])
 

@@ -79,8 +79,8 @@ struct Seg {
 };
 
 struct Lane {
-  int tok;   // query token of this lane's row
-  int qp;    // SEG_BRANCH: last visible key (the query's own cache position)
+  int tok;   // SEG_CAUSAL: the row's query token (its last visible key);
+             // SEG_BRANCH: its last visible branch key (its own cache position)
   int lo;    // SEG_BRANCH: first visible key
   float m;   // running maximum of the raw (unscaled) scores
   float l;   // running sum of exp2(s * c - m * c)
@@ -94,21 +94,25 @@ struct Lane {
 // rows 4 (i NW + w) .. +3 and V^T rows 8 (i NW + w) .. +7; lane l lands in
 // 16-byte slot l of that 1 KB, i.e. physical chunk l % 16 of K row l / 16, or
 // l % 8 of V^T row l / 8; the global address carries the logical chunk.
+// Addresses are a uniform tile base plus a 32-bit per-lane element offset
+// (d * npos + c < 2^32: cache capacities are below 2^25 positions), which
+// keeps the per-lane part of the addressing small.
 template <int NW>
 __device__ __forceinline__ void load_kv(const f16 *k, const f16 *vt, int npos, int kb,
                                         u32x4 *stage) {
   const int t = threadIdx.x, w = t >> 6, l = t & 63;
+  const f16 *kt = k + (long)kb * HD, *vtt = vt + kb;
 #pragma unroll
   for (int i = 0; i < KCH / (NW * 64); ++i) {
     const int j = i * NW + w, key = j * 4 + (l >> 4), c = (l & 15) ^ (key & 15);
-    __builtin_amdgcn_global_load_lds(k + (long)(kb + key) * HD + c * 8, stage + j * 64, 16, 0,
-                                     0);
+    const unsigned off = (unsigned)(key * HD + c * 8);
+    __builtin_amdgcn_global_load_lds(kt + off, stage + j * 64, 16, 0, 0);
   }
 #pragma unroll
   for (int i = 0; i < VCH / (NW * 64); ++i) {
     const int j = i * NW + w, d = j * 8 + (l >> 3), c = (l & 7) ^ ((d >> 1) & 7);
-    __builtin_amdgcn_global_load_lds(vt + (long)d * npos + kb + c * 8, stage + KCH + j * 64, 16,
-                                     0, 0);
+    const unsigned off = (unsigned)d * (unsigned)npos + (unsigned)(c * 8);
+    __builtin_amdgcn_global_load_lds(vtt + off, stage + KCH + j * 64, 16, 0, 0);
   }
 }
 
@@ -154,7 +158,7 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *st
         const int key = kb + b * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
         bool vis = key < sg.kvalid;
         if (sg.mode == SEG_CAUSAL) vis = vis && key <= L.tok;
-        if (sg.mode == SEG_BRANCH) vis = vis && key >= L.lo && key <= L.qp;
+        if (sg.mode == SEG_BRANCH) vis = vis && key >= L.lo && key <= L.tok;
         s[b][r] = vis ? s[b][r] : -INFINITY;
       }
       mloc = fmaxf(mloc, s[b][r]);
@@ -229,6 +233,36 @@ __device__ __forceinline__ void walk_segment(const Seg &sg, u32x4 *lds, Lane &L,
   }
 }
 
+// Tiles v0 .. v1-1 of the concatenation [prefix tiles 0 .. pre_t-1 | branch
+// tiles from key bbeg on]: one pipeline for both sources (the tile's source
+// is chosen per tile), so that one set of load offsets is live.
+template <bool PREC>
+__device__ __forceinline__ void walk_concat(const Seg &sp, const Seg &sb, int pre_t, int bbeg,
+                                            int v0, int v1, u32x4 *lds, Lane &L,
+                                            float scale_log2) {
+  constexpr int STAGE = Shape<PREC>::STAGE;
+  if (v1 <= v0) return;
+  auto src = [&](int v) -> const Seg & { return v < pre_t ? sp : sb; };
+  auto key0 = [&](int v) { return v < pre_t ? v * KT : bbeg + (v - pre_t) * KT; };
+  load_tile<PREC>(src(v0), key0(v0), lds);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  int stage = 0;
+  for (int v = v0; v < v1; ++v) {
+    u32x4 *cur = lds + stage * STAGE;
+    if (v + 1 < v1) load_tile<PREC>(src(v + 1), key0(v + 1), lds + (stage ^ 1) * STAGE);
+    const Seg &sg = src(v);
+    const int kb = key0(v);
+    if (tile_clear(sg, kb))
+      tile_step<false, PREC>(sg, kb, cur, L, scale_log2);
+    else
+      tile_step<true, PREC>(sg, kb, cur, L, scale_log2);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    stage ^= 1;
+  }
+}
+
 // mode 0: prefill (causal over the prefix cache, one chunk, direct output);
 // mode 1: candidate pass (chunk blockIdx.z of the block's prefix + branch
 //         key tiles).
@@ -247,17 +281,17 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
   const int rowc = min(row, TG - 1);
 
   Lane L;
-  L.tok = a.t0 + rowc / G;
+  const int tok = a.t0 + rowc / G;
   const int head = kvh * G + rowc % G;
-  L.lo = MODE == 1 ? a.row_lo[L.tok] : 0;
-  L.qp = MODE == 1 && a.q_pos ? a.q_pos[L.tok] : L.tok;
+  L.lo = MODE == 1 ? a.row_lo[tok] : 0;
+  L.tok = MODE == 1 && a.q_pos ? a.q_pos[tok] : tok;
   L.m = -INFINITY;
   L.l = 0.f;
 #pragma unroll
   for (int db = 0; db < HD / 32; ++db) L.o[db] = f32x16{};
   if constexpr (PREC) {
     // Queries -> registers: the chunks this lane feeds to the S^T products.
-    const long qoff = ((long)L.tok * a.n_heads + head) * HD + 8 * (lane >> 5);
+    const long qoff = ((long)tok * a.n_heads + head) * HD + 8 * (lane >> 5);
 #pragma unroll
     for (int kk = 0; kk < HD / 16; ++kk) {
       L.qh[kk] = *reinterpret_cast<const f16x8 *>(a.q + qoff + 16 * kk);
@@ -301,22 +335,19 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
     const int tot = pre_t + (hi - lo) / KT + 1;
     const int c0 = (int)((long)tot * chunk / a.nchunks);
     const int c1 = (int)((long)tot * (chunk + 1) / a.nchunks);
-    Seg sp{a.k + koff, a.vt + koff, PREC ? a.k_lo + koff : nullptr,
-           PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.P, min(c0, pre_t) * KT,
-           min(a.P, min(c1, pre_t) * KT), SEG_ALL, tok_first};
-    walk_segment<PREC>(sp, lds, L, scale_log2);
-    Seg sb{a.bk + boff, a.bvt + boff, PREC ? a.bk_lo + boff : nullptr,
-           PREC ? a.bvt_lo + boff : nullptr, a.bk_npos, a.bk_valid ? a.bk_valid : a.T,
-           lo + (max(c0, pre_t) - pre_t) * KT, min(hi + 1, lo + (max(c1, pre_t) - pre_t) * KT),
-           SEG_BRANCH, tok_first};
-    walk_segment<PREC>(sb, lds, L, scale_log2);
+    const Seg sp{a.k + koff, a.vt + koff, PREC ? a.k_lo + koff : nullptr,
+                 PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.P, 0, 0, SEG_ALL, tok_first};
+    const Seg sb{a.bk + boff, a.bvt + boff, PREC ? a.bk_lo + boff : nullptr,
+                 PREC ? a.bvt_lo + boff : nullptr, a.bk_npos, a.bk_valid ? a.bk_valid : a.T,
+                 0, 0, SEG_BRANCH, tok_first};
+    walk_concat<PREC>(sp, sb, pre_t, lo, c0, c1, lds, L, scale_log2);
   }
 
   if (row >= TG) return;
   const int h = lane >> 5;
   if (MODE == 0 || a.nchunks == 1) {
     const float inv = 1.f / L.l;
-    f16 *op = a.out + ((long)L.tok * a.out_split * a.n_heads + head) * HD;
+    f16 *op = a.out + ((long)(a.t0 + rowc / G) * a.out_split * a.n_heads + head) * HD;
     f16 *olo = op + (long)a.n_heads * HD;  // remainder half of a split row
 #pragma unroll
     for (int db = 0; db < HD / 32; ++db)
@@ -349,12 +380,13 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
   }
 }
 
-// Block per (token, query head): combine the chunk partials (nchunks <= 64).
-// Lane c of every wave reads chunk c's (max, sum); wave w sums the outputs of
-// chunks w, w + 4, ... (all its loads in flight at once), then wave 0 adds
-// the four partial sums in order.
-__global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a) {
-  __shared__ float po[4][HD];
+// Block of NW waves per (token, query head): combine the chunk partials
+// (nchunks <= 64). Lane c of every wave reads chunk c's (max, sum); wave w
+// sums the outputs of chunks w, w + NW, ... in order, eight chunks' loads in
+// flight at a time; with NW > 1, wave 0 then adds the waves' sums in order.
+template <int NW>
+__global__ __launch_bounds__(64 * NW) void k_attn_merge(AttnArgs a) {
+  __shared__ float po[NW][HD];
   const int t = blockIdx.x, head = blockIdx.y;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int G = a.n_heads / a.n_kv, TG = a.T * G;
@@ -365,29 +397,38 @@ __global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a) {
   const float M = wave_max(ml.x);
   const float wl = ml.x == -INFINITY ? 0.f : exp2f(ml.x - M);
   const float Lsum = wave_sum(ml.y * wl);
-  float v0[16], v1[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const long prow = min(w + 4 * i, a.nchunks - 1) * cstride + r0;
-    v0[i] = a.part_acc[prow * HD + lane];
-    v1[i] = a.part_acc[prow * HD + 64 + lane];
-  }
   float o0 = 0.f, o1 = 0.f;
+  for (int i0 = 0; w + NW * i0 < a.nchunks; i0 += 8) {
+    float v0[8], v1[8];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int c = w + 4 * i;
-    const float wgt = __shfl(wl, min(c, 63), 64);
-    if (c < a.nchunks) {
-      o0 += v0[i] * wgt;
-      o1 += v1[i] * wgt;
+    for (int j = 0; j < 8; ++j) {
+      const long prow = min(w + NW * (i0 + j), a.nchunks - 1) * cstride + r0;
+      v0[j] = a.part_acc[prow * HD + lane];
+      v1[j] = a.part_acc[prow * HD + 64 + lane];
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int c = w + NW * (i0 + j);
+      const float wgt = __shfl(wl, min(c, 63), 64);
+      if (c < a.nchunks) {
+        o0 += v0[j] * wgt;
+        o1 += v1[j] * wgt;
+      }
     }
   }
-  po[w][lane] = o0;
-  po[w][64 + lane] = o1;
-  __syncthreads();
-  if (w) return;
-  o0 = ((po[0][lane] + po[1][lane]) + po[2][lane]) + po[3][lane];
-  o1 = ((po[0][64 + lane] + po[1][64 + lane]) + po[2][64 + lane]) + po[3][64 + lane];
+  if constexpr (NW > 1) {
+    po[w][lane] = o0;
+    po[w][64 + lane] = o1;
+    __syncthreads();
+    if (w) return;
+    o0 = po[0][lane];
+    o1 = po[0][64 + lane];
+#pragma unroll
+    for (int i = 1; i < NW; ++i) {
+      o0 += po[i][lane];
+      o1 += po[i][64 + lane];
+    }
+  }
   const float inv = 1.f / Lsum;
   f16 *op = a.out + ((long)t * a.out_split * a.n_heads + head) * HD;
   const float x0 = o0 * inv, x1 = o1 * inv;
@@ -430,7 +471,11 @@ hipError_t attn_cascade(const AttnArgs &a, bool precise, hipStream_t s) {
 hipError_t attn_merge(const AttnArgs &a, hipStream_t s) {
   if (a.T == 0 || a.nchunks == 1) return hipSuccess;
   if (a.nchunks > 64) return hipErrorInvalidValue;
-  k_attn_merge<<<dim3(a.T, a.n_heads), 256, 0, s>>>(a);
+  // Many chunks (decode steps: few rows, single-tile chunks): four waves.
+  if (a.nchunks > 16)
+    k_attn_merge<4><<<dim3(a.T, a.n_heads), 256, 0, s>>>(a);
+  else
+    k_attn_merge<1><<<dim3(a.T, a.n_heads), 64, 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -251,9 +251,9 @@ struct vsr_ctx {
 
 enum StageKind {
   K_EMBED = 0, K_NORM, K_QKV, K_ATTN, K_MERGE, K_OPROJ, K_GATEUP, K_DOWN, K_LMIN, K_LMHEAD,
-  K_LSE, K_SELECT, K_ROWS, K_COPY
+  K_LSE, K_SELECT, K_ROWS, K_COPY, K_TAIL
 };
-static_assert(K_COPY + 1 == VSR_STAGE_KINDS, "stage kinds");
+static_assert(K_TAIL + 1 == VSR_STAGE_KINDS, "stage kinds");
 
 // Launch the expression as stage `kind`; with timing on, bracket it with events.
 #define STAGE(ctx, kind, name, ...)                                                     \
@@ -505,15 +505,16 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
     if constexpr (kMfma) {
       if (nr <= kSkinnyMaxRows) {
         // Output projection + residual + FFN norm; gate/up + SwiGLU; down
-        // projection + residual (+ the next layer's attention norm).
-        STAGE(c, K_OPROJ, "output projection",
+        // projection + residual (+ the next layer's attention norm). The
+        // prefix pass's last-row layer is timed as a kind of its own.
+        STAGE(c, tail ? K_TAIL : K_OPROJ, "output projection",
               skinny_residual(attn_r, nr, sp, wo, wf16, d, Hq * hd, x_r, ffn_g, cf.rms_eps, xn,
                               sp, gpart, s));
-        STAGE(c, K_GATEUP, "gate/up projection",
+        STAGE(c, tail ? K_TAIL : K_GATEUP, "gate/up projection",
               skinny_swiglu(xn, nr, sp, wgu, wf16, F, d, h, gpart, s));
         const bool next = l + 1 < cf.n_layers;
         const int sp_next = kMfma && l + 1 < cf.split_layers ? 2 : 1;
-        STAGE(c, K_DOWN, "down projection",
+        STAGE(c, tail ? K_TAIL : K_DOWN, "down projection",
               skinny_residual(h, nr, sp, wdown, wf16, d, F, x_r,
                               next ? static_cast<const TW *>(c->attn_norm[l + 1]) : nullptr,
                               cf.rms_eps, xn, sp_next, gpart, s));
