@@ -326,15 +326,24 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
   } else {
     // The block's key tiles: the prefix tiles, then the branch tiles from its
     // first query's segment start to its last query's position (both
-    // non-decreasing in token order; in a decode step one tile holds rows of
-    // several branches, whose segments lie between those bounds). Chunk z of
-    // nchunks walks an even share of them.
+    // non-decreasing in token order). Candidate pass: chunks of whole prefix
+    // tiles, the last one short and carrying the (few, masked) branch tiles.
+    // Draft pass (cache positions given): one tile may hold rows of several
+    // branches, whose segments lie between those bounds, so the branch tiles
+    // are many and every chunk walks an even share of all tiles.
     const int pre_t = (a.P + KT - 1) / KT;
     const int lo = a.row_lo[tok_first] & ~(KT - 1);
     const int hi = a.q_pos ? a.q_pos[tok_last] : tok_last;
     const int tot = pre_t + (hi - lo) / KT + 1;
-    const int c0 = (int)((long)tot * chunk / a.nchunks);
-    const int c1 = (int)((long)tot * (chunk + 1) / a.nchunks);
+    int c0, c1;
+    if (a.q_pos) {
+      c0 = (int)((long)tot * chunk / a.nchunks);
+      c1 = (int)((long)tot * (chunk + 1) / a.nchunks);
+    } else {
+      const int ct = (pre_t + a.nchunks - 1) / a.nchunks;
+      c0 = min(pre_t, chunk * ct);
+      c1 = chunk == a.nchunks - 1 ? tot : min(pre_t, (chunk + 1) * ct);
+    }
     const Seg sp{a.k + koff, a.vt + koff, PREC ? a.k_lo + koff : nullptr,
                  PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.P, 0, 0, SEG_ALL, tok_first};
     const Seg sb{a.bk + boff, a.bvt + boff, PREC ? a.bk_lo + boff : nullptr,
