@@ -264,8 +264,9 @@ __device__ __forceinline__ void walk_concat(const Seg &sp, const Seg &sb, int pr
 }
 
 // mode 0: prefill (causal over the prefix cache, one chunk, direct output);
-// mode 1: candidate pass (chunk blockIdx.z of the block's prefix + branch
-//         key tiles).
+// mode 1: candidate pass (chunk blockIdx.z of the prefix; the last chunk also
+//         walks the candidates' own keys);
+// mode 2: draft pass (chunk blockIdx.z of the prefix + branch-cache tiles).
 template <int MODE, bool PREC>
 __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
   constexpr int QT = Shape<PREC>::QT;
@@ -283,8 +284,8 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
   Lane L;
   const int tok = a.t0 + rowc / G;
   const int head = kvh * G + rowc % G;
-  L.lo = MODE == 1 ? a.row_lo[tok] : 0;
-  L.tok = MODE == 1 && a.q_pos ? a.q_pos[tok] : tok;
+  L.lo = MODE >= 1 ? a.row_lo[tok] : 0;
+  L.tok = MODE == 2 ? a.q_pos[tok] : tok;
   L.m = -INFINITY;
   L.l = 0.f;
 #pragma unroll
@@ -323,32 +324,40 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
            PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.T, 0, tok_last + 1, SEG_CAUSAL,
            tok_first};
     walk_segment<PREC>(sg, lds, L, scale_log2);
+  } else if (MODE == 1) {
+    // Candidate pass: chunks of whole prefix tiles (the last one short); the
+    // last chunk also walks the branch keys from the block's first query's
+    // segment start to its last query (both non-decreasing in token order).
+    const int pre_t = (a.P + KT - 1) / KT;
+    const int ct = (pre_t + a.nchunks - 1) / a.nchunks;
+    const int kb = min(a.P, chunk * ct * KT), ke = min(a.P, (chunk + 1) * ct * KT);
+    Seg sp{a.k + koff, a.vt + koff, PREC ? a.k_lo + koff : nullptr,
+           PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.P, kb, ke, SEG_ALL, tok_first};
+    walk_segment<PREC>(sp, lds, L, scale_log2);
+    if (chunk == a.nchunks - 1) {
+      const int lo = a.row_lo[tok_first] & ~(KT - 1);
+      Seg sb{a.bk + boff, a.bvt + boff, PREC ? a.bk_lo + boff : nullptr,
+             PREC ? a.bvt_lo + boff : nullptr, a.bk_npos, a.T, lo, tok_last + 1, SEG_BRANCH,
+             tok_first};
+      walk_segment<PREC>(sb, lds, L, scale_log2);
+    }
   } else {
-    // The block's key tiles: the prefix tiles, then the branch tiles from its
-    // first query's segment start to its last query's position (both
-    // non-decreasing in token order). Candidate pass: chunks of whole prefix
-    // tiles, the last one short and carrying the (few, masked) branch tiles.
-    // Draft pass (cache positions given): one tile may hold rows of several
-    // branches, whose segments lie between those bounds, so the branch tiles
-    // are many and every chunk walks an even share of all tiles.
+    // Draft pass (cache positions given): one query tile may hold rows of
+    // several branches, whose cache segments lie between the block's first
+    // query's segment start and its last query's position, so the branch
+    // tiles are many: every chunk walks an even share of [prefix tiles |
+    // branch tiles].
     const int pre_t = (a.P + KT - 1) / KT;
     const int lo = a.row_lo[tok_first] & ~(KT - 1);
-    const int hi = a.q_pos ? a.q_pos[tok_last] : tok_last;
+    const int hi = a.q_pos[tok_last];
     const int tot = pre_t + (hi - lo) / KT + 1;
-    int c0, c1;
-    if (a.q_pos) {
-      c0 = (int)((long)tot * chunk / a.nchunks);
-      c1 = (int)((long)tot * (chunk + 1) / a.nchunks);
-    } else {
-      const int ct = (pre_t + a.nchunks - 1) / a.nchunks;
-      c0 = min(pre_t, chunk * ct);
-      c1 = chunk == a.nchunks - 1 ? tot : min(pre_t, (chunk + 1) * ct);
-    }
+    const int c0 = (int)((long)tot * chunk / a.nchunks);
+    const int c1 = (int)((long)tot * (chunk + 1) / a.nchunks);
     const Seg sp{a.k + koff, a.vt + koff, PREC ? a.k_lo + koff : nullptr,
                  PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.P, 0, 0, SEG_ALL, tok_first};
     const Seg sb{a.bk + boff, a.bvt + boff, PREC ? a.bk_lo + boff : nullptr,
-                 PREC ? a.bvt_lo + boff : nullptr, a.bk_npos, a.bk_valid ? a.bk_valid : a.T,
-                 0, 0, SEG_BRANCH, tok_first};
+                 PREC ? a.bvt_lo + boff : nullptr, a.bk_npos, a.bk_valid, 0, 0, SEG_BRANCH,
+                 tok_first};
     walk_concat<PREC>(sp, sb, pre_t, lo, c0, c1, lds, L, scale_log2);
   }
 
@@ -474,6 +483,10 @@ hipError_t attn_cascade(const AttnArgs &a, bool precise, hipStream_t s) {
   if (a.T == 0 || a.t0 != 0) return a.T == 0 ? hipSuccess : hipErrorInvalidValue;
   if (precise && (!a.q_lo || !a.k_lo || !a.vt_lo || !a.bk_lo || !a.bvt_lo))
     return hipErrorInvalidValue;
+  if (a.q_pos) {  // draft pass
+    if (a.bk_valid <= 0) return hipErrorInvalidValue;
+    return precise ? launch_attn<2, true>(a, s) : launch_attn<2, false>(a, s);
+  }
   return precise ? launch_attn<1, true>(a, s) : launch_attn<1, false>(a, s);
 }
 
