@@ -153,6 +153,18 @@ def test_draft_gqa7_eight_branches(seed, split):
     check_draft(wl.cfg, toks, run_oracle(wl, ids, lens, toks))
 
 
+def test_draft_many_branches_take_the_tile_path():
+    """More branches than the few-row kernels take (40 > 32): the decode
+    steps run the tiled GEMMs and the tiled greedy LM head, and a decode
+    query tile spans many branch segments."""
+    cfg = SMALL_BF16.replace(name="small bf16 L2 d256 G2 F320 V1000, 40 branches", n_cands=40,
+                             cand_len=9)
+    wl, ids, lens = _case(cfg, 5)
+    v = make_verifier(wl, max_new=6, split_layers=1)
+    toks = run_draft(v, ids, lens, 6)
+    check_draft(cfg, toks, run_oracle(wl, ids, lens, toks))
+
+
 def test_draft_is_repeatable_and_leaves_scoring_alone():
     """A second draft overwrites the draft cache and gives the same tokens;
     scoring before and after a draft gives the same log-probs (separate
