@@ -138,7 +138,7 @@ def time_next_rows(v, cids, lens, dev, reps, log_fn):
     nk = int(r.n_keys.cpu()[0])
     log_fn(f"keyframes {kf_us:.1f} us/call, retrieve {rt_us:.1f} us/call ({nk} keyframes)")
     frame_bytes = frames.nbytes
-    bank_bytes = demb.nbytes * ((nk + 7) // 8)   # the bank is read once per 8 keyframes
+    bank_bytes = demb.nbytes * ((nk + 15) // 16)   # the bank is read once per 16 keyframes
     out.update({"keyframes_us": round(kf_us, 1),
                 "keyframes_GBs": round(frame_bytes / (kf_us * 1e-6) / 1e9, 1),
                 "retrieve_us": round(rt_us, 1),

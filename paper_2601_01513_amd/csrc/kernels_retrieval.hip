@@ -124,6 +124,31 @@ __device__ __forceinline__ void wave_best(float &s, int &i) {
   }
 }
 
+// The per-chunk top-k of keyframes g0 .. g0+ng-1 from sims [RG][RT] in LDS:
+// wave w of NWV takes keyframes w, w + NWV, ..., k passes of a wave-wide best.
+template <int NWV>
+__device__ __forceinline__ void chunk_topk(const float (*sims)[RT], int g0, int ng, int d0,
+                                           int nvalid, int k, int nchunks, SimIdx *part) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int r = w; r < ng; r += NWV) {
+    SimIdx *out = part + ((long)(g0 + r) * nchunks + blockIdx.x) * k;
+    float last_s = INFINITY;
+    int last_i = -1;
+    for (int p = 0; p < k; ++p) {
+      float bs = -INFINITY;
+      int bi = -1;
+      for (int j = lane; j < nvalid; j += 64) {
+        const float sj = sims[r][j];
+        if (before(last_s, last_i, sj, d0 + j)) keep_better(bs, bi, sj, d0 + j);
+      }
+      wave_best(bs, bi);
+      if (lane == 0) out[p] = SimIdx{bs, bi};  // -1: fewer than k documents left
+      last_s = bi < 0 ? -INFINITY : bs;
+      last_i = bi;
+    }
+  }
+}
+
 // Block (document chunk, keyframe group): thread t scores document
 // d0 + t against up to RG keyframes held in LDS (every lane reads the same
 // keyframe value: an LDS broadcast), then wave w picks the top-k of the chunk
@@ -187,46 +212,174 @@ __global__ __launch_bounds__(RT) void k_retrieve_chunk(const float *frame_emb,
     }
   }
   __syncthreads();
-  const int nvalid = min(RT, ND - d0);
-  for (int r = w; r < ng; r += RW) {
-    SimIdx *out = part + ((long)(g0 + r) * nchunks + blockIdx.x) * k;
-    float last_s = INFINITY;
-    int last_i = -1;
-    for (int p = 0; p < k; ++p) {
-      float bs = -INFINITY;
-      int bi = -1;
-      for (int j = lane; j < nvalid; j += 64) {
-        const float sj = sims[r][j];
-        if (before(last_s, last_i, sj, d0 + j)) keep_better(bs, bi, sj, d0 + j);
-      }
-      wave_best(bs, bi);
-      if (lane == 0) out[p] = SimIdx{bs, bi};  // -1: fewer than k documents left
-      last_s = bi < 0 ? -INFINITY : bs;
-      last_i = bi;
-    }
-  }
+  chunk_topk<RW>(sims, g0, ng, d0, min(RT, ND - d0), k, nchunks, part);
 }
 
-// Block r < n_keys (one wave): the top-k of keyframe r over every chunk's
-// top-k, k passes of a wave-wide best.
-__global__ __launch_bounds__(64) void k_retrieve_merge(const SimIdx *part, const int32_t *n_keys,
-                                                       int nchunks, int k, int32_t *top_idx,
-                                                       float *top_sim) {
-  const int r = blockIdx.x, lane = threadIdx.x;
-  if (r >= *n_keys) return;
+// Matrix-core scan for D % 16 == 0: the dot products of a chunk's 256
+// documents with up to 16 keyframes are a [256 x D] . [D x 16] product in
+// fp32 (v_mfma_f32_16x16x4_f32). Eight waves; wave w owns documents
+// 32 w .. 32 w + 31 as two 16-row tiles. Per 16 dimensions lane l loads 4
+// consecutive values of document (l % 16) of each tile (16 rows x 64
+// contiguous bytes per load) and the matching 4 values of keyframe (l % 16)
+// from LDS, and runs 4 products per tile (product j takes dimension
+// 4 (l / 16) + j of each lane group, the same for both operands). The
+// documents' squared norms come from the same loads. Steps of 64 dimensions;
+// the next step's loads are issued before the current step's products.
+constexpr int RM_T = 512;
+__global__ __launch_bounds__(RM_T) void k_retrieve_mfma(const float *frame_emb,
+                                                        const int32_t *key_idx,
+                                                        const int32_t *n_keys, const float *docs,
+                                                        int ND, int D, int k, int nchunks,
+                                                        SimIdx *part) {
+  constexpr int NG = RT / (RM_T / 64) / 16;  // 16-row tiles per wave
+  // The keyframes, [RG][D] (dynamic: D floats a row, so that two blocks fit
+  // a CU at D = 768).
+  extern __shared__ __align__(16) float q[];
+  __shared__ float qn[RG];
+  __shared__ float dn[RT];
+  __shared__ float sims[RG][RT];
+  const int nk = *n_keys;
+  const int g0 = blockIdx.y * RG;
+  if (g0 >= nk) return;  // uniform per block
+  const int ng = min(RG, nk - g0);
+  const int t = threadIdx.x, w = t >> 6, lane = t & 63;
+  for (int r = 0; r < RG; ++r) {  // rows past ng: zeros (their columns are unused)
+    const float *src = frame_emb + (long)key_idx[g0 + min(r, ng - 1)] * D;
+    for (int c = t; c < D; c += RM_T) q[r * D + c] = r < ng ? src[c] : 0.f;
+  }
+  __syncthreads();
+  for (int r = w; r < ng; r += RM_T / 64) {
+    float s = 0.f;
+    for (int c = lane; c < D; c += 64) s += q[r * D + c] * q[r * D + c];
+    s = wave_sum(s);
+    if (lane == 0) qn[r] = sqrtf(s);
+  }
+  const int d0 = blockIdx.x * RT;
+  const int sub = 4 * (lane >> 4);
+  const float *dp[NG];
+#pragma unroll
+  for (int g = 0; g < NG; ++g)
+    dp[g] = docs + (long)min(d0 + 16 * NG * w + 16 * g + (lane & 15), ND - 1) * D + sub;
+  const float *qp = q + (lane & 15) * D + sub;
+  f32x4 acc[NG];
+  float dd[NG];
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+    dd[g] = 0.f;
+  }
+  // Loads of the step at dimension c (pieces past D repeat the last one).
+  auto load = [&](int c, float4 (&v)[4][NG]) {
+    const int cnt = min(4, (D - c) / 16);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int cc = c + 16 * min(u, cnt - 1);
+#pragma unroll
+      for (int g = 0; g < NG; ++g) v[u][g] = *reinterpret_cast<const float4 *>(dp[g] + cc);
+    }
+  };
+  auto step = [&](int c, const float4 (&v)[4][NG]) {
+    const int cnt = min(4, (D - c) / 16);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (u >= cnt) break;
+      const float4 e = *reinterpret_cast<const float4 *>(qp + c + 16 * u);
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        const float4 x = v[u][g];
+        dd[g] += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+        acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.x, e.x, acc[g], 0, 0, 0);
+        acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.y, e.y, acc[g], 0, 0, 0);
+        acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.z, e.z, acc[g], 0, 0, 0);
+        acc[g] = __builtin_amdgcn_mfma_f32_16x16x4f32(x.w, e.w, acc[g], 0, 0, 0);
+      }
+    }
+  };
+  float4 va[4][NG], vb[4][NG];
+  load(0, va);
+  for (int c = 0; c < D; c += 128) {
+    if (c + 64 < D) load(c + 64, vb);
+    __builtin_amdgcn_sched_barrier(0);
+    step(c, va);
+    if (c + 64 >= D) break;
+    if (c + 128 < D) load(c + 128, va);
+    __builtin_amdgcn_sched_barrier(0);
+    step(c + 64, vb);
+  }
+  // Squared norm of document 16 NG w + 16 g + l % 16: the four lane groups'
+  // partial sums (fixed order).
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    float s = dd[g];
+    s += __shfl_xor(s, 16, 64);
+    s += __shfl_xor(s, 32, 64);
+    if (lane < 16) dn[16 * NG * w + 16 * g + lane] = sqrtf(s);
+  }
+  __syncthreads();
+  // Lane l holds document 16 NG w + 16 g + 4 (l / 16) + i against keyframe l % 16.
+  const int r = lane & 15;
+  if (r < ng) {
+#pragma unroll
+    for (int g = 0; g < NG; ++g)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int j = 16 * NG * w + 16 * g + 4 * (lane >> 4) + i;
+        const float den = qn[r] * dn[j];
+        sims[r][j] = den > 0.f ? acc[g][i] / den : 0.f;
+      }
+  }
+  __syncthreads();
+  chunk_topk<RM_T / 64>(sims, g0, ng, d0, min(RT, ND - d0), k, nchunks, part);
+}
+
+// Block r < n_keys: the top-k of keyframe r over every chunk's top-k. Each
+// thread holds its first MERGE_PER candidates in registers (loaded once; a
+// larger bank's further candidates are re-read on each pass); k passes of a
+// block-wide best (wave butterflies, then the waves in order).
+constexpr int MERGE_T = 1024;
+constexpr int MERGE_PER = 8;
+__global__ __launch_bounds__(MERGE_T) void k_retrieve_merge(const SimIdx *part,
+                                                            const int32_t *n_keys, int nchunks,
+                                                            int k, int32_t *top_idx,
+                                                            float *top_sim) {
+  __shared__ float ws[MERGE_T / 64];
+  __shared__ int wi[MERGE_T / 64];
+  const int r = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  if (r >= *n_keys) return;  // uniform per block
   const SimIdx *p = part + (long)r * nchunks * k;
   const int n = nchunks * k;
+  float cs[MERGE_PER];
+  int ci[MERGE_PER];
+#pragma unroll
+  for (int e = 0; e < MERGE_PER; ++e) {
+    const int j = t + e * MERGE_T;
+    const SimIdx c = j < n ? p[j] : SimIdx{-INFINITY, -1};
+    cs[e] = c.s;
+    ci[e] = c.i;
+  }
   float last_s = INFINITY;
   int last_i = -1;
   for (int q = 0; q < k; ++q) {
     float bs = -INFINITY;
     int bi = -1;
-    for (int e = lane; e < n; e += 64) {
-      const SimIdx c = p[e];
+#pragma unroll
+    for (int e = 0; e < MERGE_PER; ++e)
+      if (ci[e] >= 0 && before(last_s, last_i, cs[e], ci[e])) keep_better(bs, bi, cs[e], ci[e]);
+    for (int j = t + MERGE_PER * MERGE_T; j < n; j += MERGE_T) {
+      const SimIdx c = p[j];
       if (c.i >= 0 && before(last_s, last_i, c.s, c.i)) keep_better(bs, bi, c.s, c.i);
     }
     wave_best(bs, bi);
     if (lane == 0) {
+      ws[w] = bs;
+      wi[w] = bi;
+    }
+    __syncthreads();
+    bs = ws[0];
+    bi = wi[0];
+    for (int i = 1; i < MERGE_T / 64; ++i) keep_better(bs, bi, ws[i], wi[i]);
+    __syncthreads();
+    if (t == 0) {
       top_idx[(long)r * k + q] = bi;
       top_sim[(long)r * k + q] = bi < 0 ? 0.f : bs;
     }
@@ -314,9 +467,14 @@ hipError_t launch_retrieve(const float *frame_emb, const int32_t *key_idx, const
                            int32_t *n_sel, hipStream_t s) {
   const int nchunks = (ND + RT - 1) / RT;
   SimIdx *part = static_cast<SimIdx *>(ws);
-  k_retrieve_chunk<<<dim3(nchunks, (NF + RG - 1) / RG), RT, 0, s>>>(
-      frame_emb, key_idx, n_keys, docs, ND, D, k, nchunks, part);
-  k_retrieve_merge<<<NF, 64, 0, s>>>(part, n_keys, nchunks, k, top_idx, top_sim);
+  const dim3 grid(nchunks, (NF + RG - 1) / RG);
+  if (D % 16 == 0)
+    k_retrieve_mfma<<<grid, RM_T, RG * D * sizeof(float), s>>>(frame_emb, key_idx, n_keys, docs,
+                                                               ND, D, k, nchunks, part);
+  else
+    k_retrieve_chunk<<<grid, RT, 0, s>>>(frame_emb, key_idx, n_keys, docs, ND, D, k, nchunks,
+                                         part);
+  k_retrieve_merge<<<NF, MERGE_T, 0, s>>>(part, n_keys, nchunks, k, top_idx, top_sim);
   k_select_docs<<<1, 1024, 0, s>>>(top_idx, top_sim, n_keys, k, K, sel_idx, sel_sim, n_sel);
   return hipGetLastError();
 }

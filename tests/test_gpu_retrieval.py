@@ -159,6 +159,14 @@ def test_retrieval_sizes(nd, dim, k, K):
     check_retrieval(rc, *W.make_retrieval(rc, 3))
 
 
+def test_retrieval_million_documents():
+    """A bank whose per-chunk candidates (4096 chunks x k) exceed what the
+    merge holds in registers: the merge re-reads the rest on each pass."""
+    rc = W.RetrievalConfig("bank 2^20 x 16", 30, 16, 16, 4, 1 << 20, 16, 3, 8, 0.6)
+    _say(f"case: {rc.name}")
+    check_retrieval(rc, *W.make_retrieval(rc, 4))
+
+
 def test_retrieval_ties_take_lower_index():
     torch = _torch()
     rc = W.RetrievalConfig("ties", 10, 8, 8, 2, 40, 16, 4, 6, 0.6)
