@@ -17,36 +17,61 @@ constexpr int HB = 3 * BINS;        // bins of one frame
 constexpr int HIST_T = 1024;        // threads of the histogram block
 constexpr int HIST_W = HIST_T / 64;
 
-// Block f: the histogram of frame f. Each wave counts into its own LDS copy
-// (less contention on flat scenes), then the copies are summed.
+constexpr int HIST_SPLIT = 4;       // blocks per frame
+
+__global__ void k_zero_i32(int32_t *p, long n) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+// Block (f, part): the histogram of part `part` of HIST_SPLIT of frame f's
+// 16-byte chunks (and, for the last part, its trailing bytes), added into
+// hist[f] (zeroed before) with integer atomics: exact, so the counts do not
+// depend on the order. Each wave counts into its own LDS copy, then the
+// copies are summed.
 __global__ __launch_bounds__(HIST_T) void k_hist(const uint8_t *frames, long frame_bytes,
                                                  int32_t *hist) {
   __shared__ int32_t h[HIST_W][HB];
   const int t = threadIdx.x, w = t >> 6;
+  const int f = blockIdx.x / HIST_SPLIT, part = blockIdx.x % HIST_SPLIT;
   for (int i = t; i < HIST_W * HB; i += HIST_T) (&h[0][0])[i] = 0;
   __syncthreads();
-  const uint8_t *src = frames + (long)blockIdx.x * frame_bytes;
+  const uint8_t *src = frames + (long)f * frame_bytes;
   // 16-byte loads need every frame 16-byte aligned (the base is, by contract).
   const long n16 = frame_bytes % 16 == 0 ? frame_bytes / 16 : 0;
+  const long i0 = n16 * part / HIST_SPLIT, i1 = n16 * (part + 1) / HIST_SPLIT;
   // Byte b of the frame belongs to channel b % 3; a 16-byte chunk at byte
   // 16 i starts at channel (16 i) % 3 = i % 3.
-  for (long i = t; i < n16; i += HIST_T) {
-    const u32x4 v = reinterpret_cast<const u32x4 *>(src)[i];
-    int c = (int)(i % 3);
+  // Batches of HIST_B chunks per thread, all loads issued before counting.
+  constexpr int HIST_B = 8;
+  for (long i = i0 + t; i < i1; i += (long)HIST_B * HIST_T) {
+    u32x4 v[HIST_B];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const uint32_t byte = (v[j >> 2] >> (8 * (j & 3))) & 0xFFu;
-      atomicAdd(&h[w][c * BINS + (byte >> 2)], 1);
-      c = c == 2 ? 0 : c + 1;
+    for (int b = 0; b < HIST_B; ++b) {
+      const long ib = i + (long)b * HIST_T;
+      v[b] = ib < i1 ? reinterpret_cast<const u32x4 *>(src)[ib] : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int b = 0; b < HIST_B; ++b) {
+      const long ib = i + (long)b * HIST_T;
+      if (ib >= i1) break;
+      int c = (int)(ib % 3);
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const uint32_t byte = (v[b][j >> 2] >> (8 * (j & 3))) & 0xFFu;
+        atomicAdd(&h[w][c * BINS + (byte >> 2)], 1);
+        c = c == 2 ? 0 : c + 1;
+      }
     }
   }
-  for (long b = n16 * 16 + t; b < frame_bytes; b += HIST_T)
-    atomicAdd(&h[w][(int)(b % 3) * BINS + (src[b] >> 2)], 1);
+  if (part == HIST_SPLIT - 1)
+    for (long b = n16 * 16 + t; b < frame_bytes; b += HIST_T)
+      atomicAdd(&h[w][(int)(b % 3) * BINS + (src[b] >> 2)], 1);
   __syncthreads();
   for (int i = t; i < HB; i += HIST_T) {
     int32_t s = 0;
     for (int k = 0; k < HIST_W; ++k) s += h[k][i];
-    hist[(long)blockIdx.x * HB + i] = s;
+    if (s) atomicAdd(&hist[(long)f * HB + i], s);
   }
 }
 
@@ -450,7 +475,9 @@ hipError_t launch_keyframes(const uint8_t *frames, int NF, int H, int W, float t
                             int32_t *hist, int32_t *inter, int32_t *key_idx, int32_t *n_keys,
                             hipStream_t s) {
   const long fb = (long)H * W * 3;
-  k_hist<<<NF, HIST_T, 0, s>>>(frames, fb, hist);
+  const long nh = (long)NF * HB;
+  k_zero_i32<<<(unsigned)((nh + 255) / 256), 256, 0, s>>>(hist, nh);
+  k_hist<<<NF * HIST_SPLIT, HIST_T, 0, s>>>(frames, fb, hist);
   const double thr = (double)theta * 3.0 * (double)((long)H * W);  // (theta 3) (H W)
   k_keyframes<<<1, 1024, 0, s>>>(hist, NF, thr, inter, key_idx, n_keys);
   return hipGetLastError();
