@@ -192,9 +192,44 @@ hipError_t launch_embed_rows(const int32_t *ids, int rows, const T *embed, int d
 }
 
 // ------------------------------------------------------------------ RMSNorm
+// One row by a 256-thread block: y = x / sqrt(mean(x^2) + eps) * g (+ the
+// remainder half when split == 2). Rows of d % 4 == 0, d <= 8192 are read once
+// as float4 and kept in registers; others take the scalar two-pass path.
 template <typename TW, typename TA>
 __device__ __forceinline__ void norm_row(const float *src, const TW *g, int d, float eps,
                                          TA *dst, float *red, int split = 1) {
+  constexpr int NV = 8;  // float4 per thread: d <= 256 * 4 * NV
+  if (d % 4 == 0 && d <= 256 * 4 * NV) {
+    const int n4 = d / 4;
+    float4 v[NV];
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c4 = threadIdx.x + 256 * i;
+      v[i] = c4 < n4 ? reinterpret_cast<const float4 *>(src)[c4] : make_float4(0.f, 0.f, 0.f, 0.f);
+      ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
+    }
+    ss = block_sum256(ss, red);
+    const float r = rsqrtf(ss / (float)d + eps);
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c4 = threadIdx.x + 256 * i;
+      if (c4 >= n4) break;
+      const float x[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+      TA hi[4], lo[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float y = x[e] * r * to_f32(g[4 * c4 + e]);
+        hi[e] = from_f32<TA>(y);
+        lo[e] = from_f32<TA>(y - to_f32(hi[e]));
+      }
+      // Four outputs per store.
+      struct alignas(4 * sizeof(TA)) Q4 { TA v[4]; };
+      *reinterpret_cast<Q4 *>(dst + 4 * c4) = Q4{{hi[0], hi[1], hi[2], hi[3]}};
+      if (split == 2) *reinterpret_cast<Q4 *>(dst + d + 4 * c4) = Q4{{lo[0], lo[1], lo[2], lo[3]}};
+    }
+    return;
+  }
   float ss = 0.f;
   for (int c = threadIdx.x; c < d; c += 256) {
     const float v = src[c];
