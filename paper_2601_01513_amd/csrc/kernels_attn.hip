@@ -82,8 +82,10 @@ struct Lane {
   int tok;   // SEG_CAUSAL: the row's query token (its last visible key);
              // SEG_BRANCH: its last visible branch key (its own cache position)
   int lo;    // SEG_BRANCH: first visible key
-  float m;   // running maximum of the raw (unscaled) scores
+  float m;   // reference of the exponents (raw score units): the running
+             // maximum, moved only when a score exceeds it by more than thr
   float l;   // running sum of exp2(s * c - m * c)
+  float thr; // 8 / c: probabilities stay below 2^8 between moves
   f32x16 o[HD / 32];
   const u32x4 *qs;  // fast: the block's query tile in LDS [QT rows][16 chunks]
   int qrow;         // fast: this lane's row in it
@@ -164,7 +166,11 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *st
       mloc = fmaxf(mloc, s[b][r]);
     }
   mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-  const float mnew = fmaxf(L.m, mloc);
+  // Lazy reference: moving it costs a rescale of the 64 output accumulators,
+  // so it moves only when this tile's maximum exceeds it by more than thr
+  // (exp2 values below 2^8 stay exact to fp16's relative precision; l and o
+  // share the reference, so the normalised output is unchanged).
+  const float mnew = mloc > L.m + L.thr ? mloc : L.m;
   const float mref = mnew == -INFINITY ? 0.f : -mnew * scale_log2;  // exponent offset
   float psum = 0.f;
   f16x8 p[4], pl[4];
@@ -179,8 +185,11 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *st
       if constexpr (PREC) pl[b * 2 + (r >> 3)][r & 7] = static_cast<f16>(e - static_cast<float>(eh));
     }
   psum += __shfl_xor(psum, 32, 64);
-  if (mnew != L.m) {  // rescale only when this lane's running max moved
-    const float alpha = __builtin_amdgcn_exp2f(fmaf(L.m, scale_log2, mref));
+  // Rescale when the reference of any lane of the wave moved (a wave-uniform
+  // branch: the 64 multiplies are skipped in the common case, not predicated).
+  const bool moved = mnew != L.m;
+  if (__builtin_amdgcn_ballot_w64(moved)) {
+    const float alpha = moved ? __builtin_amdgcn_exp2f(fmaf(L.m, scale_log2, mref)) : 1.f;
     L.l *= alpha;
 #pragma unroll
     for (int db = 0; db < HD / 32; ++db) L.o[db] *= alpha;
@@ -273,9 +282,12 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
   __shared__ u32x4 lds[2 * Shape<PREC>::STAGE];
   __shared__ u32x4 qlds[PREC ? 1 : QT * 16];
   const int G = a.n_heads / a.n_kv, TG = (a.T - a.t0) * G;
-  const int kvh = blockIdx.y;
-  // Prefill tiles with more keys first.
-  const int qt = MODE == 0 ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
+  // Prefill: one block index over (query tile, KV head), tiles with more keys
+  // first across all heads, so that the longest blocks start in the first
+  // round and the short ones fill in behind them.
+  const int nqt = MODE == 0 ? (int)gridDim.x / a.n_kv : (int)gridDim.x;
+  const int kvh = MODE == 0 ? (int)blockIdx.x % a.n_kv : (int)blockIdx.y;
+  const int qt = MODE == 0 ? nqt - 1 - (int)blockIdx.x / a.n_kv : (int)blockIdx.x;
   const int q0 = qt * QT;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int row = q0 + w * 32 + (lane & 31);
@@ -314,6 +326,7 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
   L.qs = qlds;
   L.qrow = w * 32 + (lane & 31);
   const float scale_log2 = 1.4426950408889634f * rsqrtf((float)HD);
+  L.thr = 8.f / scale_log2;
   const int tok_first = a.t0 + q0 / G;
   const int tok_last = a.t0 + min(q0 + QT - 1, TG - 1) / G;
 
@@ -464,7 +477,8 @@ template <int MODE, bool PREC>
 hipError_t launch_attn(const AttnArgs &a, hipStream_t s) {
   using S = Shape<PREC>;
   const int G = a.n_heads / a.n_kv;
-  dim3 grid(((a.T - a.t0) * G + S::QT - 1) / S::QT, a.n_kv, MODE == 0 ? 1 : a.nchunks);
+  const int nqt = ((a.T - a.t0) * G + S::QT - 1) / S::QT;
+  const dim3 grid = MODE == 0 ? dim3(nqt * a.n_kv) : dim3(nqt, a.n_kv, a.nchunks);
   k_attn<MODE, PREC><<<grid, S::NT, 0, s>>>(a);
   return hipGetLastError();
 }

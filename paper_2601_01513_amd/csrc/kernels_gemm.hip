@@ -332,12 +332,20 @@ __device__ __forceinline__ void store_partial(const f32x16 (&acc)[TL::FM][TL::FN
   }
 }
 
-// Sum of the partials of local element e (row * 256 + col) of tail tile i.
+// Sum of the partials of local element e (row * 256 + col) of tail tile i,
+// in split order. All kMaxSplit loads are issued before the first add (split
+// indices past nsplit re-read the last partial and are not added), so the
+// latencies overlap instead of adding up.
 __device__ __forceinline__ float sum_partials(const float *part, const Launch &ln, int i, int e) {
   const float *p = part + (long)i * ln.nsplit * kTileElems + e;
-  float v = 0.f;
-  for (int s = 0; s < ln.nsplit; ++s) v += p[(long)s * kTileElems];
-  return v;
+  float v[kMaxSplit];
+#pragma unroll
+  for (int s = 0; s < kMaxSplit; ++s) v[s] = p[(long)min(s, ln.nsplit - 1) * kTileElems];
+  float sum = 0.f;
+#pragma unroll
+  for (int s = 0; s < kMaxSplit; ++s)
+    if (s < ln.nsplit) sum += v[s];
+  return sum;
 }
 
 __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.f + __expf(-g)) * u; }
