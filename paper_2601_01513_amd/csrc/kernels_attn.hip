@@ -84,7 +84,8 @@ struct Lane {
   int lo;    // SEG_BRANCH: first visible key
   float m;   // reference of the exponents (raw score units): the running
              // maximum, moved only when a score exceeds it by more than thr
-  float l;   // running sum of exp2(s * c - m * c)
+  float l;   // running sum of exp2(s * c - m * c) over this lane's half of
+             // the keys (the halves are added once, after the walk)
   float thr; // 8 / c: probabilities stay below 2^8 between moves
   f32x16 o[HD / 32];
   const u32x4 *qs;  // fast: the block's query tile in LDS [QT rows][16 chunks]
@@ -122,6 +123,21 @@ template <bool PREC>
 __device__ __forceinline__ void load_tile(const Seg &sg, int kb, u32x4 *stage) {
   load_kv<Shape<PREC>::NW>(sg.k, sg.vt, sg.npos, kb, stage);
   if constexpr (PREC) load_kv<Shape<PREC>::NW>(sg.k_lo, sg.vt_lo, sg.npos, kb, stage + KCH + VCH);
+}
+
+// Lane pairs (l, l ^ 32) hold the two halves of a query's keys; these
+// combine a value over the pair through v_permlane32_swap (no LDS trip). The
+// swap of x with itself leaves (x[l], x[l ^ 32]) in some order in every lane.
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  // r[0] is the lower-half lane's value in both halves: the same order in both.
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 __device__ __forceinline__ f32x16 mfma(f16x8 a, f16x8 b, f32x16 c) {
@@ -165,7 +181,7 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *st
       }
       mloc = fmaxf(mloc, s[b][r]);
     }
-  mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+  mloc = max_halves(mloc);
   // Lazy reference: moving it costs a rescale of the 64 output accumulators,
   // so it moves only when this tile's maximum exceeds it by more than thr
   // (exp2 values below 2^8 stay exact to fp16's relative precision; l and o
@@ -184,7 +200,6 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *st
       p[b * 2 + (r >> 3)][r & 7] = eh;
       if constexpr (PREC) pl[b * 2 + (r >> 3)][r & 7] = static_cast<f16>(e - static_cast<float>(eh));
     }
-  psum += __shfl_xor(psum, 32, 64);
   // Rescale when the reference of any lane of the wave moved (a wave-uniform
   // branch: the 64 multiplies are skipped in the common case, not predicated).
   const bool moved = mnew != L.m;
@@ -374,6 +389,7 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
     walk_concat<PREC>(sp, sb, pre_t, lo, c0, c1, lds, L, scale_log2);
   }
 
+  L.l = sum_halves(L.l);
   if (row >= TG) return;
   const int h = lane >> 5;
   if (MODE == 0 || a.nchunks == 1) {
