@@ -35,6 +35,14 @@ def _short(name: str) -> str:
         base = "k_attn<0> (prefill" + (", precise)" if precise else ")")
     elif "k_attnILi1" in name or "k_attn<1" in name:
         base = "k_attn<1> (cascade" + (", precise)" if precise else ")")
+    elif "k_attnILi2" in name or "k_attn<2" in name:
+        base = "k_attn<2> (draft" + (", precise)" if precise else ")")
+    elif base == "k_skinny":
+        # k_skinny<rows per group, A split, bf16 weights, greedy LM head>
+        m = re.search(r"k_skinnyILi(\d+)ELi(\d+)ELb(\d)ELb(\d)E", name)
+        if m:
+            base = "k_skinny (" + ("greedy LM head" if m.group(4) == "1" else "product") + \
+                (", split A" if m.group(2) == "2" else "") + ")"
     return base
 
 
