@@ -43,11 +43,14 @@ constexpr int KT = 64;    // keys per tile
 constexpr int KCH = KT * 16;   // 16-byte chunks of a K tile  [64 keys][128 dims]
 constexpr int VCH = HD * 8;    // 16-byte chunks of a V^T tile [128 dims][64 keys]
 
-// Block shape of the fast (PREC = false) and precise (PREC = true) variants.
-// An LDS stage holds [K | V^T] tiles, precise: [K | V^T | K lo | V^T lo].
-template <bool PREC>
+// Block shape of the fast (PREC = false), precise (PREC = true) and decode
+// (DEC: one wave, the draft pass's decode steps with at most 32 stacked query
+// rows per KV head, where a wider block would mostly compute padding rows)
+// variants. An LDS stage holds [K | V^T] tiles, precise: [K | V^T | K lo |
+// V^T lo].
+template <bool PREC, bool DEC = false>
 struct Shape {
-  static constexpr int NW = PREC ? 4 : 8;  // waves per block
+  static constexpr int NW = PREC ? 4 : (DEC ? 1 : 8);  // waves per block
   static constexpr int NT = NW * 64;
   static constexpr int QT = NW * 32;       // stacked query rows per block
   static constexpr int STAGE = (PREC ? 2 : 1) * (KCH + VCH);
@@ -119,10 +122,11 @@ __device__ __forceinline__ void load_kv(const f16 *k, const f16 *vt, int npos, i
   }
 }
 
-template <bool PREC>
+template <bool PREC, bool DEC>
 __device__ __forceinline__ void load_tile(const Seg &sg, int kb, u32x4 *stage) {
-  load_kv<Shape<PREC>::NW>(sg.k, sg.vt, sg.npos, kb, stage);
-  if constexpr (PREC) load_kv<Shape<PREC>::NW>(sg.k_lo, sg.vt_lo, sg.npos, kb, stage + KCH + VCH);
+  constexpr int NW = Shape<PREC, DEC>::NW;
+  load_kv<NW>(sg.k, sg.vt, sg.npos, kb, stage);
+  if constexpr (PREC) load_kv<NW>(sg.k_lo, sg.vt_lo, sg.npos, kb, stage + KCH + VCH);
 }
 
 // Lane pairs (l, l ^ 32) hold the two halves of a query's keys; these
@@ -235,18 +239,18 @@ __device__ __forceinline__ bool tile_clear(const Seg &sg, int kb) {
   return sg.mode == SEG_ALL;
 }
 
-template <bool PREC>
+template <bool PREC, bool DEC>
 __device__ __forceinline__ void walk_segment(const Seg &sg, u32x4 *lds, Lane &L,
                                              float scale_log2) {
-  constexpr int STAGE = Shape<PREC>::STAGE;
+  constexpr int STAGE = Shape<PREC, DEC>::STAGE;
   if (sg.kend <= sg.kbeg) return;
-  load_tile<PREC>(sg, sg.kbeg, lds);
+  load_tile<PREC, DEC>(sg, sg.kbeg, lds);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   int stage = 0;
   for (int kb = sg.kbeg; kb < sg.kend; kb += KT) {
     u32x4 *cur = lds + stage * STAGE;
-    if (kb + KT < sg.kend) load_tile<PREC>(sg, kb + KT, lds + (stage ^ 1) * STAGE);
+    if (kb + KT < sg.kend) load_tile<PREC, DEC>(sg, kb + KT, lds + (stage ^ 1) * STAGE);
     if (tile_clear(sg, kb))
       tile_step<false, PREC>(sg, kb, cur, L, scale_log2);
     else
@@ -260,21 +264,21 @@ __device__ __forceinline__ void walk_segment(const Seg &sg, u32x4 *lds, Lane &L,
 // Tiles v0 .. v1-1 of the concatenation [prefix tiles 0 .. pre_t-1 | branch
 // tiles from key bbeg on]: one pipeline for both sources (the tile's source
 // is chosen per tile), so that one set of load offsets is live.
-template <bool PREC>
+template <bool PREC, bool DEC>
 __device__ __forceinline__ void walk_concat(const Seg &sp, const Seg &sb, int pre_t, int bbeg,
                                             int v0, int v1, u32x4 *lds, Lane &L,
                                             float scale_log2) {
-  constexpr int STAGE = Shape<PREC>::STAGE;
+  constexpr int STAGE = Shape<PREC, DEC>::STAGE;
   if (v1 <= v0) return;
   auto src = [&](int v) -> const Seg & { return v < pre_t ? sp : sb; };
   auto key0 = [&](int v) { return v < pre_t ? v * KT : bbeg + (v - pre_t) * KT; };
-  load_tile<PREC>(src(v0), key0(v0), lds);
+  load_tile<PREC, DEC>(src(v0), key0(v0), lds);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   int stage = 0;
   for (int v = v0; v < v1; ++v) {
     u32x4 *cur = lds + stage * STAGE;
-    if (v + 1 < v1) load_tile<PREC>(src(v + 1), key0(v + 1), lds + (stage ^ 1) * STAGE);
+    if (v + 1 < v1) load_tile<PREC, DEC>(src(v + 1), key0(v + 1), lds + (stage ^ 1) * STAGE);
     const Seg &sg = src(v);
     const int kb = key0(v);
     if (tile_clear(sg, kb))
@@ -291,10 +295,10 @@ __device__ __forceinline__ void walk_concat(const Seg &sp, const Seg &sb, int pr
 // mode 1: candidate pass (chunk blockIdx.z of the prefix; the last chunk also
 //         walks the candidates' own keys);
 // mode 2: draft pass (chunk blockIdx.z of the prefix + branch-cache tiles).
-template <int MODE, bool PREC>
-__global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
-  constexpr int QT = Shape<PREC>::QT;
-  __shared__ u32x4 lds[2 * Shape<PREC>::STAGE];
+template <int MODE, bool PREC, bool DEC = false>
+__global__ __launch_bounds__((Shape<PREC, DEC>::NT)) void k_attn(AttnArgs a) {
+  constexpr int QT = Shape<PREC, DEC>::QT;
+  __shared__ u32x4 lds[2 * Shape<PREC, DEC>::STAGE];
   __shared__ u32x4 qlds[PREC ? 1 : QT * 16];
   const int G = a.n_heads / a.n_kv, TG = (a.T - a.t0) * G;
   // Prefill: one block index over (query tile, KV head), tiles with more keys
@@ -351,7 +355,7 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
     Seg sg{a.k + koff, a.vt + koff, PREC ? a.k_lo + koff : nullptr,
            PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.T, 0, tok_last + 1, SEG_CAUSAL,
            tok_first};
-    walk_segment<PREC>(sg, lds, L, scale_log2);
+    walk_segment<PREC, DEC>(sg, lds, L, scale_log2);
   } else if (MODE == 1) {
     // Candidate pass: chunks of whole prefix tiles (the last one short); the
     // last chunk also walks the branch keys from the block's first query's
@@ -361,13 +365,13 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
     const int kb = min(a.P, chunk * ct * KT), ke = min(a.P, (chunk + 1) * ct * KT);
     Seg sp{a.k + koff, a.vt + koff, PREC ? a.k_lo + koff : nullptr,
            PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.P, kb, ke, SEG_ALL, tok_first};
-    walk_segment<PREC>(sp, lds, L, scale_log2);
+    walk_segment<PREC, DEC>(sp, lds, L, scale_log2);
     if (chunk == a.nchunks - 1) {
       const int lo = a.row_lo[tok_first] & ~(KT - 1);
       Seg sb{a.bk + boff, a.bvt + boff, PREC ? a.bk_lo + boff : nullptr,
              PREC ? a.bvt_lo + boff : nullptr, a.bk_npos, a.T, lo, tok_last + 1, SEG_BRANCH,
              tok_first};
-      walk_segment<PREC>(sb, lds, L, scale_log2);
+      walk_segment<PREC, DEC>(sb, lds, L, scale_log2);
     }
   } else {
     // Draft pass (cache positions given): one query tile may hold rows of
@@ -386,7 +390,7 @@ __global__ __launch_bounds__(Shape<PREC>::NT) void k_attn(AttnArgs a) {
     const Seg sb{a.bk + boff, a.bvt + boff, PREC ? a.bk_lo + boff : nullptr,
                  PREC ? a.bvt_lo + boff : nullptr, a.bk_npos, a.bk_valid, 0, 0, SEG_BRANCH,
                  tok_first};
-    walk_concat<PREC>(sp, sb, pre_t, lo, c0, c1, lds, L, scale_log2);
+    walk_concat<PREC, DEC>(sp, sb, pre_t, lo, c0, c1, lds, L, scale_log2);
   }
 
   L.l = sum_halves(L.l);
@@ -489,13 +493,13 @@ __global__ __launch_bounds__(64 * NW) void k_attn_merge(AttnArgs a) {
   }
 }
 
-template <int MODE, bool PREC>
+template <int MODE, bool PREC, bool DEC = false>
 hipError_t launch_attn(const AttnArgs &a, hipStream_t s) {
-  using S = Shape<PREC>;
+  using S = Shape<PREC, DEC>;
   const int G = a.n_heads / a.n_kv;
   const int nqt = ((a.T - a.t0) * G + S::QT - 1) / S::QT;
   const dim3 grid = MODE == 0 ? dim3(nqt * a.n_kv) : dim3(nqt, a.n_kv, a.nchunks);
-  k_attn<MODE, PREC><<<grid, S::NT, 0, s>>>(a);
+  k_attn<MODE, PREC, DEC><<<grid, S::NT, 0, s>>>(a);
   return hipGetLastError();
 }
 
@@ -515,7 +519,11 @@ hipError_t attn_cascade(const AttnArgs &a, bool precise, hipStream_t s) {
     return hipErrorInvalidValue;
   if (a.q_pos) {  // draft pass
     if (a.bk_valid <= 0) return hipErrorInvalidValue;
-    return precise ? launch_attn<2, true>(a, s) : launch_attn<2, false>(a, s);
+    if (precise) return launch_attn<2, true>(a, s);
+    // Decode steps: all stacked query rows of a KV head in one wave.
+    if ((a.T - a.t0) * (a.n_heads / a.n_kv) <= Shape<false, true>::QT)
+      return launch_attn<2, false, true>(a, s);
+    return launch_attn<2, false>(a, s);
   }
   return precise ? launch_attn<1, true>(a, s) : launch_attn<1, false>(a, s);
 }
