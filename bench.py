@@ -1,8 +1,9 @@
 """Benchmark of the verifier scoring pass on one GPU.
 
-A step is one verify pass: vsr_prefill over the shared prefix followed by
-vsr_score of all candidates (the prefix KV is rebuilt every step). Inputs are
-seeded synthetic tensors resident in HBM before the timed region.
+A step is one verify pass: vsr_verify, the prefill over the shared prefix
+and the scoring of all candidates as one fused pass (the prefix KV is rebuilt
+every step). Inputs are seeded synthetic tensors resident in HBM before the
+timed region.
 
 Prints one JSON line: candidate tokens scored per second over the timed steps,
 the roofline position of the dominant kernel (from per-launch HIP-event
@@ -34,14 +35,14 @@ PEAK_HBM_GBS = 8000.0
 
 # Kernels as the profiler sees them, and the stages each one serves.
 KERNELS = {
-    "k_gemm_swiglu": ["prefill.gate_up_swiglu", "score.gate_up_swiglu"],
-    "k_gemm_residual": ["prefill.o_proj", "prefill.down_proj", "score.o_proj", "score.down_proj"],
-    "k_gemm_qkv": ["prefill.qkv_rope", "score.qkv_rope"],
-    "k_attn<0> (prefill)": ["prefill.attention"],
-    "k_attn<1> (cascade)": ["score.attention"],
-    "k_attn_merge": ["score.attn_merge"],
-    "k_gemm_lmhead": ["score.lm_head_lse"],
-    "k_rmsnorm": ["prefill.rmsnorm", "score.rmsnorm"],
+    "k_gemm_swiglu": ["verify.gate_up_swiglu"],
+    "k_gemm_residual": ["verify.o_proj", "verify.down_proj"],
+    "k_gemm_qkv": ["verify.qkv_rope"],
+    "k_attn<0> (prefill)": ["verify.attention"],
+    "k_attn<1> (cascade)": ["verify.cand_attention"],
+    "k_attn_merge": ["verify.attn_merge"],
+    "k_gemm_lmhead": ["verify.lm_head_lse"],
+    "k_rmsnorm": ["verify.rmsnorm"],
 }
 
 
@@ -50,28 +51,26 @@ def log(msg):
 
 
 def stage_flops(cfg, P, lens):
-    """Algorithmic FLOPs of one verify pass per stage (multiply-add = 2).
+    """Algorithmic FLOPs of one fused verify pass per stage (multiply-add = 2).
 
-    The prefix pass's last layer needs keys/values for every prefix row but
-    attention, projections and FFN only for the last row (the one predicting
-    candidate token 0), which is all the library computes there; those
-    one-row projections run the few-row kernels and are timed as a stage of
-    their own (prefill.tail_proj).
+    The prefix rows and the candidate rows share every projection. The last
+    layer needs keys/values for every row but attention, projections and FFN
+    only for the last prefix row (the one predicting candidate token 0) and
+    the candidate rows, which is all the library computes there.
     """
     d, hq, hd, F, V = cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ff, cfg.vocab
     L = cfg.n_layers
     T = int(sum(lens))
-    f = {}
-    for ph, rows, body in (("prefill", P, P * max(L - 1, 0)), ("score", T, T * L)):
-        f[f"{ph}.qkv_rope"] = 2.0 * rows * cfg.qkv_rows * d * L
-        f[f"{ph}.o_proj"] = 2.0 * body * d * hq * hd
-        f[f"{ph}.gate_up_swiglu"] = 2.0 * body * 2 * F * d
-        f[f"{ph}.down_proj"] = 2.0 * body * d * F
-    f["prefill.tail_proj"] = 2.0 * (d * hq * hd + 3 * F * d) if L else 0.0
+    rows = P + T
+    body = rows * max(L - 1, 0) + (T + 1 if L else 0)
+    f = {"verify.qkv_rope": 2.0 * rows * cfg.qkv_rows * d * L,
+         "verify.o_proj": 2.0 * body * d * hq * hd,
+         "verify.gate_up_swiglu": 2.0 * body * 2 * F * d,
+         "verify.down_proj": 2.0 * body * d * F}
     # QK^T and PV over the visible keys of every query (causal / cascade).
-    f["prefill.attention"] = 4.0 * hd * hq * ((P * (P + 1) / 2) * (L - 1) + P) if L else 0.0
-    f["score.attention"] = 4.0 * hd * hq * sum(n * P + n * (n + 1) / 2 for n in lens) * L
-    f["score.lm_head_lse"] = 2.0 * T * V * d
+    f["verify.attention"] = 4.0 * hd * hq * ((P * (P + 1) / 2) * (L - 1) + P) if L else 0.0
+    f["verify.cand_attention"] = 4.0 * hd * hq * sum(n * P + n * (n + 1) / 2 for n in lens) * L
+    f["verify.lm_head_lse"] = 2.0 * T * V * d
     return f
 
 
@@ -292,8 +291,7 @@ def main():
            torch.empty(1, dtype=torch.int32, device=dev))
 
     def step():
-        v.prefill(vis, ids)
-        v.score(cids, lens, out=out)
+        v.verify(vis, ids, cids, lens, out=out)
 
     for _ in range(args.warmup):
         step()
@@ -343,8 +341,11 @@ def main():
                 "launches": launches, "avg_launch_ms": round(avg_ms, 4),
                 "flop_per_launch": kflops / launches}
 
-    pre = sum(ms for k, ms in per_step.items() if k.startswith("prefill."))
-    sco = sum(ms for k, ms in per_step.items() if k.startswith("score."))
+    total = sum(per_step.values())
+    gemm = sum(per_step.get(f"verify.{k}", 0.0)
+               for k in ("qkv_rope", "o_proj", "gate_up_swiglu", "down_proj", "lm_head_lse"))
+    attn = sum(per_step.get(f"verify.{k}", 0.0)
+               for k in ("attention", "cand_attention", "attn_merge"))
     result = {
         "metric": METRIC, "value": round(value, 1), "unit": "candidate tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -355,8 +356,8 @@ def main():
                    "heads": f"{cfg.n_heads}/{cfg.n_kv_heads}", "d_ff": cfg.d_ff,
                    "vocab": cfg.vocab, "prefix": cfg.n_prefix, "visual_rows": cfg.n_visual,
                    "candidates": M, "cand_len": cmax, "tokens_scored": tokens},
-        "breakdown": {"prefill_kernel_ms": round(pre, 3), "score_kernel_ms": round(sco, 3),
-                      "score_only_tok_s": round(tokens / (sco / 1e3), 1) if sco else None},
+        "breakdown": {"kernel_ms": round(total, 3), "gemm_ms": round(gemm, 3),
+                      "attention_ms": round(attn, 3)},
         "roofline": roofline,
     }
     if not args.no_next_rows:

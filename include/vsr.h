@@ -13,7 +13,10 @@
  *   vsr_score    teacher-forces M candidates against that cache and returns
  *                lp[m][j] = log P(c_mj | prefix, c_m<j)   (j < n_m, else 0),
  *                score[m] = sum_j lp[m][j]                 (Eq. 6),
- *                argmax   = lowest m with the largest score (Eq. 7).
+ *                argmax   = lowest m with the largest score (Eq. 7);
+ *   vsr_verify   both in one pass (the prefix rows and the candidate rows
+ *                share every projection launch), leaving the prefix cache
+ *                as vsr_prefill does.
  *
  * Each candidate sees the prefix plus its own earlier tokens only (the drafts
  * are scored independently, Eq. 6); candidate token j sits at position P + j.
@@ -157,6 +160,23 @@ int vsr_score(vsr_ctx *ctx, const int32_t *cand_ids, const int32_t *cand_len,
               int32_t M, int32_t Cmax, float *logprobs, float *scores,
               int32_t *argmax);
 
+/* vsr_prefill followed by vsr_score, computed as one pass (Section 3.1,
+ * Eq. 6-7): the prefix rows and the candidate rows go through each
+ * projection of each layer as one set of rows, so the candidates add rows to
+ * the prefix's matrix products instead of running products of their own;
+ * per layer the prefix rows attend causally over the prefix and each
+ * candidate row over the prefix and its own earlier tokens, as in the two
+ * calls. Arguments as vsr_prefill (visual, n_visual, ids, n_text) and
+ * vsr_score (cand_ids .. argmax), with the same checks and errors; the
+ * outputs agree with the two calls' to rounding (products of other row
+ * groupings). On success the context holds the prefix cache, as after
+ * vsr_prefill, for later vsr_score / vsr_reliability / vsr_draft calls. A
+ * call rejected by its argument checks changes nothing; one that fails later
+ * leaves no prefix current (like vsr_prefill). */
+int vsr_verify(vsr_ctx *ctx, const void *visual, int32_t n_visual, const int32_t *ids,
+               int32_t n_text, const int32_t *cand_ids, const int32_t *cand_len, int32_t M,
+               int32_t Cmax, float *logprobs, float *scores, int32_t *argmax);
+
 /* Stage 1 of the two-stage verification (Section 3.2, Eq. 11-13): the
  * reliability of M drafts against the current prefix. Branch m (the draft's
  * answer, entity and reasoning tokens followed by the verification prompt)
@@ -278,18 +298,22 @@ void vsr_destroy(vsr_ctx *ctx);
 
 /* ---- measurement (not part of the method) ----------------------------------
  * Per-stage kernel timing for benchmarks: while enabled, every stage launch of
- * vsr_prefill / vsr_score / vsr_reliability / vsr_draft is bracketed by HIP
- * events on the context's stream. Stage s of the prefix pass is s, of the
- * candidate pass (score, reliability) VSR_STAGE_KINDS + s, of the draft
- * pass 2 VSR_STAGE_KINDS + s (there kind 9 is the LM head + chunk argmax and
- * kind 11 the greedy pick);
+ * vsr_prefill / vsr_score / vsr_reliability / vsr_draft / vsr_verify is
+ * bracketed by HIP events on the context's stream. Stage s of the prefix pass
+ * is s, of the candidate pass (score, reliability) VSR_STAGE_KINDS + s, of the
+ * draft pass 2 VSR_STAGE_KINDS + s (there kind 9 is the LM head + chunk argmax
+ * and kind 11 the greedy pick), of the fused pass of vsr_verify on bf16
+ * contexts 3 VSR_STAGE_KINDS + s (there kind 3 is the prefix rows' attention,
+ * kind 15 the candidate rows'; on fp32 contexts vsr_verify records prefix and
+ * candidate passes);
  * kinds: 0 embedding, 1 RMSNorm, 2 QKV projection + rotary + cache write,
  * 3 attention, 4 attention merge, 5 output projection, 6 gate/up + SwiGLU,
  * 7 down projection, 8 LM-head inputs, 9 LM head + chunk LSE,
  * 10 LSE merge + target gather, 11 sum + argmax, 12 row tables, 13 copy,
- * 14 the prefix pass's last-row layer projections (O, gate/up, down). */
-#define VSR_STAGE_KINDS 15
-#define VSR_STAGES (3 * VSR_STAGE_KINDS)
+ * 14 the prefix pass's last-row layer projections (O, gate/up, down),
+ * 15 the candidate rows' attention of the fused pass. */
+#define VSR_STAGE_KINDS 16
+#define VSR_STAGES (4 * VSR_STAGE_KINDS)
 
 /* Times the stage kinds whose bits are set in kinds (bit k: kind k, in all
  * passes; VSR_PROFILE_ALL: every kind; 0: timing off) and clears what was

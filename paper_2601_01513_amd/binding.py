@@ -19,7 +19,7 @@ GEMM_WEIGHT_KEYS = ("wqkv", "wo", "wgu", "wdown")  # per layer, plus lm_head
 VSR_MAX_CANDS = 256
 
 EXPORTS = ["vsr_workspace_size", "vsr_create", "vsr_load_weights", "vsr_prefill",
-           "vsr_score", "vsr_reliability", "vsr_draft", "vsr_align_select", "vsr_weights_to_f16",
+           "vsr_score", "vsr_verify", "vsr_reliability", "vsr_draft", "vsr_align_select", "vsr_weights_to_f16",
            "vsr_keyframes", "vsr_retrieve_workspace_size", "vsr_retrieve", "vsr_last_error",
            "vsr_destroy", "vsr_profile_enable", "vsr_profile_read"]
 
@@ -27,14 +27,14 @@ VSR_SELECT_TWO_STAGE, VSR_SELECT_ADDITION, VSR_SELECT_INVERT = 0, 1, 2
 SELECT_STRATEGIES = {"two_stage": VSR_SELECT_TWO_STAGE, "addition": VSR_SELECT_ADDITION,
                      "invert": VSR_SELECT_INVERT}
 
-VSR_STAGE_KINDS = 15
-VSR_STAGES = 3 * VSR_STAGE_KINDS
+VSR_STAGE_KINDS = 16
+VSR_STAGES = 4 * VSR_STAGE_KINDS
 VSR_PROFILE_ALL = (1 << VSR_STAGE_KINDS) - 1
 STAGE_KINDS = ["embed", "rmsnorm", "qkv_rope", "attention", "attn_merge", "o_proj",
                "gate_up_swiglu", "down_proj", "lm_inputs", "lm_head_lse", "lse_gather",
-               "sum_argmax", "row_tables", "copy", "tail_proj"]
+               "sum_argmax", "row_tables", "copy", "tail_proj", "cand_attention"]
 STAGE_NAMES = ([f"prefill.{k}" for k in STAGE_KINDS] + [f"score.{k}" for k in STAGE_KINDS]
-               + [f"draft.{k}" for k in STAGE_KINDS])
+               + [f"draft.{k}" for k in STAGE_KINDS] + [f"verify.{k}" for k in STAGE_KINDS])
 
 
 class VsrConfig(ctypes.Structure):
@@ -89,6 +89,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                               ctypes.POINTER(ctypes.c_int32), ctypes.c_int32, ctypes.c_int32,
                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     lib.vsr_score.restype = ctypes.c_int
+    lib.vsr_verify.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                               ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                               ctypes.POINTER(ctypes.c_int32), ctypes.c_int32, ctypes.c_int32,
+                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.vsr_verify.restype = ctypes.c_int
     lib.vsr_reliability.argtypes = [ctypes.c_void_p, ctypes.c_void_p,
                                     ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
                                     ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -240,6 +245,24 @@ class Verifier:
         lp, sc, am = out
         self._check(self.lib.vsr_score(self.h, _ptr(cand_ids), lens, M, cmax, _ptr(lp),
                                        _ptr(sc), _ptr(am)))
+        return lp, sc, am
+
+    def verify(self, visual, ids, cand_ids, cand_len: Sequence[int], out=None):
+        """prefill(visual, ids) and score(cand_ids, cand_len) as one fused
+        pass; same arguments and outputs, and the prefix stays current."""
+        torch = self._torch
+        nv = 0 if visual is None else int(visual.shape[0])
+        nt = 0 if ids is None else int(ids.shape[0])
+        self._keep = (visual, ids)
+        M, cmax = int(cand_ids.shape[0]), int(cand_ids.shape[1])
+        lens = (ctypes.c_int32 * M)(*[int(x) for x in cand_len])
+        if out is None:
+            out = (torch.empty((M, cmax), dtype=torch.float32, device=self.device),
+                   torch.empty(M, dtype=torch.float32, device=self.device),
+                   torch.empty(1, dtype=torch.int32, device=self.device))
+        lp, sc, am = out
+        self._check(self.lib.vsr_verify(self.h, _ptr(visual), nv, _ptr(ids), nt, _ptr(cand_ids),
+                                        lens, M, cmax, _ptr(lp), _ptr(sc), _ptr(am)))
         return lp, sc, am
 
     def reliability(self, branch_ids, branch_len: Sequence[int], yes_id: int, no_id: int,

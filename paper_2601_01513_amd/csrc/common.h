@@ -158,6 +158,14 @@ struct QKVOut {
   T *q_lo = nullptr, *k_lo = nullptr, *vt_lo = nullptr;
   // Cache position of each row's key / value (NULL: the row index).
   const int32_t *cache_row = nullptr;
+  // Prefix and candidate rows in one projection: rows >= split go to a second
+  // pair of caches (k2 / vt2 and their remainder planes, capacity kv_npos2) at
+  // cache position row - split, rotated at position row_pos2[row - split];
+  // rows below split as above. split = INT32_MAX: one destination.
+  int split = 0x7fffffff;
+  T *k2 = nullptr, *vt2 = nullptr, *k2_lo = nullptr, *vt2_lo = nullptr;
+  int kv_npos2 = 0;
+  const int32_t *row_pos2 = nullptr;
 };
 
 // Stores one rotate-half pair (dims d and d + 64 of head slot `slot` of the
@@ -167,8 +175,10 @@ struct QKVOut {
 // where the remainder planes are given. head_dim 128.
 __device__ __forceinline__ void qkv_store(const QKVOut<f16> &o, int n_heads, int n_kv, int slot,
                                           int row, int d, float x1, float x2) {
+  const bool second = row >= o.split;  // a candidate row of a fused pass
+  const int row2 = row - o.split;
   if (slot < n_heads + n_kv) {
-    const int pos = o.row_pos ? o.row_pos[row] : row;
+    const int pos = second ? o.row_pos2[row2] : o.row_pos ? o.row_pos[row] : row;
     const float2 cs = o.rope[(long)pos * 64 + d];
     const float y1 = x1 * cs.x - x2 * cs.y, y2 = x2 * cs.x + x1 * cs.y;
     x1 = y1;
@@ -185,27 +195,31 @@ __device__ __forceinline__ void qkv_store(const QKVOut<f16> &o, int n_heads, int
       o.q_lo[off + d] = l1;
       o.q_lo[off + d + 64] = l2;
     }
-  } else if (slot < n_heads + n_kv) {
-    const int crow = o.cache_row ? o.cache_row[row] : row;
-    const long off = ((long)(slot - n_heads) * o.kv_npos + crow) * 128;
-    o.k[off + d] = h1;
-    o.k[off + d + 64] = h2;
-    if (o.k_lo) {
-      o.k_lo[off + d] = l1;
-      o.k_lo[off + d + 64] = l2;
-    }
   } else {
-    // Values go to the Vt cache at the attention kernel's interleaved
-    // position: within each aligned group of 16, quarters 1 and 2 swap.
-    const long base = (long)(slot - n_heads - n_kv) * 128 * o.kv_npos;
-    const int crow = o.cache_row ? o.cache_row[row] : row;
-    const int pp = (crow & ~12) | ((crow & 4) << 1) | ((crow & 8) >> 1);
-    const long o1 = base + (long)d * o.kv_npos + pp, o2 = base + (long)(d + 64) * o.kv_npos + pp;
-    o.vt[o1] = h1;
-    o.vt[o2] = h2;
-    if (o.vt_lo) {
-      o.vt_lo[o1] = l1;
-      o.vt_lo[o2] = l2;
+    const int crow = second ? row2 : o.cache_row ? o.cache_row[row] : row;
+    const int npos = second ? o.kv_npos2 : o.kv_npos;
+    if (slot < n_heads + n_kv) {
+      f16 *k = second ? o.k2 : o.k, *k_lo = second ? o.k2_lo : o.k_lo;
+      const long off = ((long)(slot - n_heads) * npos + crow) * 128;
+      k[off + d] = h1;
+      k[off + d + 64] = h2;
+      if (k_lo) {
+        k_lo[off + d] = l1;
+        k_lo[off + d + 64] = l2;
+      }
+    } else {
+      // Values go to the Vt cache at the attention kernel's interleaved
+      // position: within each aligned group of 16, quarters 1 and 2 swap.
+      f16 *vt = second ? o.vt2 : o.vt, *vt_lo = second ? o.vt2_lo : o.vt_lo;
+      const long base = (long)(slot - n_heads - n_kv) * 128 * npos;
+      const int pp = (crow & ~12) | ((crow & 4) << 1) | ((crow & 8) >> 1);
+      const long o1 = base + (long)d * npos + pp, o2 = base + (long)(d + 64) * npos + pp;
+      vt[o1] = h1;
+      vt[o2] = h2;
+      if (vt_lo) {
+        vt_lo[o1] = l1;
+        vt_lo[o2] = l2;
+      }
     }
   }
 }

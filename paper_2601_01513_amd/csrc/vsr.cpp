@@ -89,7 +89,9 @@ Plan make_plan(const vsr_config &c) {
   p.max_t = c.max_cands * c.max_cand_len;
   p.bk_npos = (int)align_up(p.max_t, 64);
   p.lm_rows = std::max(p.max_t, 2 * c.max_cands);
-  p.rows_max = std::max(c.max_prefix, p.lm_rows);
+  // MFMA contexts run the prefix and the candidate rows of vsr_verify as one
+  // set of rows.
+  p.rows_max = std::max(c.max_prefix + (c.dtype == VSR_BF16 ? p.max_t : 0), p.lm_rows);
   p.dec_S = c.max_new > 0 ? c.max_cand_len + c.max_new : 0;
   p.dec_npos = c.max_new > 0 ? (int)align_up((size_t)c.max_cands * p.dec_S, 64) : 0;
   p.rope_npos = p.kv_npos + c.max_cand_len + c.max_new;
@@ -203,7 +205,7 @@ struct vsr_ctx {
     hipEvent_t a, b;
   };
   int prof = 0;  // bitmask of the stage kinds being timed
-  int phase = 0;  // 0 prefix pass, 1 candidate pass, 2 draft pass
+  int phase = 0;  // 0 prefix pass, 1 candidate pass, 2 draft pass, 3 fused verify pass
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
   hipEvent_t event() {
@@ -251,9 +253,9 @@ struct vsr_ctx {
 
 enum StageKind {
   K_EMBED = 0, K_NORM, K_QKV, K_ATTN, K_MERGE, K_OPROJ, K_GATEUP, K_DOWN, K_LMIN, K_LMHEAD,
-  K_LSE, K_SELECT, K_ROWS, K_COPY, K_TAIL
+  K_LSE, K_SELECT, K_ROWS, K_COPY, K_TAIL, K_CATTN
 };
-static_assert(K_TAIL + 1 == VSR_STAGE_KINDS, "stage kinds");
+static_assert(K_CATTN + 1 == VSR_STAGE_KINDS, "stage kinds");
 
 // Launch the expression as stage `kind`; with timing on, bracket it with events.
 #define STAGE(ctx, kind, name, ...)                                                     \
@@ -374,7 +376,12 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
   // mode 2 (draft): branch keys/values go to the persistent draft cache at
   // the rows' cache positions; queries see the prefix and their branch up to
   // their own position.
+  // mode 3 (fused verify pass, MFMA path): rows 0 .. P-1 are the prefix (mode
+  // 0 for them), rows P .. rows-1 the candidates (mode 1): one set of rows
+  // through every projection, two attention launches per layer.
   const bool draft = mode == 2;
+  const bool fused = mode == 3;
+  const int P = c->P;
   const int32_t *cache_row = draft ? c->at<int32_t>(p.cache_row) : nullptr;
   hipStream_t s = c->stream;
   // Few-row products stream their weights (skinny kernels); their residual
@@ -400,11 +407,18 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
     QKVOut<TA> qo;
     qo.q = q;
     qo.rope = c->at<float2>(p.rope);
-    if (mode == 0) {
+    if (mode == 0 || fused) {
       qo.k = kc;
       qo.vt = vtc;
       qo.kv_npos = p.kv_npos;
       qo.row_pos = nullptr;
+      if (fused) {
+        qo.split = P;
+        qo.k2 = c->at<TA>(p.bk);
+        qo.vt2 = c->at<TA>(p.bvt);
+        qo.kv_npos2 = p.bk_npos;
+        qo.row_pos2 = c->at<int32_t>(p.row_pos);
+      }
     } else if (!draft) {
       qo.k = c->at<TA>(p.bk);
       qo.vt = c->at<TA>(p.bvt);
@@ -424,8 +438,12 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
     const int bk_npos = draft ? p.dec_npos : p.bk_npos;
     if (precise) {
       qo.q_lo = c->at<TA>(p.q_lo);
-      qo.k_lo = mode == 0 ? c->at<TA>(p.kc_lo) + l * layer_cache : bk_lo;
-      qo.vt_lo = mode == 0 ? c->at<TA>(p.vtc_lo) + l * layer_cache : bvt_lo;
+      qo.k_lo = mode == 0 || fused ? c->at<TA>(p.kc_lo) + l * layer_cache : bk_lo;
+      qo.vt_lo = mode == 0 || fused ? c->at<TA>(p.vtc_lo) + l * layer_cache : bvt_lo;
+      if (fused) {
+        qo.k2_lo = bk_lo;
+        qo.vt2_lo = bvt_lo;
+      }
     }
     if constexpr (kMfma) {
       if (rows <= kSkinnyMaxRows)
@@ -441,8 +459,10 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
     // The prefix's last layer only feeds the last prefix row (the hidden state
     // that predicts candidate token 0): its keys/values are needed for every
     // row, its attention output, projections and FFN for row P-1 only.
-    const bool tail = mode == 0 && l == cf.n_layers - 1;
-    const int r0 = tail ? rows - 1 : 0, nr = tail ? 1 : rows;
+    // In the fused pass the same holds for the prefix rows: the last layer
+    // takes rows P-1 .. rows-1 (the last prefix row and the candidates).
+    const bool tail = (mode == 0 || fused) && l == cf.n_layers - 1;
+    const int r0 = tail ? (fused ? P - 1 : rows - 1) : 0, nr = rows - r0;
     if constexpr (kMfma) {
       AttnArgs a{};
       a.t0 = r0;
@@ -472,7 +492,23 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
         a.bk_lo = bk_lo;
         a.bvt_lo = bvt_lo;
       }
-      if (mode == 0) {
+      if (fused) {
+        // Prefix rows (causal over the prefix cache), then the candidate rows
+        // (their queries, outputs and remainder planes start at row P).
+        AttnArgs ap = a;
+        ap.T = P;
+        ap.t0 = tail ? P - 1 : 0;
+        ap.q_pos = nullptr;
+        STAGE(c, K_ATTN, "prefill attention", attn_prefill(ap, precise, s));
+        const size_t qoff = (size_t)P * Hq * hd;
+        a.T = rows - P;
+        a.t0 = 0;
+        a.q = q + qoff;
+        if (precise) a.q_lo = c->at<f16>(p.q_lo) + qoff;
+        a.out = attn + qoff * sp;
+        STAGE(c, K_CATTN, "candidate attention", attn_cascade(a, precise, s));
+        STAGE(c, K_MERGE, "cascade merge", attn_merge(a, s));
+      } else if (mode == 0) {
         STAGE(c, K_ATTN, "prefill attention", attn_prefill(a, precise, s));
       } else {
         STAGE(c, K_ATTN, "cascade attention", attn_cascade(a, precise, s));
@@ -635,6 +671,53 @@ int score_impl(vsr_ctx *c, const Branches &br, const int32_t *cand_ids, float *l
   return VSR_OK;
 }
 
+// Prefix and candidates in one pass (MFMA contexts): the prefix rows and the
+// candidate rows go through every projection together (one GEMM launch per
+// projection for both); per layer, the prefix rows attend causally over the
+// prefix cache and the candidate rows over the prefix + their own keys. The
+// prefix cache is left filled, as after a prefill.
+template <typename TW, typename TA>
+int verify_impl(vsr_ctx *c, const void *visual, int nv, const int32_t *ids, int nt,
+                const Branches &br, const int32_t *cand_ids, float *logprobs, float *scores,
+                int32_t *argmax) {
+  const vsr_config &cf = c->cfg;
+  const Plan &p = c->plan;
+  const int P = nv + nt, T_rows = br.cu[br.M];
+  hipStream_t s = c->stream;
+  float *x = c->at<float>(p.x);
+  STAGE(c, K_EMBED, "prefix embedding",
+        launch_embed_prefix<TW>(static_cast<const TW *>(visual), nv, ids, nt,
+                                static_cast<const TW *>(c->embed), cf.vocab, cf.d_model, x, s));
+  c->P = P;
+  int32_t *row_lo = c->at<int32_t>(p.row_lo), *row_pos = c->at<int32_t>(p.row_pos);
+  int32_t *lm_tgt = c->at<int32_t>(p.lm_tgt);
+  float *xc = x + (size_t)P * cf.d_model;  // the candidate rows
+  STAGE(c, K_ROWS, "row tables",
+        launch_row_tables(br, P, cand_ids, cf.vocab, row_lo, row_pos, lm_tgt, s));
+  STAGE(c, K_EMBED, "candidate embedding",
+        launch_embed_rows<TW>(lm_tgt, T_rows, static_cast<const TW *>(c->embed), cf.d_model, xc,
+                              s));
+  const Split split = cascade_split(T_rows, P + br.cmax, cf.n_heads, cf.n_kv_heads);
+  int rc = run_layers<TW, TA>(c, P + T_rows, 3, split);
+  if (rc) return rc;
+  STAGE(c, K_COPY, "last prefix row",
+        hipMemcpyAsync(c->at<float>(p.h_last), x + (size_t)(P - 1) * cf.d_model,
+                       (size_t)cf.d_model * 4, hipMemcpyDeviceToDevice, s));
+  c->prefilled = true;
+  STAGE(c, K_LMIN, "lm inputs",
+        launch_lm_inputs<TW, TA>(xc, c->at<float>(p.h_last), row_lo,
+                                 static_cast<const TW *>(c->final_norm), T_rows, cf.d_model,
+                                 cf.rms_eps, c->at<TA>(p.xn), s));
+  int lm_chunks = 1;
+  rc = lm_head<TW, TA>(c, T_rows, &lm_chunks);
+  if (rc) return rc;
+  STAGE(c, K_LSE, "lse gather",
+        launch_lse_gather(br, c->at<float2>(p.lm_part), lm_chunks, c->at<float>(p.tgt),
+                          logprobs, s));
+  STAGE(c, K_SELECT, "reduce/select", launch_reduce_select(br, logprobs, scores, argmax, s));
+  return VSR_OK;
+}
+
 template <typename TW, typename TA>
 int reliability_impl(vsr_ctx *c, const Branches &br, const int32_t *ids, int yes_id, int no_id,
                      float delta, float *lp_yes_no, float *rel, int32_t *keep) {
@@ -784,6 +867,58 @@ extern "C" int vsr_score(vsr_ctx *ctx, const int32_t *cand_ids, const int32_t *c
   }
   const int rc = set_device(ctx);
   if (rc) return rc;
+  ctx->phase = 1;
+  return ctx->cfg.dtype == VSR_BF16
+             ? score_impl<bf16, f16>(ctx, br, cand_ids, logprobs, scores, argmax)
+             : score_impl<float, float>(ctx, br, cand_ids, logprobs, scores, argmax);
+}
+
+extern "C" int vsr_verify(vsr_ctx *ctx, const void *visual, int32_t n_visual,
+                          const int32_t *ids, int32_t n_text, const int32_t *cand_ids,
+                          const int32_t *cand_len, int32_t M, int32_t Cmax, float *logprobs,
+                          float *scores, int32_t *argmax) {
+  if (!ctx) return VSR_EINVAL;
+  if (!ctx->have_weights) return ctx->fail(VSR_ESTATE, "verify before vsr_load_weights");
+  if (n_visual < 0 || n_text < 0) return ctx->fail(VSR_EINVAL, "negative prefix length");
+  const long long P = (long long)n_visual + n_text;
+  if (P < 1) return ctx->fail(VSR_EINVAL, "empty prefix (n_visual + n_text must be >= 1)");
+  if (P > ctx->cfg.max_prefix)
+    return ctx->fail(VSR_ERANGE, "prefix length %lld exceeds max_prefix %d", P,
+                     ctx->cfg.max_prefix);
+  if (n_visual > 0 && !visual) return ctx->fail(VSR_EINVAL, "visual is NULL");
+  if (n_text > 0 && !ids) return ctx->fail(VSR_EINVAL, "ids is NULL");
+  if (M < 1 || Cmax < 1) return ctx->fail(VSR_EINVAL, "M and Cmax must be >= 1");
+  if (M > ctx->cfg.max_cands)
+    return ctx->fail(VSR_ERANGE, "M = %d exceeds max_cands %d", M, ctx->cfg.max_cands);
+  if (Cmax > ctx->cfg.max_cand_len)
+    return ctx->fail(VSR_ERANGE, "Cmax = %d exceeds max_cand_len %d", Cmax,
+                     ctx->cfg.max_cand_len);
+  if (!cand_ids || !cand_len || !logprobs || !scores || !argmax)
+    return ctx->fail(VSR_EINVAL, "verify: NULL argument");
+  Branches br{};
+  br.M = M;
+  br.cmax = Cmax;
+  br.cu[0] = 0;
+  for (int m = 0; m < M; ++m) {
+    if (cand_len[m] < 0 || cand_len[m] > Cmax)
+      return ctx->fail(VSR_EINVAL, "cand_len[%d] = %d outside [0, Cmax]", m, cand_len[m]);
+    br.cu[m + 1] = br.cu[m] + cand_len[m];
+  }
+  int rc = set_device(ctx);
+  if (rc) return rc;
+  ctx->prefilled = false;
+  if (ctx->cfg.dtype == VSR_BF16 && br.cu[M] > 0) {
+    ctx->phase = 3;
+    return verify_impl<bf16, f16>(ctx, visual, n_visual, ids, n_text, br, cand_ids, logprobs,
+                                  scores, argmax);
+  }
+  // fp32 contexts, or no candidate tokens: the two passes one after the other.
+  ctx->phase = 0;
+  rc = ctx->cfg.dtype == VSR_BF16
+           ? prefill_impl<bf16, f16>(ctx, visual, n_visual, ids, n_text)
+           : prefill_impl<float, float>(ctx, visual, n_visual, ids, n_text);
+  if (rc) return rc;
+  ctx->prefilled = true;
   ctx->phase = 1;
   return ctx->cfg.dtype == VSR_BF16
              ? score_impl<bf16, f16>(ctx, br, cand_ids, logprobs, scores, argmax)

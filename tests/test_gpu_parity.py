@@ -54,6 +54,21 @@ def run_gpu(wl, cand_ids=None, cand_len=None, verifier=None, split_layers=None):
     return lp.cpu().numpy(), sc.cpu().numpy(), int(am.cpu()[0]), v
 
 
+def run_gpu_verify(wl, cand_ids=None, cand_len=None, verifier=None, split_layers=None):
+    """The same pass through vsr_verify (prefix and candidates fused)."""
+    torch = _torch()
+    from paper_2601_01513_amd.binding import Verifier
+    cfg = wl.cfg
+    v = verifier or Verifier(cfg, wl.weights, device="cuda", split_layers=split_layers)
+    ids = torch.tensor(wl.prefix_ids, dtype=torch.int32, device="cuda") if cfg.n_text else None
+    vis = wl.visual if cfg.n_visual else None
+    cids = wl.cand_ids if cand_ids is None else cand_ids
+    lens = wl.cand_len if cand_len is None else cand_len
+    lp, sc, am = v.verify(vis, ids, torch.tensor(cids, dtype=torch.int32, device="cuda"), lens)
+    torch.cuda.synchronize()
+    return lp.cpu().numpy(), sc.cpu().numpy(), int(am.cpu()[0]), v
+
+
 def run_oracle(wl, dtype=np.float64, cand_ids=None, cand_len=None, cands=None):
     hw = W.host_weights(wl.weights, lazy=True)
     vis = W.to_host_f32(wl.visual)
@@ -196,11 +211,14 @@ def test_full_width_two_layers(cfg):
     wl = _case(cfg2, 0, split=1)
     t0 = time.time()
     gpu = run_gpu(wl, split_layers=1)
+    fused = run_gpu_verify(wl, verifier=gpu[3])
     _say(f"  gpu done in {time.time() - t0:.1f}s, running oracle (fp32)")
     t0 = time.time()
     ora = run_oracle(wl, dtype=np.float32)
     _say(f"  oracle done in {time.time() - t0:.1f}s")
     check(cfg2, gpu, ora, wl.cand_len)
+    _say("  fused verify pass:")
+    check(cfg2, fused, ora, wl.cand_len)
 
 
 def check_sampled(cfg, gpu, ora, lens, cands):
@@ -223,13 +241,17 @@ def check_sampled(cfg, gpu, ora, lens, cands):
 
 @pytest.mark.timeout(900)
 def test_full_depth_7b_sampled():
-    """The 7B-class workload at full depth and size; the oracle (float32)
-    scores two of the eight candidates."""
+    """The 7B-class workload at full depth and size, through vsr_prefill +
+    vsr_score and through vsr_verify; the oracle (float32) scores two of the
+    eight candidates."""
     wl = _case(W.B7, 1)
     gpu = run_gpu(wl)
+    fused = run_gpu_verify(wl, verifier=gpu[3])
     cands = [0, 5]
     ora = run_oracle(wl, dtype=np.float32, cands=cands)
     check_sampled(wl.cfg, gpu, ora, wl.cand_len, cands)
+    _say("  fused verify pass (the benchmark's pass):")
+    check_sampled(wl.cfg, fused, ora, wl.cand_len, cands)
 
 
 @pytest.mark.timeout(900)
