@@ -30,13 +30,17 @@ def _rows(path):
 def _short(name: str) -> str:
     m = re.search(r"(k_[a-z_0-9]+)", name)
     base = m.group(1) if m else name[:40]
-    precise = "ELb1E" in name or ", true>" in name
+    # k_attn<mode, precise, ...>: the first bool is the precise variant.
+    ma = re.search(r"k_attnILi\dELb(\d)", name) or re.search(r"k_attn<\d, (true|false)", name)
+    precise = bool(ma) and ma.group(1) in ("1", "true")
     if "k_attnILi0" in name or "k_attn<0" in name:
         base = "k_attn<0> (prefill" + (", precise)" if precise else ")")
     elif "k_attnILi1" in name or "k_attn<1" in name:
         base = "k_attn<1> (cascade" + (", precise)" if precise else ")")
     elif "k_attnILi2" in name or "k_attn<2" in name:
-        base = "k_attn<2> (draft" + (", precise)" if precise else ")")
+        dec = "k_attnILi2ELb0ELb1E" in name or "k_attn<2, false, true>" in name
+        base = "k_attn<2> (draft" + (", precise)" if precise else
+                                     ", decode blocks)" if dec else ")")
     elif base == "k_skinny":
         # k_skinny<rows per group, A split, bf16 weights, greedy LM head>
         m = re.search(r"k_skinnyILi(\d+)ELi(\d+)ELb(\d)ELb(\d)E", name)
