@@ -24,8 +24,8 @@ thread_local std::string g_create_error;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Key split of the candidate pass: enough blocks to cover the chip, at least
-// 256 of a block's `keys` (prefix + branch keys it walks) per chunk; a pass
+// Key split of the candidate pass: at most one round of blocks on the chip,
+// at least 256 of a block's `keys` (prefix + branch keys it walks) per chunk; a pass
 // with one query tile per KV head (decode steps) is latency-bound and takes
 // chunks of one 64-key tile. At most 64 chunks (the merge's limit).
 struct Split {
@@ -35,7 +35,9 @@ Split cascade_split(int T, int keys, int n_heads, int n_kv) {
   const int G = n_heads / n_kv;
   const int qt = attn_query_tile();
   const int qtiles = (T * G + qt - 1) / qt * n_kv;
-  int n = std::max(1, (512 + qtiles - 1) / qtiles);
+  // One round of the 256 CUs (a block per CU): more chunks add a round, and
+  // partials for the merge to read, sooner than they shorten the blocks.
+  int n = std::max(1, 256 / qtiles);
   n = std::min(n, std::max(1, keys / (qtiles == n_kv ? 64 : 256)));
   return {std::min(n, 64)};
 }
