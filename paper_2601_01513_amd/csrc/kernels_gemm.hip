@@ -718,8 +718,12 @@ hipError_t gemm_swiglu(const f16 *A, const void *W, bool w_f16, int rows, int F,
                        int asplit, f16 *h, float *part, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
-  const Launch ln = plan_launch((rows + TL::BM - 1) / TL::BM, (F + 127) / 128, 8,
-                                K / BK * asplit);
+  // Row-tile groups of at most 9, evenly sized (16 row tiles: 2 x 8; 18: 2 x
+  // 9): measured 1.6% faster than groups of 8 on 4608 rows, where the last
+  // group of 2 row tiles shares its operand panels poorly.
+  const int nm = (rows + TL::BM - 1) / TL::BM;
+  const int ng = (nm + 8) / 9;
+  const Launch ln = plan_launch(nm, (F + 127) / 128, (nm + ng - 1) / ng, K / BK * asplit);
   VSR_WLAUNCH(k_gemm_swiglu, ln.blocks(), A, W16, rows, F, K, asplit, ln, h, part);
   if (ln.ntail > 0)
     k_reduce_swiglu<<<ln.ntail * 128, 256, 0, s>>>(part, ln, rows, F, asplit, h);
