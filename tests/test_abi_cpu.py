@@ -73,7 +73,22 @@ def test_null_context_calls_fail_cleanly():
     assert lib.vsr_prefill(None, None, 0, None, 1) == B.VSR_EINVAL
     lens = (ctypes.c_int32 * 1)(1)
     assert lib.vsr_score(None, None, lens, 1, 1, None, None, None) == B.VSR_EINVAL
+    assert lib.vsr_verify(None, None, 0, None, 1, None, lens, 1, 1, None, None, None) == \
+        B.VSR_EINVAL
     lib.vsr_destroy(None)
+
+
+def test_workspace_holds_the_fused_rows():
+    """bf16 contexts size their activation rows for vsr_verify (prefix rows +
+    candidate rows in one pass): more candidate tokens, more workspace, even
+    where the prefix is the larger of the two; fp32 contexts do not fuse."""
+    _lib()
+    base = B.make_config(W.B7)
+    more = B.make_config(W.B7, max_cand_len=W.B7.cand_len + 64)
+    assert B.workspace_size(more) > B.workspace_size(base)
+    f32 = B.make_config(W.TINY_F32)
+    f32_more = B.make_config(W.TINY_F32, max_prefix=W.TINY_F32.n_prefix + 64)
+    assert B.workspace_size(f32_more) > B.workspace_size(f32)
 
 
 def test_workspace_grows_with_the_maxima():
