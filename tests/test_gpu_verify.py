@@ -55,6 +55,15 @@ def test_verify_agrees_with_prefill_and_score():
     assert d <= 2e-2
 
 
+def test_verify_is_deterministic():
+    """Fixed-order reductions everywhere: two passes on the same inputs are
+    bitwise equal (GQA-7, 8 x 64 ragged candidates, one precise layer)."""
+    wl = _case(GQA7_BF16, 2, split=1)
+    a = run_gpu_verify(wl, split_layers=1)
+    b = run_gpu_verify(wl, verifier=a[3])
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]) and a[2] == b[2]
+
+
 def test_verify_few_rows():
     """Prefix + candidate rows <= 32: every projection on the few-row kernels,
     which route the candidate rows' keys and values to the branch cache."""
