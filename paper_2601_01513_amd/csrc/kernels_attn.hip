@@ -18,13 +18,17 @@
 // lane, and the Vt cache stores positions in the matching order (within each
 // aligned group of 16 positions the middle two quarters are swapped), so a
 // lane's V^T operand is one 16-byte LDS read. Softmax runs online in fp32:
-// the running maximum is kept on the raw scores and the scale folds into the
-// exponent, exp2(s * c - m * c) with c = log2(e) / sqrt(hd), one FMA per
-// score; operands (queries, keys, values, probabilities) are fp16.
+// the reference maximum is kept on the raw scores and the scale folds into
+// the exponent, exp2(s * c - m * c) with c = log2(e) / sqrt(hd), one FMA per
+// score; the reference moves (and the output is rescaled) only when a tile's
+// maximum exceeds it by a factor 2^8 after scaling. A query's 64 keys of a
+// tile sit in two lanes (l, l ^ 32), combined by v_permlane32_swap; operands
+// (queries, keys, values, probabilities) are fp16.
 //
-// The candidate pass may split a block's keys (its prefix tiles, then its
+// The candidate and draft passes may split a block's keys (prefix tiles, then
 // branch tiles) into chunks (more blocks on the chip); each chunk writes (max,
-// sum, unnormalised output) partials and attn_merge combines them.
+// sum, unnormalised output) partials and attn_merge combines them. Decode
+// steps (at most 32 stacked query rows per KV head) run one-wave blocks.
 //
 // Precise variant (the leading layers of a deep model, where rounding is
 // amplified most): queries, keys and values arrive as fp16 value + fp16
