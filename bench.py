@@ -357,7 +357,15 @@ def main():
                    "vocab": cfg.vocab, "prefix": cfg.n_prefix, "visual_rows": cfg.n_visual,
                    "candidates": M, "cand_len": cmax, "tokens_scored": tokens},
         "breakdown": {"kernel_ms": round(total, 3), "gemm_ms": round(gemm, 3),
-                      "attention_ms": round(attn, 3)},
+                      "attention_ms": round(attn, 3),
+                      # every stage with algorithmic FLOPs: ms per pass, TF/s
+                      # and fraction of the bf16 MFMA peak (untimed profiled pass)
+                      "stages": {k.split(".", 1)[1]: {
+                          "ms": round(per_step[k], 3),
+                          "tflops": round(flops[k] / (per_step[k] * 1e-3) / 1e12, 1),
+                          "frac": round(flops[k] / (per_step[k] * 1e-3) / 1e12
+                                        / PEAK_BF16_TFLOPS, 4)}
+                          for k in sorted(flops) if per_step.get(k, 0.0) > 0}},
         "roofline": roofline,
     }
     if not args.no_next_rows:
