@@ -300,7 +300,8 @@ struct AttnArgs {
   int t0;               // first query token
   int P;                // mode 1: prefix length
   int n_heads, n_kv;
-  int nchunks;          // mode 1: key split of each block (partials when > 1)
+  int nchunks;          // key split of each block (partials when > 1; the
+                        // prefill only with t0 = 0)
   f16 *out;             // [T][out_split][n_heads][hd] when nchunks == 1 (or merged)
   int out_split;        // 2: [hi | lo] rows for a split output projection
   float *part_acc;      // [nchunks][n_kv][T*G][hd]
@@ -317,6 +318,10 @@ struct AttnArgs {
 int attn_query_tile();  // stacked query rows per attention block
 // precise = true: q/k/v and the probabilities are carried as fp16 value +
 // remainder (three MFMAs per product); needs the *_lo planes of AttnArgs.
+// Prefill: with a.nchunks > 1 (only for t0 = 0) the keys of each block are
+// split into chunks that write partials, and attn_merge(a) writes the output;
+// prefill_chunks gives the split for T query tokens.
+int prefill_chunks(int T, int n_heads, int n_kv);
 hipError_t attn_prefill(const AttnArgs &a, bool precise, hipStream_t s);
 hipError_t attn_cascade(const AttnArgs &a, bool precise, hipStream_t s);
 hipError_t attn_merge(const AttnArgs &a, hipStream_t s);

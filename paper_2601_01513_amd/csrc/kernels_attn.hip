@@ -36,6 +36,8 @@
 // takes three MFMAs (hi.hi + hi.lo + lo.hi), which leaves an error of the
 // order of fp32 rounding. Its blocks hold 128 query rows on 4 waves with the
 // queries in registers, so that the doubled key/value ring fits in LDS.
+#include <algorithm>
+
 #include "common.h"
 
 namespace vsr {
@@ -356,9 +358,13 @@ __global__ __launch_bounds__((Shape<PREC, DEC>::NT)) void k_attn(AttnArgs a) {
   const int chunk = blockIdx.z;
   const long koff = (long)kvh * a.kv_npos * HD, boff = (long)kvh * a.bk_npos * HD;
   if (MODE == 0) {
+    // Causal keys 0 .. tok_last; with nchunks > 1 (few blocks on the chip)
+    // chunk `chunk` takes an even share of the block's key tiles.
+    const int nt = (tok_last + KT) / KT;
+    const int kb = (int)((long)nt * chunk / a.nchunks) * KT;
+    const int ke = min(tok_last + 1, (int)((long)nt * (chunk + 1) / a.nchunks) * KT);
     Seg sg{a.k + koff, a.vt + koff, PREC ? a.k_lo + koff : nullptr,
-           PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.T, 0, tok_last + 1, SEG_CAUSAL,
-           tok_first};
+           PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.T, kb, ke, SEG_CAUSAL, tok_first};
     walk_segment<PREC, DEC>(sg, lds, L, scale_log2);
   } else if (MODE == 1) {
     // Candidate pass: chunks of whole prefix tiles (the last one short); the
@@ -400,7 +406,7 @@ __global__ __launch_bounds__((Shape<PREC, DEC>::NT)) void k_attn(AttnArgs a) {
   L.l = sum_halves(L.l);
   if (row >= TG) return;
   const int h = lane >> 5;
-  if (MODE == 0 || a.nchunks == 1) {
+  if (a.nchunks == 1) {
     const float inv = 1.f / L.l;
     f16 *op = a.out + ((long)(a.t0 + rowc / G) * a.out_split * a.n_heads + head) * HD;
     f16 *olo = op + (long)a.n_heads * HD;  // remainder half of a split row
@@ -502,7 +508,7 @@ hipError_t launch_attn(const AttnArgs &a, hipStream_t s) {
   using S = Shape<PREC, DEC>;
   const int G = a.n_heads / a.n_kv;
   const int nqt = ((a.T - a.t0) * G + S::QT - 1) / S::QT;
-  const dim3 grid = MODE == 0 ? dim3(nqt * a.n_kv) : dim3(nqt, a.n_kv, a.nchunks);
+  const dim3 grid = MODE == 0 ? dim3(nqt * a.n_kv, 1, a.nchunks) : dim3(nqt, a.n_kv, a.nchunks);
   k_attn<MODE, PREC, DEC><<<grid, S::NT, 0, s>>>(a);
   return hipGetLastError();
 }
@@ -511,8 +517,17 @@ hipError_t launch_attn(const AttnArgs &a, hipStream_t s) {
 
 int attn_query_tile() { return QT_FAST; }
 
+int prefill_chunks(int T, int n_heads, int n_kv) {
+  // Fewer than ~1.5 rounds of blocks (few KV heads, short prefixes): split
+  // each block's causal keys into up to 4 chunks, merged by attn_merge.
+  const int blocks = (T * (n_heads / n_kv) + QT_FAST - 1) / QT_FAST * n_kv;
+  return std::max(1, std::min(4, (384 + blocks - 1) / blocks));
+}
+
 hipError_t attn_prefill(const AttnArgs &a, bool precise, hipStream_t s) {
   if (a.T <= a.t0) return hipSuccess;
+  if (a.nchunks < 1 || a.nchunks > 64 || (a.nchunks > 1 && a.t0 != 0))
+    return hipErrorInvalidValue;
   if (precise && (!a.q_lo || !a.k_lo || !a.vt_lo)) return hipErrorInvalidValue;
   return precise ? launch_attn<0, true>(a, s) : launch_attn<0, false>(a, s);
 }

@@ -108,6 +108,17 @@ Plan make_plan(const vsr_config &c) {
       const Split s = cascade_split(T, keys_max, c.n_heads, c.n_kv_heads);
       if (s.nchunks > 1) part_rows = std::max(part_rows, (size_t)s.nchunks * T * G);
     }
+    // Prefill with split keys: the split only changes where the query-tile
+    // count does, so the largest prefix of each tile count bounds it.
+    const int qt = attn_query_tile();
+    for (int tiles = 1;; ++tiles) {
+      const int T = std::min(c.max_prefix, (tiles * qt) / G);
+      if (T >= 1) {
+        const int n = prefill_chunks(T, c.n_heads, c.n_kv_heads);
+        if (n > 1) part_rows = std::max(part_rows, (size_t)n * T * G);
+      }
+      if (T >= c.max_prefix) break;
+    }
   }
   // Split-K partials of the MFMA GEMMs: the largest need over every row count
   // (the split only changes where the 256-row tile count does).
@@ -501,7 +512,9 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
         ap.T = P;
         ap.t0 = tail ? P - 1 : 0;
         ap.q_pos = nullptr;
+        ap.nchunks = tail ? 1 : prefill_chunks(P, Hq, Hkv);
         STAGE(c, K_ATTN, "prefill attention", attn_prefill(ap, precise, s));
+        if (ap.nchunks > 1) STAGE(c, K_MERGE, "prefill merge", attn_merge(ap, s));
         const size_t qoff = (size_t)P * Hq * hd;
         a.T = rows - P;
         a.t0 = 0;
@@ -511,7 +524,9 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
         STAGE(c, K_CATTN, "candidate attention", attn_cascade(a, precise, s));
         STAGE(c, K_MERGE, "cascade merge", attn_merge(a, s));
       } else if (mode == 0) {
+        a.nchunks = tail ? 1 : prefill_chunks(rows, Hq, Hkv);
         STAGE(c, K_ATTN, "prefill attention", attn_prefill(a, precise, s));
+        if (a.nchunks > 1) STAGE(c, K_MERGE, "prefill merge", attn_merge(a, s));
       } else {
         STAGE(c, K_ATTN, "cascade attention", attn_cascade(a, precise, s));
         STAGE(c, K_MERGE, "cascade merge", attn_merge(a, s));
