@@ -74,6 +74,20 @@ def test_verify_few_rows():
     check(cfg, run_gpu_verify(wl), run_oracle(wl), wl.cand_len)
 
 
+@pytest.mark.parametrize("split", [0, 1])
+def test_verify_degenerate_sizes(split):
+    """A one-token prefix (P = 1: the last layer's prefix row is row 0), one
+    candidate of one token, and a single 256-row tile holding both."""
+    cfg = SMALL_BF16.replace(name="small bf16 P1 M1x1", n_prefix=1, n_visual=0, n_cands=1,
+                             cand_len=1)
+    wl = _case(cfg, 11, split=split)
+    check(cfg, run_gpu_verify(wl, split_layers=split), run_oracle(wl), wl.cand_len)
+    cfg = SMALL_BF16.replace(name="small bf16 P1 M3x70", n_prefix=1, n_visual=1, n_cands=3,
+                             cand_len=70)
+    wl = _case(cfg, 12, lens=[70, 1, 33], split=split)
+    check(cfg, run_gpu_verify(wl, split_layers=split), run_oracle(wl), wl.cand_len)
+
+
 def test_verify_fp32_and_no_candidate_tokens():
     """fp32 contexts and candidates of no tokens take the two passes in turn."""
     wl = _case(W.TINY_F32, 5)
