@@ -173,13 +173,24 @@ struct QKVOut {
 // position, then q to its rows, k to the key cache and v to the Vt cache (at
 // the attention kernel's interleaved position), each with its fp16 remainder
 // where the remainder planes are given. head_dim 128.
-__device__ __forceinline__ void qkv_store(const QKVOut<f16> &o, int n_heads, int n_kv, int slot,
-                                          int row, int d, float x1, float x2) {
+// Rotary position of row `row`.
+__device__ __forceinline__ int qkv_row_pos(const QKVOut<f16> &o, int row) {
+  // One load through a selected pointer (two loads into one register in
+  // different branches would make the second wait for the first).
+  const int32_t *p = row >= o.split ? o.row_pos2 + (row - o.split)
+                                    : o.row_pos ? o.row_pos + row : nullptr;
+  return p ? *p : row;
+}
+
+// qkv_store with the rotary-table entry of (row's position, d) given as cs
+// (unused for value slots), so that a caller can load the entries of many
+// rows before it stores any of them.
+__device__ __forceinline__ void qkv_store_cs(const QKVOut<f16> &o, int n_heads, int n_kv,
+                                             int slot, int row, int d, float x1, float x2,
+                                             float2 cs) {
   const bool second = row >= o.split;  // a candidate row of a fused pass
   const int row2 = row - o.split;
   if (slot < n_heads + n_kv) {
-    const int pos = second ? o.row_pos2[row2] : o.row_pos ? o.row_pos[row] : row;
-    const float2 cs = o.rope[(long)pos * 64 + d];
     const float y1 = x1 * cs.x - x2 * cs.y, y2 = x2 * cs.x + x1 * cs.y;
     x1 = y1;
     x2 = y2;
@@ -222,6 +233,13 @@ __device__ __forceinline__ void qkv_store(const QKVOut<f16> &o, int n_heads, int
       }
     }
   }
+}
+
+__device__ __forceinline__ void qkv_store(const QKVOut<f16> &o, int n_heads, int n_kv, int slot,
+                                          int row, int d, float x1, float x2) {
+  const float2 cs = slot < n_heads + n_kv ? o.rope[(long)qkv_row_pos(o, row) * 64 + d]
+                                          : make_float2(1.f, 0.f);
+  qkv_store_cs(o, n_heads, n_kv, slot, row, d, x1, x2, cs);
 }
 
 

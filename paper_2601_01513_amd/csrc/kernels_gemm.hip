@@ -530,17 +530,45 @@ __global__ __launch_bounds__(NT) void k_gemm_qkv(const f16 *__restrict__ A,
   const int wm = w / TL::WN, wn = w % TL::WN;
   const int slot = wk.tn * 2 + wn;
   if (slot >= nslots) return;
+  if (slot >= n_heads + n_kv) {  // values: no rotary
 #pragma unroll
-  for (int fm = 0; fm < TL::FM; ++fm)
+    for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + acc_row<TL>(wm, fm, r, lane);
+        if (row >= rows) continue;
+#pragma unroll
+        for (int fn = 0; fn < 2; ++fn)
+          qkv_store_cs(o, n_heads, n_kv, slot, row, fn * 32 + (lane & 31), acc[fm][fn][r],
+                       acc[fm][fn + 2][r], make_float2(1.f, 0.f));
+      }
+    return;
+  }
+  // Queries and keys: the positions and rotary-table entries of a block's 16
+  // rows are all loaded before any of its stores. The compiler cannot move a
+  // load above a store that may alias it, so loading them row by row waited
+  // out two memory round trips per row.
+#pragma unroll
+  for (int fm = 0; fm < TL::FM; ++fm) {
+    int pos[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      pos[r] = qkv_row_pos(o, min(m0 + acc_row<TL>(wm, fm, r, lane), rows - 1));
+    float2 cs[16][2];
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+#pragma unroll
+      for (int fn = 0; fn < 2; ++fn) cs[r][fn] = o.rope[(long)pos[r] * 64 + fn * 32 + (lane & 31)];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = m0 + acc_row<TL>(wm, fm, r, lane);
       if (row >= rows) continue;
 #pragma unroll
       for (int fn = 0; fn < 2; ++fn)
-        qkv_store(o, n_heads, n_kv, slot, row, fn * 32 + (lane & 31), acc[fm][fn][r],
-                  acc[fm][fn + 2][r]);
+        qkv_store_cs(o, n_heads, n_kv, slot, row, fn * 32 + (lane & 31), acc[fm][fn][r],
+                     acc[fm][fn + 2][r], cs[r][fn]);
     }
+  }
 }
 
 // Tail tiles: rotary + cache scatter from the summed partials. Block (tail
