@@ -253,14 +253,23 @@ __device__ __forceinline__ void walk_segment(const Seg &sg, u32x4 *lds, Lane &L,
   load_tile<PREC, DEC>(sg, sg.kbeg, lds);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  // The mask-free tiles come first (tile_clear holds for a prefix of the
+  // walk), so the two variants run in two loops: with one loop around both,
+  // the fast kernels spilled about 20 registers inside it.
   int stage = 0;
-  for (int kb = sg.kbeg; kb < sg.kend; kb += KT) {
+  int kb = sg.kbeg;
+  for (; kb < sg.kend && tile_clear(sg, kb); kb += KT) {
     u32x4 *cur = lds + stage * STAGE;
     if (kb + KT < sg.kend) load_tile<PREC, DEC>(sg, kb + KT, lds + (stage ^ 1) * STAGE);
-    if (tile_clear(sg, kb))
-      tile_step<false, PREC>(sg, kb, cur, L, scale_log2);
-    else
-      tile_step<true, PREC>(sg, kb, cur, L, scale_log2);
+    tile_step<false, PREC>(sg, kb, cur, L, scale_log2);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    stage ^= 1;
+  }
+  for (; kb < sg.kend; kb += KT) {
+    u32x4 *cur = lds + stage * STAGE;
+    if (kb + KT < sg.kend) load_tile<PREC, DEC>(sg, kb + KT, lds + (stage ^ 1) * STAGE);
+    tile_step<true, PREC>(sg, kb, cur, L, scale_log2);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     stage ^= 1;
@@ -281,16 +290,22 @@ __device__ __forceinline__ void walk_concat(const Seg &sp, const Seg &sb, int pr
   load_tile<PREC, DEC>(src(v0), key0(v0), lds);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  // Mask-free tiles first (whole prefix tiles), then the masked ones (a
+  // short last prefix tile, the branch tiles), as in walk_segment.
   int stage = 0;
-  for (int v = v0; v < v1; ++v) {
+  int v = v0;
+  for (; v < v1 && tile_clear(src(v), key0(v)); ++v) {
     u32x4 *cur = lds + stage * STAGE;
     if (v + 1 < v1) load_tile<PREC, DEC>(src(v + 1), key0(v + 1), lds + (stage ^ 1) * STAGE);
-    const Seg &sg = src(v);
-    const int kb = key0(v);
-    if (tile_clear(sg, kb))
-      tile_step<false, PREC>(sg, kb, cur, L, scale_log2);
-    else
-      tile_step<true, PREC>(sg, kb, cur, L, scale_log2);
+    tile_step<false, PREC>(src(v), key0(v), cur, L, scale_log2);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    stage ^= 1;
+  }
+  for (; v < v1; ++v) {
+    u32x4 *cur = lds + stage * STAGE;
+    if (v + 1 < v1) load_tile<PREC, DEC>(src(v + 1), key0(v + 1), lds + (stage ^ 1) * STAGE);
+    tile_step<true, PREC>(src(v), key0(v), cur, L, scale_log2);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     stage ^= 1;
