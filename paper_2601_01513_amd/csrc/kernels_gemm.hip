@@ -348,7 +348,12 @@ __device__ __forceinline__ float sum_partials(const float *part, const Launch &l
   return sum;
 }
 
-__device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.f + __expf(-g)) * u; }
+// silu(g) * u with the hardware reciprocal (about 1 ulp; the result is
+// rounded to fp16 next): an IEEE division here cost ten instructions per
+// output of the gate/up epilogue. Large negative g: exp(-g) = inf, rcp = 0.
+__device__ __forceinline__ float silu_mul(float g, float u) {
+  return g * __builtin_amdgcn_rcpf(1.f + __expf(-g)) * u;
+}
 
 // Activation store: fp16 value at base + col; with split = 2 also its fp16
 // remainder at base + n + col (row layout [hi | lo]).
