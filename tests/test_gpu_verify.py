@@ -6,7 +6,8 @@ argmax where the oracle's top-2 margin exceeds 0.1).
 
 Cases: small bf16 shapes with ragged and empty candidates and none, some or
 all layers precise; seven query heads per KV head; a pass small enough
-(prefix + candidate rows <= 32) for the few-row kernels; the fp32 and
+(prefix + candidate rows <= 32) for the few-row kernels; a one-row prefix
+with one one-token candidate, and with candidates inside one row tile; the fp32 and
 no-candidate-token fallbacks; the prefix state it leaves for later calls;
 argument errors. The full-size 7B-class pass (the benchmark's) is checked in
 test_gpu_parity.py next to the two-call pass.
