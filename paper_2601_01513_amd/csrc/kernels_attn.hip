@@ -9,8 +9,9 @@
 // once per candidate.
 //
 // A 512-thread block owns 256 stacked query rows (32 per wave, two waves per
-// SIMD) and walks 64-key tiles through a two-stage LDS ring filled by direct
-// global->LDS loads. Each wave computes S^T = K . Q^T on MFMA 32x32x16 (keys
+// SIMD; each lane holds its query's operand chunks in registers) and walks
+// 64-key tiles through a two-stage LDS ring filled by direct global->LDS
+// loads. Each wave computes S^T = K . Q^T on MFMA 32x32x16 (keys
 // as MFMA rows, queries as columns), so a lane owns one query's scores and
 // every per-query softmax quantity is a per-lane scalar. The probabilities
 // feed O^T += V^T . P^T straight from registers: the MFMA k-index of that
@@ -34,8 +35,8 @@
 // amplified most): queries, keys and values arrive as fp16 value + fp16
 // remainder planes and the probabilities are split the same way; each product
 // takes three MFMAs (hi.hi + hi.lo + lo.hi), which leaves an error of the
-// order of fp32 rounding. Its blocks hold 128 query rows on 4 waves with the
-// queries in registers, so that the doubled key/value ring fits in LDS.
+// order of fp32 rounding. Its blocks hold 128 query rows on 4 waves, whose
+// query remainders also sit in registers.
 #include <algorithm>
 
 #include "common.h"
@@ -97,9 +98,7 @@ struct Lane {
              // the keys (the halves are added once, after the walk)
   float thr; // 8 / c: probabilities stay below 2^8 between moves
   f32x16 o[HD / 32];
-  const u32x4 *qs;  // fast: the block's query tile in LDS [QT rows][16 chunks]
-  int qrow;         // fast: this lane's row in it
-  f16x8 qh[HD / 16], ql[HD / 16];  // precise: chunks 2kk + h of the row, hi / lo
+  f16x8 qh[HD / 16], ql[HD / 16];  // chunks 2kk + h of the row (precise: hi / lo)
 };
 
 // Direct loads of key tile kb into an LDS stage. Load i of wave w fills K
@@ -164,7 +163,7 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *st
   f32x16 s[2] = {f32x16{}, f32x16{}};
 #pragma unroll
   for (int kk = 0; kk < HD / 16; ++kk) {
-    const f16x8 qf = PREC ? L.qh[kk] : as_f16x8(L.qs[ks_idx(L.qrow, 2 * kk + h)]);
+    const f16x8 qf = L.qh[kk];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       const int ki = ks_idx(b * 32 + (lane & 31), 2 * kk + h);
@@ -320,7 +319,6 @@ template <int MODE, bool PREC, bool DEC = false>
 __global__ __launch_bounds__((Shape<PREC, DEC>::NT)) void k_attn(AttnArgs a) {
   constexpr int QT = Shape<PREC, DEC>::QT;
   __shared__ u32x4 lds[2 * Shape<PREC, DEC>::STAGE];
-  __shared__ u32x4 qlds[PREC ? 1 : QT * 16];
   const int G = a.n_heads / a.n_kv, TG = (a.T - a.t0) * G;
   // Prefill: one block index over (query tile, KV head), tiles with more keys
   // first across all heads, so that the longest blocks start in the first
@@ -342,29 +340,16 @@ __global__ __launch_bounds__((Shape<PREC, DEC>::NT)) void k_attn(AttnArgs a) {
   L.l = 0.f;
 #pragma unroll
   for (int db = 0; db < HD / 32; ++db) L.o[db] = f32x16{};
-  if constexpr (PREC) {
-    // Queries -> registers: the chunks this lane feeds to the S^T products.
+  {
+    // Queries -> registers: the chunks this lane feeds to the S^T products
+    // (no per-tile LDS reads of the query tile).
     const long qoff = ((long)tok * a.n_heads + head) * HD + 8 * (lane >> 5);
 #pragma unroll
     for (int kk = 0; kk < HD / 16; ++kk) {
       L.qh[kk] = *reinterpret_cast<const f16x8 *>(a.q + qoff + 16 * kk);
-      L.ql[kk] = *reinterpret_cast<const f16x8 *>(a.q_lo + qoff + 16 * kk);
-    }
-  } else {
-    // Query tile -> LDS (same layout and swizzle as a K tile): wave w's rows
-    // 32 w .. 32 w + 31, four rows per direct load.
-    u32x4 *qdst = qlds;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int rl = w * 32 + i * 4 + (lane >> 4);          // LDS row
-      const int rg = min(q0 + rl, TG - 1);                   // stacked row it holds
-      const int c = (lane & 15) ^ (rl & 15);
-      const f16 *src = a.q + ((long)(a.t0 + rg / G) * a.n_heads + kvh * G + rg % G) * HD + c * 8;
-      __builtin_amdgcn_global_load_lds(src, qdst + (w * 32 + i * 4) * 16, 16, 0, 0);
+      if constexpr (PREC) L.ql[kk] = *reinterpret_cast<const f16x8 *>(a.q_lo + qoff + 16 * kk);
     }
   }
-  L.qs = qlds;
-  L.qrow = w * 32 + (lane & 31);
   const float scale_log2 = 1.4426950408889634f * rsqrtf((float)HD);
   L.thr = 8.f / scale_log2;
   const int tok_first = a.t0 + q0 / G;
