@@ -43,11 +43,18 @@ lazily fetched layer list streams them.
 from __future__ import annotations
 
 import math
+import os
+from concurrent.futures import ThreadPoolExecutor
 from typing import Dict, List, Optional, Sequence
 
 import numpy as np
+from threadpoolctl import threadpool_limits
 
 ROW_BLOCK = 1024  # query rows per attention block (bounds memory, not maths)
+# Host threads for independent heads: the CPUs this process may use, at most
+# the OpenMP thread count when one is set (a share of a larger machine).
+THREADS = max(1, min(len(os.sched_getaffinity(0)),
+                     int(os.environ.get("OMP_NUM_THREADS") or 1 << 30)))
 
 
 def _c(a, dtype):
@@ -88,23 +95,37 @@ def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
     q [nq][Hq][hd]; k, v [nk][Hkv][hd]; a query at position p sees the keys
     whose position is <= p. Query head h reads KV head floor(h / G),
     G = Hq / Hkv. Softmax of q.k / sqrt(hd) over the visible keys.
+
+    Queries are taken ROW_BLOCK rows at a time (memory only). A block's
+    products are formed with the keys that at least one of its queries sees;
+    a key hidden from every query of the block would get probability exactly
+    0, so leaving it out changes nothing. Heads are independent and run on a
+    pool of host threads (BLAS single-threaded inside it); each head's
+    arithmetic is the same as in a loop over heads.
     """
     nq, hq, hd = q.shape
     hkv = k.shape[1]
     g = hq // hkv
     scale = 1.0 / math.sqrt(hd)
     out = np.empty_like(q)
+    q_pos, k_pos = np.asarray(q_pos), np.asarray(k_pos)
     for r0 in range(0, nq, ROW_BLOCK):
         r1 = min(nq, r0 + ROW_BLOCK)
-        visible = k_pos[None, :] <= q_pos[r0:r1, None]
-        for h in range(hq):
+        seen = k_pos <= q_pos[r0:r1].max()
+        kb, vb = k[seen], v[seen]
+        hidden = k_pos[seen][None, :] > q_pos[r0:r1, None]
+
+        def one_head(h):
             kh = h // g
-            s = (q[r0:r1, h, :] @ k[:, kh, :].T) * scale
-            s = np.where(visible, s, -np.inf)
-            s = s - s.max(axis=1, keepdims=True)
-            p = np.exp(s)
-            p = p / p.sum(axis=1, keepdims=True)
-            out[r0:r1, h, :] = p @ v[:, kh, :]
+            s = q[r0:r1, h, :] @ kb[:, kh, :].T
+            s *= scale
+            np.putmask(s, hidden, -np.inf)
+            s -= s.max(axis=1, keepdims=True)
+            np.exp(s, out=s)
+            s /= s.sum(axis=1, keepdims=True)
+            out[r0:r1, h, :] = s @ vb[:, kh, :]
+        with threadpool_limits(1, user_api="blas"), ThreadPoolExecutor(min(hq, THREADS)) as ex:
+            list(ex.map(one_head, range(hq)))
     return out
 
 
