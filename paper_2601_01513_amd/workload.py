@@ -215,6 +215,27 @@ def make_workload(cfg: VerifierConfig, seed: int, device="cpu") -> Workload:
                     make_visual(cfg, seed, device), prefix_ids, cand_ids, lens)
 
 
+def input_fingerprint(wl: Workload, samples: int = 4096) -> str:
+    """SHA-256 over the exact bits of the ids and lengths and of an evenly
+    strided sample of every weight tensor and of the visual rows: names the
+    generated inputs without copying them all to the host."""
+    import hashlib
+    torch = _torch()
+    h = hashlib.sha256()
+    for a in (wl.prefix_ids, wl.cand_ids, wl.cand_len):
+        h.update(np.ascontiguousarray(a).tobytes())
+    tensors = [wl.weights["embed"], wl.weights["lm_head"], wl.weights["final_norm"], wl.visual]
+    for lw in wl.weights["layers"]:
+        tensors += [lw[k] for k in sorted(lw)]
+    for t in tensors:
+        flat = t.detach().reshape(-1)
+        step = max(1, flat.numel() // samples)
+        s = flat[::step][:samples].contiguous()
+        bits = s.view(torch.int16) if s.element_size() == 2 else s.view(torch.int32)
+        h.update(bits.cpu().numpy().tobytes())
+    return h.hexdigest()
+
+
 def to_host_f32(t) -> np.ndarray:
     """Exact host copy of a (bf16 or fp32) tensor as float32."""
     return t.detach().float().cpu().numpy()
