@@ -54,6 +54,8 @@ extern "C" {
 #define VSR_ERANGE (-3)  /* a size exceeds the maxima given at create     */
 #define VSR_ENOMEM (-4)  /* workspace smaller than vsr_workspace_size     */
 #define VSR_EHIP (-5)    /* a HIP runtime call failed (message has text)  */
+#define VSR_EID (-6)     /* checked call: an id outside [0, vocab) was read */
+#define VSR_ENONFINITE (-7) /* checked call: a NaN or infinity in the results */
 
 /* Arithmetic types of weights, visual rows and activations. */
 #define VSR_F32 0
@@ -140,7 +142,8 @@ int vsr_load_weights(vsr_ctx *ctx, const vsr_weights *w);
  *   visual : device [n_visual][d_model] rows fed directly as layer-0 inputs
  *            (may be NULL when n_visual == 0);
  *   ids    : device [n_text] int32 text ids in [0, vocab) (may be NULL when
- *            n_text == 0); out-of-range ids are read as id 0.
+ *            n_text == 0); out-of-range ids are read as id 0 (VSR_EID
+ *            under vsr_set_checks).
  * P = n_visual + n_text must satisfy 1 <= P <= max_prefix. Replaces any
  * earlier prefix. */
 int vsr_prefill(vsr_ctx *ctx, const void *visual, int32_t n_visual,
@@ -150,7 +153,8 @@ int vsr_prefill(vsr_ctx *ctx, const void *visual, int32_t n_visual,
  * (Eq. 6-7). May be called any number of times after one prefill.
  *   cand_ids : device [M][Cmax] int32, row m holds candidate m's tokens in
  *              positions 0..cand_len[m]-1 (the rest is ignored);
- *              out-of-range ids are read as id 0;
+ *              out-of-range ids are read as id 0 (VSR_EID under
+ *              vsr_set_checks);
  *   cand_len : HOST [M] int32, each in [0, Cmax];
  *   logprobs : device [M][Cmax] float out; 0 past each candidate's length;
  *   scores   : device [M] float out, sum of each candidate's log-probs;
@@ -292,6 +296,27 @@ int vsr_retrieve(const float *frame_emb, const int32_t *key_idx, const int32_t *
  * give bit-identical results. src and dst 16-byte aligned. Enqueued on
  * hip_stream (NULL = default); errors via vsr_last_error(NULL). */
 int vsr_weights_to_f16(const void *src, void *dst, size_t n, void *hip_stream);
+
+/* Call validator, off by default. With checks set, every later vsr_prefill,
+ * vsr_score, vsr_verify, vsr_reliability and vsr_draft call on the context
+ * clears a status word in the workspace before its launches, then waits for
+ * its stream and reads the word once after them (the call becomes
+ * synchronous), and returns
+ *   VSR_EID        (VSR_CHECK_IDS) if a text, candidate, branch or prompt id
+ *                  outside [0, vocab) was read; such ids are used as id 0,
+ *                  checked or not, so the results are those of id 0;
+ *   VSR_ENONFINITE (VSR_CHECK_FINITE) if a result is NaN or infinite: the
+ *                  scores (vsr_score, vsr_verify), the Yes/No log-probs
+ *                  (vsr_reliability) or the last prefix row's hidden state
+ *                  (vsr_prefill). A NaN or infinite visual row, or an fp16
+ *                  activation that overflows (|x| > 65504) on the bf16 path,
+ *                  propagates to them.
+ * VSR_EID is reported before VSR_ENONFINITE. Either way the outputs are
+ * written as in an unchecked call and the prefix state changes as it would
+ * on success. checks: an OR of the bits below (0 turns checking off). */
+#define VSR_CHECK_IDS 1
+#define VSR_CHECK_FINITE 2
+int vsr_set_checks(vsr_ctx *ctx, int checks);
 
 /* Releases the context (not the workspace or the weights). NULL is a no-op. */
 void vsr_destroy(vsr_ctx *ctx);

@@ -14,6 +14,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libvsr.so")
 
 VSR_OK, VSR_EINVAL, VSR_ESTATE, VSR_ERANGE, VSR_ENOMEM, VSR_EHIP = 0, -1, -2, -3, -4, -5
+VSR_EID, VSR_ENONFINITE = -6, -7
+VSR_CHECK_IDS, VSR_CHECK_FINITE = 1, 2
 VSR_F32, VSR_BF16, VSR_F16 = 0, 1, 2
 GEMM_WEIGHT_KEYS = ("wqkv", "wo", "wgu", "wdown")  # per layer, plus lm_head
 VSR_MAX_CANDS = 256
@@ -21,7 +23,7 @@ VSR_MAX_CANDS = 256
 EXPORTS = ["vsr_workspace_size", "vsr_create", "vsr_load_weights", "vsr_prefill",
            "vsr_score", "vsr_verify", "vsr_reliability", "vsr_draft", "vsr_align_select", "vsr_weights_to_f16",
            "vsr_keyframes", "vsr_retrieve_workspace_size", "vsr_retrieve", "vsr_last_error",
-           "vsr_destroy", "vsr_profile_enable", "vsr_profile_read"]
+           "vsr_destroy", "vsr_set_checks", "vsr_profile_enable", "vsr_profile_read"]
 
 VSR_SELECT_TWO_STAGE, VSR_SELECT_ADDITION, VSR_SELECT_INVERT = 0, 1, 2
 SELECT_STRATEGIES = {"two_stage": VSR_SELECT_TWO_STAGE, "addition": VSR_SELECT_ADDITION,
@@ -129,6 +131,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vsr_last_error.restype = ctypes.c_char_p
     lib.vsr_destroy.argtypes = [ctypes.c_void_p]
     lib.vsr_destroy.restype = None
+    lib.vsr_set_checks.argtypes = [ctypes.c_void_p, ctypes.c_int]
+    lib.vsr_set_checks.restype = ctypes.c_int
     lib.vsr_profile_enable.argtypes = [ctypes.c_void_p, ctypes.c_int]
     lib.vsr_profile_enable.restype = ctypes.c_int
     lib.vsr_profile_read.argtypes = [ctypes.c_void_p, ctypes.POINTER(ctypes.c_double),
@@ -301,6 +305,13 @@ class Verifier:
         self._check(self.lib.vsr_draft(self.h, _ptr(prompt_ids), lens, M, cmax, int(n_new),
                                        _ptr(out)))
         return out
+
+    def set_checks(self, ids: bool = True, finite: bool = True):
+        """Call validator (vsr_set_checks): later calls wait for their stream
+        and raise VsrError with code VSR_EID / VSR_ENONFINITE on a bad id or a
+        non-finite result (their outputs are still written)."""
+        self._check(self.lib.vsr_set_checks(
+            self.h, (VSR_CHECK_IDS if ids else 0) | (VSR_CHECK_FINITE if finite else 0)))
 
     def profile(self, enable, kinds=None):
         """Turns per-stage kernel timing on or off (clears recorded launches).

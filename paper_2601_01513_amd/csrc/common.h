@@ -62,17 +62,29 @@ struct Branches {
 // Rotary table: cs[p][i] = (cos, sin)(p * base^(-2i/hd)), i < hd/2, p < npos.
 hipError_t launch_rope_table(float2 *cs, int npos, int hd, float base, hipStream_t s);
 
+// Status word of a checked call (vsr_set_checks): kernels that read an id
+// outside [0, vocab) (and use id 0 instead) set kFlagBadId; the finiteness
+// check of a call's outputs sets kFlagNonFinite.
+constexpr int32_t kFlagBadId = 1;
+constexpr int32_t kFlagNonFinite = 2;
+hipError_t launch_flags_clear(int32_t *flags, hipStream_t s);
+// Sets kFlagNonFinite in *flags if any of x[0 .. n) is NaN or infinite.
+hipError_t launch_check_finite(const float *x, long n, int32_t *flags, hipStream_t s);
+
 // Row tables of one score call: for packed row t of candidate m at offset j,
 // row_lo[t] = cu[m] (first row of its candidate), row_pos[t] = P + j,
-// lm_tgt[t] = cand_ids[m][j] (clamped into [0, vocab)).
+// lm_tgt[t] = cand_ids[m][j] (clamped into [0, vocab); a clamped id sets
+// kFlagBadId in *flags).
 hipError_t launch_row_tables(const Branches &br, int P, const int32_t *cand_ids, int vocab,
-                             int32_t *row_lo, int32_t *row_pos, int32_t *lm_tgt,
-                             hipStream_t s);
+                             int32_t *flags, int32_t *row_lo, int32_t *row_pos,
+                             int32_t *lm_tgt, hipStream_t s);
 
-// x[p] = visual[p] for p < n_visual, else embed[ids[p - n_visual]] (fp32 out).
+// x[p] = visual[p] for p < n_visual, else embed[ids[p - n_visual]] (fp32 out;
+// an id outside [0, vocab) reads row 0 and sets kFlagBadId in *flags).
 template <typename T>
 hipError_t launch_embed_prefix(const T *visual, int n_visual, const int32_t *ids, int n_text,
-                               const T *embed, int vocab, int d, float *x, hipStream_t s);
+                               const T *embed, int vocab, int d, float *x, int32_t *flags,
+                               hipStream_t s);
 // x[t] = embed[ids[t]] for t < rows (ids already in [0, vocab)).
 template <typename T>
 hipError_t launch_embed_rows(const int32_t *ids, int rows, const T *embed, int d, float *x,
@@ -93,8 +105,8 @@ hipError_t launch_lm_inputs(const float *x, const float *h_last, const int32_t *
 // tables, per-step tables, the last prompt row's norm per branch and the
 // greedy pick from the LM-head argmax partials.
 hipError_t launch_draft_rows(const Branches &br, int P, int S, const int32_t *ids, int vocab,
-                             int32_t *row_lo, int32_t *row_pos, int32_t *cache_row,
-                             int32_t *lm_tgt, hipStream_t s);
+                             int32_t *flags, int32_t *row_lo, int32_t *row_pos,
+                             int32_t *cache_row, int32_t *lm_tgt, hipStream_t s);
 hipError_t launch_draft_step(const Branches &br, int P, int S, int step, int32_t *row_lo,
                              int32_t *row_pos, int32_t *cache_row, hipStream_t s);
 template <typename TW, typename TA>

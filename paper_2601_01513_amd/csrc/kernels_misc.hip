@@ -3,6 +3,8 @@
 // merge with the target gather, and the per-candidate sum and argmax
 // (Eq. 6-7). All of them read and write rows with consecutive lanes on
 // consecutive elements; reductions run in a fixed order (no atomics).
+#include <algorithm>
+
 #include "common.h"
 
 namespace vsr {
@@ -36,25 +38,30 @@ hipError_t launch_rope_table(float2 *cs, int npos, int hd, float base, hipStream
 
 // --------------------------------------------------------------- row tables
 __global__ void k_row_tables(Branches br, int P, const int32_t *cand_ids, int vocab,
-                             int32_t *row_lo, int32_t *row_pos, int32_t *lm_tgt) {
+                             int32_t *flags, int32_t *row_lo, int32_t *row_pos,
+                             int32_t *lm_tgt) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= br.cu[br.M]) return;
   int m = 0;
   while (br.cu[m + 1] <= t) ++m;
   const int j = t - br.cu[m];
   int id = cand_ids[(long)m * br.cmax + j];
-  if (id < 0 || id >= vocab) id = 0;
+  if (id < 0 || id >= vocab) {
+    atomicOr(flags, kFlagBadId);
+    id = 0;
+  }
   row_lo[t] = br.cu[m];
   row_pos[t] = P + j;
   lm_tgt[t] = id;
 }
 
 hipError_t launch_row_tables(const Branches &br, int P, const int32_t *cand_ids, int vocab,
-                             int32_t *row_lo, int32_t *row_pos, int32_t *lm_tgt,
-                             hipStream_t s) {
+                             int32_t *flags, int32_t *row_lo, int32_t *row_pos,
+                             int32_t *lm_tgt, hipStream_t s) {
   const int T = br.cu[br.M];
   if (T == 0) return hipSuccess;
-  k_row_tables<<<(T + 255) / 256, 256, 0, s>>>(br, P, cand_ids, vocab, row_lo, row_pos, lm_tgt);
+  k_row_tables<<<(T + 255) / 256, 256, 0, s>>>(br, P, cand_ids, vocab, flags, row_lo, row_pos,
+                                               lm_tgt);
   return hipGetLastError();
 }
 
@@ -63,15 +70,18 @@ hipError_t launch_row_tables(const Branches &br, int P, const int32_t *cand_ids,
 // prompt and the new tokens): row_lo = m S, row_pos = P + j (rotary),
 // cache_row = m S + j, lm_tgt = the prompt id (clamped).
 __global__ void k_draft_rows(Branches br, int P, int S, const int32_t *ids, int vocab,
-                             int32_t *row_lo, int32_t *row_pos, int32_t *cache_row,
-                             int32_t *lm_tgt) {
+                             int32_t *flags, int32_t *row_lo, int32_t *row_pos,
+                             int32_t *cache_row, int32_t *lm_tgt) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= br.cu[br.M]) return;
   int m = 0;
   while (br.cu[m + 1] <= t) ++m;
   const int j = t - br.cu[m];
   int id = ids[(long)m * br.cmax + j];
-  if (id < 0 || id >= vocab) id = 0;
+  if (id < 0 || id >= vocab) {
+    atomicOr(flags, kFlagBadId);
+    id = 0;
+  }
   row_lo[t] = m * S;
   row_pos[t] = P + j;
   cache_row[t] = m * S + j;
@@ -79,10 +89,10 @@ __global__ void k_draft_rows(Branches br, int P, int S, const int32_t *ids, int 
 }
 
 hipError_t launch_draft_rows(const Branches &br, int P, int S, const int32_t *ids, int vocab,
-                             int32_t *row_lo, int32_t *row_pos, int32_t *cache_row,
-                             int32_t *lm_tgt, hipStream_t s) {
+                             int32_t *flags, int32_t *row_lo, int32_t *row_pos,
+                             int32_t *cache_row, int32_t *lm_tgt, hipStream_t s) {
   const int T = br.cu[br.M];
-  k_draft_rows<<<(T + 255) / 256, 256, 0, s>>>(br, P, S, ids, vocab, row_lo, row_pos,
+  k_draft_rows<<<(T + 255) / 256, 256, 0, s>>>(br, P, S, ids, vocab, flags, row_lo, row_pos,
                                                cache_row, lm_tgt);
   return hipGetLastError();
 }
@@ -149,17 +159,47 @@ hipError_t launch_argmax_merge(const float2 *part, int nchunks, int M, int n_new
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------- call validator
+// The status word of a checked call: cleared at its start, bits set by the
+// kernels that meet a bad id or a non-finite result, read once at its end.
+__global__ void k_flags_clear(int32_t *flags) {
+  if (threadIdx.x == 0) flags[0] = 0;
+}
+
+hipError_t launch_flags_clear(int32_t *flags, hipStream_t s) {
+  k_flags_clear<<<1, 64, 0, s>>>(flags);
+  return hipGetLastError();
+}
+
+// Sets kFlagNonFinite if any of x[0 .. n) is NaN or infinite.
+__global__ __launch_bounds__(256) void k_check_finite(const float *x, long n, int32_t *flags) {
+  bool bad = false;
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long)gridDim.x * 256)
+    bad |= !isfinite(x[i]);
+  if (__any(bad) && (threadIdx.x & 63) == 0) atomicOr(flags, kFlagNonFinite);
+}
+
+hipError_t launch_check_finite(const float *x, long n, int32_t *flags, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const long blocks = std::min<long>((n + 255) / 256, 1024);
+  k_check_finite<<<(unsigned)blocks, 256, 0, s>>>(x, n, flags);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------- embedding
 template <typename T>
 __global__ void k_embed_prefix(const T *visual, int n_visual, const int32_t *ids,
-                               const T *embed, int vocab, int d, float *x) {
+                               const T *embed, int vocab, int d, float *x, int32_t *flags) {
   const int p = blockIdx.x;
   const T *src;
   if (p < n_visual) {
     src = visual + (long)p * d;
   } else {
     int id = ids[p - n_visual];
-    if (id < 0 || id >= vocab) id = 0;
+    if (id < 0 || id >= vocab) {
+      if (threadIdx.x == 0) atomicOr(flags, kFlagBadId);
+      id = 0;
+    }
     src = embed + (long)id * d;
   }
   float *dst = x + (long)p * d;
@@ -168,9 +208,10 @@ __global__ void k_embed_prefix(const T *visual, int n_visual, const int32_t *ids
 
 template <typename T>
 hipError_t launch_embed_prefix(const T *visual, int n_visual, const int32_t *ids, int n_text,
-                               const T *embed, int vocab, int d, float *x, hipStream_t s) {
+                               const T *embed, int vocab, int d, float *x, int32_t *flags,
+                               hipStream_t s) {
   const int P = n_visual + n_text;
-  k_embed_prefix<T><<<P, 256, 0, s>>>(visual, n_visual, ids, embed, vocab, d, x);
+  k_embed_prefix<T><<<P, 256, 0, s>>>(visual, n_visual, ids, embed, vocab, d, x, flags);
   return hipGetLastError();
 }
 
@@ -504,7 +545,7 @@ hipError_t launch_reduce_select(const Branches &br, const float *logprobs, float
 
 #define VSR_INST(T)                                                                          \
   template hipError_t launch_embed_prefix<T>(const T *, int, const int32_t *, int, const T *, \
-                                             int, int, float *, hipStream_t);               \
+                                             int, int, float *, int32_t *, hipStream_t);    \
   template hipError_t launch_embed_rows<T>(const int32_t *, int, const T *, int, float *,     \
                                            hipStream_t);
 VSR_INST(float)

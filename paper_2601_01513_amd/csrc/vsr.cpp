@@ -48,7 +48,7 @@ struct Plan {
   int lm_rows;  // LM-head rows: candidate rows, or 2 per branch (reliability)
   size_t x, xn, q, q_lo, attn, h, kc, vtc, kc_lo, vtc_lo, bk, bvt, bk_lo, bvt_lo, kd, vtd,
       kd_lo, vtd_lo, part_acc, part_ml, lm_part, tgt, row_lo, row_pos, cache_row, dec_ids,
-      lm_tgt, rope, h_last, gemm_part, total;
+      lm_tgt, rope, h_last, gemm_part, flags, total;
 };
 
 // Returns an empty message if cfg is supported.
@@ -193,6 +193,7 @@ Plan make_plan(const vsr_config &c) {
   p.rope = take((size_t)p.rope_npos * (hd / 2) * 8);
   p.h_last = take(d * 4);
   p.gemm_part = take(gemm_part * 4);
+  p.flags = take(64);
   p.total = off;
   return p;
 }
@@ -207,6 +208,7 @@ struct vsr_ctx {
   int device;
   bool have_weights = false;
   bool prefilled = false;
+  int checks = 0;  // VSR_CHECK_* bits of vsr_set_checks
   int P = 0;
   const void *embed = nullptr, *lm_head = nullptr, *final_norm = nullptr;
   std::vector<const void *> attn_norm, wqkv, wo, ffn_norm, wgu, wdown;
@@ -604,7 +606,7 @@ int prefill_impl(vsr_ctx *c, const void *visual, int nv, const int32_t *ids, int
   STAGE(c, K_EMBED, "prefix embedding",
            launch_embed_prefix<TW>(static_cast<const TW *>(visual), nv, ids, nt,
                                    static_cast<const TW *>(c->embed), cf.vocab, cf.d_model, x,
-                                   c->stream));
+                                   c->at<int32_t>(p.flags), c->stream));
   c->P = P;
   const int rc = run_layers<TW, TA>(c, P, 0, Split{1});
   if (rc) return rc;
@@ -627,7 +629,8 @@ int branch_forward(vsr_ctx *c, const Branches &br, const int32_t *cand_ids) {
   int32_t *row_lo = c->at<int32_t>(p.row_lo), *row_pos = c->at<int32_t>(p.row_pos);
   int32_t *lm_tgt = c->at<int32_t>(p.lm_tgt);
   STAGE(c, K_ROWS, "row tables",
-        launch_row_tables(br, c->P, cand_ids, cf.vocab, row_lo, row_pos, lm_tgt, s));
+        launch_row_tables(br, c->P, cand_ids, cf.vocab, c->at<int32_t>(p.flags), row_lo, row_pos,
+                          lm_tgt, s));
   STAGE(c, K_EMBED, "candidate embedding",
         launch_embed_rows<TW>(lm_tgt, T_rows, static_cast<const TW *>(c->embed), cf.d_model,
                               c->at<float>(p.x), s));
@@ -704,13 +707,15 @@ int verify_impl(vsr_ctx *c, const void *visual, int nv, const int32_t *ids, int 
   float *x = c->at<float>(p.x);
   STAGE(c, K_EMBED, "prefix embedding",
         launch_embed_prefix<TW>(static_cast<const TW *>(visual), nv, ids, nt,
-                                static_cast<const TW *>(c->embed), cf.vocab, cf.d_model, x, s));
+                                static_cast<const TW *>(c->embed), cf.vocab, cf.d_model, x,
+                                c->at<int32_t>(p.flags), s));
   c->P = P;
   int32_t *row_lo = c->at<int32_t>(p.row_lo), *row_pos = c->at<int32_t>(p.row_pos);
   int32_t *lm_tgt = c->at<int32_t>(p.lm_tgt);
   float *xc = x + (size_t)P * cf.d_model;  // the candidate rows
   STAGE(c, K_ROWS, "row tables",
-        launch_row_tables(br, P, cand_ids, cf.vocab, row_lo, row_pos, lm_tgt, s));
+        launch_row_tables(br, P, cand_ids, cf.vocab, c->at<int32_t>(p.flags), row_lo, row_pos,
+                          lm_tgt, s));
   STAGE(c, K_EMBED, "candidate embedding",
         launch_embed_rows<TW>(lm_tgt, T_rows, static_cast<const TW *>(c->embed), cf.d_model, xc,
                               s));
@@ -795,8 +800,8 @@ int draft_impl(vsr_ctx *c, const Branches &br, const int32_t *ids, int n_new, in
     return VSR_OK;
   };
   STAGE(c, K_ROWS, "draft rows",
-        launch_draft_rows(br, c->P, p.dec_S, ids, cf.vocab, row_lo, row_pos, cache_row, lm_tgt,
-                          s));
+        launch_draft_rows(br, c->P, p.dec_S, ids, cf.vocab, c->at<int32_t>(p.flags), row_lo,
+                          row_pos, cache_row, lm_tgt, s));
   STAGE(c, K_EMBED, "draft embedding",
         launch_embed_rows<TW>(lm_tgt, T_rows, static_cast<const TW *>(c->embed), cf.d_model,
                               x, s));
@@ -835,6 +840,31 @@ int set_device(vsr_ctx *c) {
   return VSR_OK;
 }
 
+// Checked calls (vsr_set_checks): the status word is cleared before the
+// call's launches and read once after them (the call then waits for its
+// stream). `vals` (n floats, device) are the call's results whose finiteness
+// is checked.
+int checks_begin(vsr_ctx *c) {
+  if (!c->checks) return VSR_OK;
+  HIPCHECK(c, "checks", launch_flags_clear(c->at<int32_t>(c->plan.flags), c->stream));
+  return VSR_OK;
+}
+
+int checks_end(vsr_ctx *c, int rc, const float *vals, long n) {
+  if (rc != VSR_OK || !c->checks) return rc;
+  int32_t *flags = c->at<int32_t>(c->plan.flags);
+  if ((c->checks & VSR_CHECK_FINITE) && vals)
+    HIPCHECK(c, "checks", launch_check_finite(vals, n, flags, c->stream));
+  int32_t f = 0;
+  HIPCHECK(c, "checks", hipMemcpyAsync(&f, flags, sizeof f, hipMemcpyDeviceToHost, c->stream));
+  HIPCHECK(c, "checks", hipStreamSynchronize(c->stream));
+  if ((c->checks & VSR_CHECK_IDS) && (f & kFlagBadId))
+    return c->fail(VSR_EID, "an id outside [0, vocab) was read (it was used as id 0)");
+  if ((c->checks & VSR_CHECK_FINITE) && (f & kFlagNonFinite))
+    return c->fail(VSR_ENONFINITE, "the results hold a NaN or an infinity");
+  return VSR_OK;
+}
+
 }  // namespace
 
 extern "C" int vsr_prefill(vsr_ctx *ctx, const void *visual, int32_t n_visual,
@@ -853,11 +883,13 @@ extern "C" int vsr_prefill(vsr_ctx *ctx, const void *visual, int32_t n_visual,
   if (rc) return rc;
   ctx->prefilled = false;
   ctx->phase = 0;
+  rc = checks_begin(ctx);
+  if (rc) return rc;
   rc = ctx->cfg.dtype == VSR_BF16
            ? prefill_impl<bf16, f16>(ctx, visual, n_visual, ids, n_text)
            : prefill_impl<float, float>(ctx, visual, n_visual, ids, n_text);
   if (rc == VSR_OK) ctx->prefilled = true;
-  return rc;
+  return checks_end(ctx, rc, ctx->at<float>(ctx->plan.h_last), ctx->cfg.d_model);
 }
 
 extern "C" int vsr_score(vsr_ctx *ctx, const int32_t *cand_ids, const int32_t *cand_len,
@@ -882,12 +914,15 @@ extern "C" int vsr_score(vsr_ctx *ctx, const int32_t *cand_ids, const int32_t *c
       return ctx->fail(VSR_EINVAL, "cand_len[%d] = %d outside [0, Cmax]", m, cand_len[m]);
     br.cu[m + 1] = br.cu[m] + cand_len[m];
   }
-  const int rc = set_device(ctx);
+  int rc = set_device(ctx);
   if (rc) return rc;
   ctx->phase = 1;
-  return ctx->cfg.dtype == VSR_BF16
-             ? score_impl<bf16, f16>(ctx, br, cand_ids, logprobs, scores, argmax)
-             : score_impl<float, float>(ctx, br, cand_ids, logprobs, scores, argmax);
+  rc = checks_begin(ctx);
+  if (rc) return rc;
+  rc = ctx->cfg.dtype == VSR_BF16
+           ? score_impl<bf16, f16>(ctx, br, cand_ids, logprobs, scores, argmax)
+           : score_impl<float, float>(ctx, br, cand_ids, logprobs, scores, argmax);
+  return checks_end(ctx, rc, scores, M);
 }
 
 extern "C" int vsr_verify(vsr_ctx *ctx, const void *visual, int32_t n_visual,
@@ -924,10 +959,13 @@ extern "C" int vsr_verify(vsr_ctx *ctx, const void *visual, int32_t n_visual,
   int rc = set_device(ctx);
   if (rc) return rc;
   ctx->prefilled = false;
+  rc = checks_begin(ctx);
+  if (rc) return rc;
   if (ctx->cfg.dtype == VSR_BF16 && br.cu[M] > 0) {
     ctx->phase = 3;
-    return verify_impl<bf16, f16>(ctx, visual, n_visual, ids, n_text, br, cand_ids, logprobs,
-                                  scores, argmax);
+    rc = verify_impl<bf16, f16>(ctx, visual, n_visual, ids, n_text, br, cand_ids, logprobs,
+                                scores, argmax);
+    return checks_end(ctx, rc, scores, M);
   }
   // fp32 contexts, or no candidate tokens: the two passes one after the other.
   ctx->phase = 0;
@@ -937,9 +975,10 @@ extern "C" int vsr_verify(vsr_ctx *ctx, const void *visual, int32_t n_visual,
   if (rc) return rc;
   ctx->prefilled = true;
   ctx->phase = 1;
-  return ctx->cfg.dtype == VSR_BF16
-             ? score_impl<bf16, f16>(ctx, br, cand_ids, logprobs, scores, argmax)
-             : score_impl<float, float>(ctx, br, cand_ids, logprobs, scores, argmax);
+  rc = ctx->cfg.dtype == VSR_BF16
+           ? score_impl<bf16, f16>(ctx, br, cand_ids, logprobs, scores, argmax)
+           : score_impl<float, float>(ctx, br, cand_ids, logprobs, scores, argmax);
+  return checks_end(ctx, rc, scores, M);
 }
 
 extern "C" int vsr_reliability(vsr_ctx *ctx, const int32_t *branch_ids,
@@ -969,14 +1008,17 @@ extern "C" int vsr_reliability(vsr_ctx *ctx, const int32_t *branch_ids,
       return ctx->fail(VSR_EINVAL, "branch_len[%d] = %d outside [1, Cmax]", m, branch_len[m]);
     br.cu[m + 1] = br.cu[m] + branch_len[m];
   }
-  const int rc = set_device(ctx);
+  int rc = set_device(ctx);
   if (rc) return rc;
   ctx->phase = 1;
-  return ctx->cfg.dtype == VSR_BF16
-             ? reliability_impl<bf16, f16>(ctx, br, branch_ids, yes_id, no_id, delta, lp_yes_no,
-                                           rel, keep)
-             : reliability_impl<float, float>(ctx, br, branch_ids, yes_id, no_id, delta,
-                                              lp_yes_no, rel, keep);
+  rc = checks_begin(ctx);
+  if (rc) return rc;
+  rc = ctx->cfg.dtype == VSR_BF16
+           ? reliability_impl<bf16, f16>(ctx, br, branch_ids, yes_id, no_id, delta, lp_yes_no,
+                                         rel, keep)
+           : reliability_impl<float, float>(ctx, br, branch_ids, yes_id, no_id, delta,
+                                            lp_yes_no, rel, keep);
+  return checks_end(ctx, rc, lp_yes_no, 2L * M);
 }
 
 extern "C" int vsr_draft(vsr_ctx *ctx, const int32_t *prompt_ids, const int32_t *prompt_len,
@@ -1003,12 +1045,14 @@ extern "C" int vsr_draft(vsr_ctx *ctx, const int32_t *prompt_ids, const int32_t 
       return ctx->fail(VSR_EINVAL, "prompt_len[%d] = %d outside [1, Cmax]", m, prompt_len[m]);
     br.cu[m + 1] = br.cu[m] + prompt_len[m];
   }
-  const int rc = set_device(ctx);
+  int rc = set_device(ctx);
   if (rc) return rc;
   ctx->phase = 2;
-  return ctx->cfg.dtype == VSR_BF16
-             ? draft_impl<bf16, f16>(ctx, br, prompt_ids, n_new, tokens)
-             : draft_impl<float, float>(ctx, br, prompt_ids, n_new, tokens);
+  rc = checks_begin(ctx);
+  if (rc) return rc;
+  rc = ctx->cfg.dtype == VSR_BF16 ? draft_impl<bf16, f16>(ctx, br, prompt_ids, n_new, tokens)
+                                  : draft_impl<float, float>(ctx, br, prompt_ids, n_new, tokens);
+  return checks_end(ctx, rc, nullptr, 0);
 }
 
 extern "C" int vsr_align_select(const float *ent, const float *frames, int32_t M, int32_t NF,
@@ -1129,6 +1173,14 @@ extern "C" int vsr_weights_to_f16(const void *src, void *dst, size_t n, void *hi
     g_create_error = std::string("HIP error in weights_to_f16: ") + hipGetErrorString(e);
     return VSR_EHIP;
   }
+  return VSR_OK;
+}
+
+extern "C" int vsr_set_checks(vsr_ctx *ctx, int checks) {
+  if (!ctx) return VSR_EINVAL;
+  if (checks & ~(VSR_CHECK_IDS | VSR_CHECK_FINITE))
+    return ctx->fail(VSR_EINVAL, "set_checks: unknown check bits 0x%x", checks);
+  ctx->checks = checks;
   return VSR_OK;
 }
 

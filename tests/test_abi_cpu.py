@@ -216,3 +216,9 @@ def test_retrieval_calls_reject_bad_arguments():
                       (dict(ws=0x50004), b"aligned"), (dict(wsb=ws - 1), b"smaller")):
         assert rt(**bad) == B.VSR_EINVAL, bad
         assert word in lib.vsr_last_error(None), (bad, lib.vsr_last_error(None))
+
+
+def test_set_checks_without_context_fails_cleanly():
+    lib = _lib()
+    assert lib.vsr_set_checks(None, B.VSR_CHECK_IDS) == B.VSR_EINVAL
+    assert (B.VSR_EID, B.VSR_ENONFINITE) == (-6, -7)
