@@ -386,32 +386,28 @@ __global__ __launch_bounds__(NT) void k_gemm_residual(const f16 *__restrict__ A,
   }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w / TL::WN, wn = w % TL::WN;
-  static_assert(TL::FN % 2 == 0, "column blocks taken in pairs");
   if (m0 + TL::BM <= rows && n0 + TL::BN <= N) {
-    // Whole tile: the residual values of two MFMA column blocks are all
-    // loaded before any of them is stored back. The compiler cannot move a
-    // load of x above a store to x, so an element-by-element x += acc waits
-    // out one memory round trip per element (measured: 24 us of the O
-    // projection's 140 us, 40 us of the down projection's 645 us).
+    // Whole tile: the residual values of one MFMA column block (32 per
+    // lane) are all loaded before any of them is stored back. The compiler
+    // cannot move a load of x above a store to x, so an element-by-element
+    // x += acc waits out one memory round trip per element (measured: 24 us
+    // of the O projection's 140 us, 40 us of the down projection's 645 us);
+    // two column blocks at a time (64 values beside the 128 accumulators)
+    // spilled registers.
 #pragma unroll
-    for (int f0 = 0; f0 < TL::FN; f0 += 2) {
-      float xv[2][TL::FM][16];
+    for (int fn = 0; fn < TL::FN; ++fn) {
+      float xv[TL::FM][16];
+      const int col = n0 + acc_col<TL>(wn, fn, lane);
 #pragma unroll
-      for (int g = 0; g < 2; ++g)
+      for (int fm = 0; fm < TL::FM; ++fm)
 #pragma unroll
-        for (int fm = 0; fm < TL::FM; ++fm)
+        for (int r = 0; r < 16; ++r)
+          xv[fm][r] = x[(long)(m0 + acc_row<TL>(wm, fm, r, lane)) * N + col];
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            xv[g][fm][r] = x[(long)(m0 + acc_row<TL>(wm, fm, r, lane)) * N + n0 +
-                             acc_col<TL>(wn, f0 + g, lane)];
+      for (int fm = 0; fm < TL::FM; ++fm)
 #pragma unroll
-      for (int g = 0; g < 2; ++g)
-#pragma unroll
-        for (int fm = 0; fm < TL::FM; ++fm)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            x[(long)(m0 + acc_row<TL>(wm, fm, r, lane)) * N + n0 + acc_col<TL>(wn, f0 + g, lane)] =
-                xv[g][fm][r] + acc[fm][f0 + g][r];
+        for (int r = 0; r < 16; ++r)
+          x[(long)(m0 + acc_row<TL>(wm, fm, r, lane)) * N + col] = xv[fm][r] + acc[fm][fn][r];
     }
     return;
   }
