@@ -74,6 +74,54 @@ def stage_flops(cfg, P, lens):
     return f
 
 
+def stage_bytes(cfg, P, lens):
+    """Algorithmic HBM bytes of one fused verify pass per stage: every operand
+    read once and every output written once, in the storage types of the
+    path (fp16 GEMM weights and activations, fp16 K/V caches, fp32 residual
+    stream and partials). Precise-layer remainder planes are left out (an
+    implementation choice, not the method's work)."""
+    d, hq, hkv, hd, F, V = (cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.d_ff,
+                            cfg.vocab)
+    L = cfg.n_layers
+    T = int(sum(lens))
+    rows = P + T
+    body = rows * max(L - 1, 0) + (T + 1 if L else 0)   # rows past attention
+    qd = hq * hd
+    kv = 2 * hkv * hd * 2                                # K + V bytes per position
+    b = {"verify.qkv_rope": L * cfg.qkv_rows * d * 2 + rows * L * (d * 2 + qd * 2 + kv),
+         "verify.o_proj": L * d * qd * 2 + body * (qd * 2 + d * 8),
+         "verify.gate_up_swiglu": L * 2 * F * d * 2 + body * (d * 2 + F * 2),
+         "verify.down_proj": L * d * F * 2 + body * (F * 2 + d * 8),
+         # prefix keys/values once per layer, queries in, outputs out
+         "verify.attention": L * P * kv + (P * max(L - 1, 0) + 1) * qd * 4,
+         # the prefix keys/values once for all candidates, their own keys, q, out
+         "verify.cand_attention": L * (P * kv + T * kv + T * qd * 4),
+         # LM head once, inputs, per-chunk partials and target logits
+         "verify.lm_head_lse": V * d * 2 + T * d * 2 + (V // 256 + 1) * T * 8 + T * 4,
+         # two norms per layer: fp32 rows in, fp16 rows out
+         "verify.rmsnorm": (rows * max(L - 1, 0) + rows + (T + 1 if L else 0)) * d * 6,
+         "verify.embed": rows * d * 6}
+    return b
+
+
+def stage_row(fl, nb, ms):
+    """One breakdown row: achieved rates and the roofline position."""
+    sec = ms * 1e-3
+    row = {"ms": round(ms, 3)}
+    t_mfma = fl / (PEAK_BF16_TFLOPS * 1e12)
+    t_hbm = (nb or 0) / (PEAK_HBM_GBS * 1e9)
+    if fl:
+        row["tflops"] = round(fl / sec / 1e12, 1)
+        row["mfma_frac"] = round(fl / sec / 1e12 / PEAK_BF16_TFLOPS, 4)
+    if nb:
+        row["GBs"] = round(nb / sec / 1e9, 1)
+        row["hbm_frac"] = round(nb / sec / 1e9 / PEAK_HBM_GBS, 4)
+        row["flop_per_byte"] = round(fl / nb, 1) if fl else 0.0
+    row["bound"] = "mfma" if t_mfma >= t_hbm else "hbm"
+    row["frac"] = round(max(t_mfma, t_hbm) / sec, 4)
+    return row
+
+
 def measured_traffic(kname):
     """HBM bytes per launch of `kname` from the committed counter runs
     (profiles/traffic.json), or None if absent or if the kernel source has
@@ -195,41 +243,69 @@ def time_draft(dev, log_fn, reps=3):
     return res
 
 
-def cpu_baseline(wl, log_fn):
-    """The oracle (float64, shared-prefix mode) on the same workload with 1 and
-    2 of its layers; the per-layer cost is extrapolated to the full depth."""
-    import numpy as np
-    import oracle
+def blas_info():
+    """(threads, vendor string) of the BLAS numpy uses."""
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()
-                       if i.get("user_api") == "blas"] or [os.cpu_count() or 1])
+        for i in threadpool_info():
+            if i.get("user_api") == "blas":
+                return (int(i.get("num_threads", 1)),
+                        f"{i.get('internal_api')} {i.get('version')} "
+                        f"({i.get('threading_layer')}, {i.get('architecture')})")
     except Exception:
-        threads = os.cpu_count() or 1
+        pass
+    return 1, "unknown"
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, log_fn, sample_layers=3):
+    """The plain fp32 oracle (oracle.score_shared_prefix, float32) on this
+    workload's own inputs, with its first `sample_layers` layers: one bounded
+    run, timed per part (embedding + host copies, each layer, LM head), and
+    the per-layer time scaled to the full depth."""
+    import numpy as np
+    import oracle
+    threads, vendor = blas_info()
     cfg = wl.cfg
+    nl = min(sample_layers, cfg.n_layers)
+    t0 = time.perf_counter()
     hw = {"embed": W.to_host_f32(wl.weights["embed"]),
           "lm_head": W.to_host_f32(wl.weights["lm_head"]),
-          "final_norm": W.to_host_f32(wl.weights["final_norm"])}
+          "final_norm": W.to_host_f32(wl.weights["final_norm"]),
+          "layers": W.HostLayers(wl.weights["layers"][:nl])}
     vis = W.to_host_f32(wl.visual)
-    times = {}
-    for nl in (1, 2):
-        w = dict(hw, layers=W.HostLayers(wl.weights["layers"][:nl]))
-        c = cfg.replace(n_layers=nl)
-        t0 = time.perf_counter()
-        oracle.score_shared_prefix(c, w, vis, wl.prefix_ids, wl.cand_ids, wl.cand_len,
-                                   dtype=np.float64)
-        times[nl] = time.perf_counter() - t0
-        log_fn(f"cpu oracle: {nl} layer(s) in {times[nl]:.1f}s")
-    per_layer = max(times[2] - times[1], 1e-9)
-    base = max(times[1] - per_layer, 0.0)
-    full = base + per_layer * cfg.n_layers
+    marks = []
+    c = cfg.replace(n_layers=nl)
+    t1 = time.perf_counter()
+    oracle.score_shared_prefix(c, hw, vis, wl.prefix_ids, wl.cand_ids, wl.cand_len,
+                               dtype=np.float32, progress=lambda l: marks.append(time.perf_counter()))
+    t2 = time.perf_counter()
+    layer_s = [b - a for a, b in zip([t1] + marks[:-1], marks)]
+    per_layer = sum(layer_s) / len(layer_s)
+    tail = t2 - marks[-1]
+    full = (t1 - t0) + per_layer * cfg.n_layers + tail
+    log_fn(f"cpu oracle (fp32): setup {t1 - t0:.1f}s, layers "
+           f"{', '.join(f'{x:.1f}' for x in layer_s)}s, LM head {tail:.1f}s")
     tokens = int(sum(wl.cand_len))
-    return {"value": tokens / full, "unit": "candidate tokens/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": (f"float64 oracle, shared-prefix mode, on this workload with 1 and 2 of "
-                       f"its {cfg.n_layers} layers ({times[1]:.1f}s, {times[2]:.1f}s); "
-                       f"per-layer time extrapolated to {cfg.n_layers} layers = "
-                       f"{full:.1f}s per verify pass")}
+    return {"value": tokens / full, "unit": "candidate tokens/s",
+            "cores": max(threads, oracle.decoder.THREADS), "kind": "oracle",
+            "sample": (f"plain fp32 oracle (oracle.score_shared_prefix, float32, shared-prefix "
+                       f"mode) on this workload's inputs with its first {nl} of {cfg.n_layers} "
+                       f"layers in one run ({t2 - t0:.1f}s: host copies + embedding "
+                       f"{t1 - t0:.1f}s, {per_layer:.2f}s per layer, LM head {tail:.1f}s); "
+                       f"the per-layer time scaled to {cfg.n_layers} layers gives "
+                       f"{full:.1f}s per verify pass (extrapolated). Host: {cpu_model()}; "
+                       f"BLAS {vendor}, {threads} threads; attention heads on "
+                       f"{oracle.decoder.THREADS} threads")}
 
 
 def main():
@@ -307,6 +383,7 @@ def main():
     stages = v.profile_read()
     v.profile(False)
     flops = stage_flops(cfg, cfg.n_prefix, lens)
+    nbytes = stage_bytes(cfg, cfg.n_prefix, lens)
     per_step = {k: ms / nprof for k, (ms, n) in stages.items()}
     if args.stages:
         for k, ms in sorted(per_step.items(), key=lambda kv: -kv[1]):
@@ -319,14 +396,22 @@ def main():
 
     # Timed steps: events around the dominant kernel's launches only.
     v.profile(True, kinds=sorted({s.split(".", 1)[1] for s in kst}))
+    st = torch.cuda.current_stream(dev)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    marks[0].record(st)
+    for i in range(args.steps):
         step()
+        marks[i + 1].record(st)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     timed = v.profile_read()
     v.profile(False)
+    step_ms = sorted(a.elapsed_time(b) for a, b in zip(marks[:-1], marks[1:]))
+
+    def pct(q):
+        return round(step_ms[min(len(step_ms) - 1, int(round(q * (len(step_ms) - 1))))], 3)
 
     ms_step = (t1 - t0) * 1e3 / args.steps
     tokens = sum(lens)
@@ -350,8 +435,13 @@ def main():
         "metric": METRIC if args.workload == 2 else "candidate tokens scored/sec and ms per verify pass",
         "value": round(value, 1), "unit": "candidate tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 3), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16" if cfg.dtype == W.BF16 else "f32",
+        "ms_per_step": round(ms_step, 3),
+        "ms_per_step_p10_p50_p90": [pct(0.1), pct(0.5), pct(0.9)],
+        "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": (f"bf16 weights, fp16 MFMA operands, fp32 accumulation; "
+                  f"{v.c.split_layers} precise layer(s) with fp16 value+remainder operands"
+                  if cfg.dtype == W.BF16 else "f32"),
         "data": "synthetic (seeded, random-init weights)",
         "config": {"workload": cfg.name, "layers": cfg.n_layers, "d_model": cfg.d_model,
                    "heads": f"{cfg.n_heads}/{cfg.n_kv_heads}", "d_ff": cfg.d_ff,
@@ -359,14 +449,15 @@ def main():
                    "candidates": M, "cand_len": cmax, "tokens_scored": tokens},
         "breakdown": {"kernel_ms": round(total, 3), "gemm_ms": round(gemm, 3),
                       "attention_ms": round(attn, 3),
-                      # every stage with algorithmic FLOPs: ms per pass, TF/s
-                      # and fraction of the bf16 MFMA peak (untimed profiled pass)
-                      "stages": {k.split(".", 1)[1]: {
-                          "ms": round(per_step[k], 3),
-                          "tflops": round(flops[k] / (per_step[k] * 1e-3) / 1e12, 1),
-                          "frac": round(flops[k] / (per_step[k] * 1e-3) / 1e12
-                                        / PEAK_BF16_TFLOPS, 4)}
-                          for k in sorted(flops) if per_step.get(k, 0.0) > 0}},
+                      # every stage of the untimed profiled pass with its
+                      # algorithmic work: ms per pass, TF/s and GB/s, the
+                      # fractions of the bf16 MFMA peak and of HBM peak, the
+                      # bound its arithmetic intensity selects (ridge 312.5
+                      # FLOP/B) and the roofline fraction against that bound
+                      "stages": {k.split(".", 1)[1]: stage_row(flops.get(k, 0.0), nbytes.get(k),
+                                                               per_step[k])
+                                 for k in sorted(set(flops) | set(nbytes))
+                                 if per_step.get(k, 0.0) > 0}},
         "roofline": roofline,
     }
     if not args.no_next_rows:

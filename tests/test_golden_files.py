@@ -30,3 +30,9 @@ def test_golden_file_is_current_and_consistent(path):
         assert sorted(rec["cands"]) == list(range(cfg.n_cands))
         best = int(np.argmax(sc))
         assert rec["argmax"] == best
+
+
+def test_golden_set_covers_the_full_size_workloads():
+    have = {(load(p)["workload_index"], load(p)["seed"]) for p in FILES}
+    for w in (1, 2, 3, 4):
+        assert any(k[0] == w for k in have), f"no stored oracle output for workload {w}"
