@@ -245,7 +245,7 @@ int vsr_align_select(const float *ent, const float *frames, int32_t M, int32_t N
 /* Message of the last failed call on this context ("" if none). With
  * ctx == NULL: message of the last failed context-free call on this thread
  * (vsr_create, vsr_align_select, vsr_weights_to_f16, vsr_keyframes,
- * vsr_retrieve). */
+ * vsr_retrieve, vsr_retrieve_static). */
 const char *vsr_last_error(const vsr_ctx *ctx);
 
 /* Keyframes of a video (Section 3.1, Eq. 1). Each frame is compared with the
@@ -288,6 +288,24 @@ int vsr_retrieve(const float *frame_emb, const int32_t *key_idx, const int32_t *
                  int32_t NF, const float *docs, int32_t ND, int32_t D, int32_t k, int32_t K,
                  void *workspace, size_t ws_bytes, int32_t *top_idx, float *top_sim,
                  int32_t *sel_idx, float *sel_sim, int32_t *n_sel, void *hip_stream);
+
+/* vsr_retrieve for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same computation, arguments, outputs and errors as vsr_retrieve minus
+ * the workspace. The per-chunk partial lists live in a library-owned static
+ * device array of VSR_RETRIEVE_STATIC_BYTES (32 MiB) on each GPU the call runs
+ * on (the current device), allocated with the library's code on that GPU and
+ * held until the process ends; the call itself allocates nothing. Sizes whose
+ * vsr_retrieve_workspace_size(NF, ND, k) exceeds it (e.g. more than 1M
+ * documents at 220 keyframes and k = 3) fail with VSR_ERANGE. Every call on a
+ * GPU shares that GPU's array: calls that overlap in time on one GPU (two
+ * streams, or two host threads) race and must be serialised by the caller.
+ * Device indices up to 63. */
+#define VSR_RETRIEVE_STATIC_BYTES (32u << 20)
+int vsr_retrieve_static(const float *frame_emb, const int32_t *key_idx, const int32_t *n_keys,
+                        int32_t NF, const float *docs, int32_t ND, int32_t D, int32_t k,
+                        int32_t K, int32_t *top_idx, float *top_sim, int32_t *sel_idx,
+                        float *sel_sim, int32_t *n_sel, void *hip_stream);
 
 /* Weight preparation for gemm_weights = VSR_F16: writes the n bf16 values of
  * src (device) to dst (device, n fp16 values, not overlapping src) with the

@@ -19,10 +19,12 @@ VSR_CHECK_IDS, VSR_CHECK_FINITE = 1, 2
 VSR_F32, VSR_BF16, VSR_F16 = 0, 1, 2
 GEMM_WEIGHT_KEYS = ("wqkv", "wo", "wgu", "wdown")  # per layer, plus lm_head
 VSR_MAX_CANDS = 256
+VSR_RETRIEVE_STATIC_BYTES = 32 << 20
 
 EXPORTS = ["vsr_workspace_size", "vsr_create", "vsr_load_weights", "vsr_prefill",
            "vsr_score", "vsr_verify", "vsr_reliability", "vsr_draft", "vsr_align_select", "vsr_weights_to_f16",
-           "vsr_keyframes", "vsr_retrieve_workspace_size", "vsr_retrieve", "vsr_last_error",
+           "vsr_keyframes", "vsr_retrieve_workspace_size", "vsr_retrieve", "vsr_retrieve_static",
+           "vsr_last_error",
            "vsr_destroy", "vsr_set_checks", "vsr_profile_enable", "vsr_profile_read"]
 
 VSR_SELECT_TWO_STAGE, VSR_SELECT_ADDITION, VSR_SELECT_INVERT = 0, 1, 2
@@ -127,6 +129,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                  ctypes.c_void_p, ctypes.c_void_p]
     lib.vsr_retrieve.restype = ctypes.c_int
+    lib.vsr_retrieve_static.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+                                        ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.vsr_retrieve_static.restype = ctypes.c_int
     lib.vsr_last_error.argtypes = [ctypes.c_void_p]
     lib.vsr_last_error.restype = ctypes.c_char_p
     lib.vsr_destroy.argtypes = [ctypes.c_void_p]
@@ -436,6 +444,16 @@ class Retriever:
             self.ND, self.D, self.k, self.K, _ptr(self.ws), self.ws.numel(), _ptr(self.top_idx),
             _ptr(self.top_sim), _ptr(self.sel_idx), _ptr(self.sel_sim), _ptr(self.n_sel),
             self.stream.cuda_stream))
+        return self.top_idx, self.top_sim, self.sel_idx, self.sel_sim, self.n_sel
+
+    def retrieve_static(self, frame_emb, docs):
+        """retrieve() through vsr_retrieve_static: the library's static
+        scratch instead of this object's workspace (no allocation in the call)."""
+        self._emb = (frame_emb, docs)
+        self._check(self.lib.vsr_retrieve_static(
+            _ptr(frame_emb), _ptr(self.key_idx), _ptr(self.n_keys), self.NF, _ptr(docs),
+            self.ND, self.D, self.k, self.K, _ptr(self.top_idx), _ptr(self.top_sim),
+            _ptr(self.sel_idx), _ptr(self.sel_sim), _ptr(self.n_sel), self.stream.cuda_stream))
         return self.top_idx, self.top_sim, self.sel_idx, self.sel_sim, self.n_sel
 
 

@@ -142,6 +142,14 @@ hipError_t launch_retrieve(const float *frame_emb, const int32_t *key_idx, const
                            int32_t *top_idx, float *top_sim, int32_t *sel_idx, float *sel_sim,
                            int32_t *n_sel, hipStream_t s);
 
+// Retrieval with library-owned scratch (vsr_retrieve_static): the size of
+// the file-scope device array, and its device address on the current device
+// (looked up once per device; the largest device index it serves is
+// kMaxDevices - 1).
+constexpr size_t kRetrieveStaticBytes = size_t(32) << 20;
+constexpr int kMaxDevices = 64;
+hipError_t retrieve_static_scratch(void **ptr);
+
 // Per-row merge of the LM-head partials: lse over the vocabulary chunks,
 // lp = target logit - lse, scattered to logprobs[m][j] (zeros elsewhere).
 hipError_t launch_lse_gather(const Branches &br, const float2 *part, int nchunks,

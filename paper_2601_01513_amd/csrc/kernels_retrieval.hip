@@ -6,6 +6,8 @@
 // calls give identical results: histogram counts are integer LDS atomics;
 // the keyframe test compares an integer sum with theta * 3HW in float64;
 // rankings break ties by the lower document index.
+#include <mutex>
+
 #include "common.h"
 
 namespace vsr {
@@ -504,6 +506,36 @@ hipError_t launch_retrieve(const float *frame_emb, const int32_t *key_idx, const
   k_retrieve_merge<<<NF, MERGE_T, 0, s>>>(part, n_keys, nchunks, k, top_idx, top_sim);
   k_select_docs<<<1, 1024, 0, s>>>(top_idx, top_sim, n_keys, k, K, sel_idx, sel_sim, n_sel);
   return hipGetLastError();
+}
+
+// ---- the same retrieval with library-owned scratch ------------------------
+// For callers that cannot allocate device memory: the per-chunk partial lists
+// live in this file-scope array (one copy per GPU, held until the process
+// ends). Host code never passes the array's name to a kernel: it is a
+// host-side stand-in there. The device address comes from
+// hipGetSymbolAddress, looked up once per device with that device current.
+static __device__ __align__(256) unsigned char scratch[kRetrieveStaticBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t retrieve_static_scratch(void **ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace vsr

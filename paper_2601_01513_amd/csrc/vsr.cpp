@@ -1154,6 +1154,47 @@ extern "C" int vsr_retrieve(const float *frame_emb, const int32_t *key_idx,
   return VSR_OK;
 }
 
+extern "C" int vsr_retrieve_static(const float *frame_emb, const int32_t *key_idx,
+                                   const int32_t *n_keys, int32_t NF, const float *docs,
+                                   int32_t ND, int32_t D, int32_t k, int32_t K,
+                                   int32_t *top_idx, float *top_sim, int32_t *sel_idx,
+                                   float *sel_sim, int32_t *n_sel, void *hip_stream) {
+  g_create_error.clear();
+  const char *msg = retrieve_sizes_error(NF, ND, k);
+  if (!msg) {
+    if (!frame_emb || !key_idx || !n_keys || !docs || !top_idx || !top_sim || !sel_idx ||
+        !sel_sim || !n_sel)
+      msg = "retrieve_static: NULL argument";
+    else if (D < 1 || D > 1024) msg = "D must lie in [1, 1024]";
+    else if (K < 1 || K > 64) msg = "K must lie in [1, 64]";
+    else if (reinterpret_cast<uintptr_t>(docs) & 15) msg = "docs must be 16-byte aligned";
+  }
+  if (msg) {
+    g_create_error = msg;
+    return VSR_EINVAL;
+  }
+  const size_t need = retrieve_workspace_bytes(NF, ND, k);
+  if (need > kRetrieveStaticBytes) {
+    char buf[256];
+    snprintf(buf, sizeof buf,
+             "retrieve_static: NF=%d, ND=%d, k=%d need %zu bytes of scratch, more than the "
+             "library's %zu (use vsr_retrieve with a workspace)",
+             NF, ND, k, need, kRetrieveStaticBytes);
+    g_create_error = buf;
+    return VSR_ERANGE;
+  }
+  void *scratch = nullptr;
+  hipError_t e = retrieve_static_scratch(&scratch);
+  if (e == hipSuccess)
+    e = launch_retrieve(frame_emb, key_idx, n_keys, NF, docs, ND, D, k, K, scratch, top_idx,
+                        top_sim, sel_idx, sel_sim, n_sel, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) {
+    g_create_error = std::string("HIP error in retrieve_static: ") + hipGetErrorString(e);
+    return VSR_EHIP;
+  }
+  return VSR_OK;
+}
+
 extern "C" int vsr_weights_to_f16(const void *src, void *dst, size_t n, void *hip_stream) {
   g_create_error.clear();
   const uintptr_t a = reinterpret_cast<uintptr_t>(src), b = reinterpret_cast<uintptr_t>(dst);

@@ -218,6 +218,28 @@ def test_retrieval_calls_reject_bad_arguments():
         assert word in lib.vsr_last_error(None), (bad, lib.vsr_last_error(None))
 
 
+def test_retrieve_static_rejects_bad_arguments_and_oversize():
+    """Argument and size checks of the no-allocation retrieval run before any
+    HIP call (the pointers below are never dereferenced)."""
+    lib = _lib()
+    r = dict(fe=0x10000, ki=0x20000, nk=0x30000, NF=220, docs=0x40000, ND=100_000, D=768, k=3,
+             K=3, ti=0x60000, ts=0x70000, si=0x80000, ss=0x90000, ns=0xA0000)
+
+    def rs(**kw):
+        a = dict(r, **kw)
+        return lib.vsr_retrieve_static(a["fe"], a["ki"], a["nk"], a["NF"], a["docs"], a["ND"],
+                                       a["D"], a["k"], a["K"], a["ti"], a["ts"], a["si"],
+                                       a["ss"], a["ns"], None)
+    for bad, word in ((dict(docs=None), b"NULL"), (dict(D=0), b"D must"), (dict(K=65), b"K must"),
+                      (dict(k=17), b"k must"), (dict(docs=0x40004), b"aligned")):
+        assert rs(**bad) == B.VSR_EINVAL, bad
+        assert word in lib.vsr_last_error(None), (bad, lib.vsr_last_error(None))
+    assert lib.vsr_retrieve_workspace_size(220, 1 << 24, 3) > B.VSR_RETRIEVE_STATIC_BYTES
+    assert lib.vsr_retrieve_workspace_size(220, 1_000_000, 3) <= B.VSR_RETRIEVE_STATIC_BYTES
+    assert rs(ND=1 << 24) == B.VSR_ERANGE
+    assert b"scratch" in lib.vsr_last_error(None)
+
+
 def test_set_checks_without_context_fails_cleanly():
     lib = _lib()
     assert lib.vsr_set_checks(None, B.VSR_CHECK_IDS) == B.VSR_EINVAL
