@@ -70,11 +70,14 @@ class VsrError(RuntimeError):
 _lib = None
 
 
-def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
-    """Loads libvsr.so (raises if it has not been built)."""
+def load_library(path: Optional[str] = None) -> ctypes.CDLL:
+    """Loads libvsr.so (raises if it has not been built). The path defaults to
+    the in-tree build; the VSR_LIBRARY environment variable names another
+    build of the same library (e.g. to compare two builds on one machine)."""
     global _lib
     if _lib is not None:
         return _lib
+    path = path or os.environ.get("VSR_LIBRARY") or LIB_PATH
     if not os.path.exists(path):
         raise RuntimeError(
             f"{path} is missing: build it with `python -m paper_2601_01513_amd.build`")
