@@ -189,11 +189,6 @@ struct QKVOut {
   const int32_t *row_pos2 = nullptr;
 };
 
-// Stores one rotate-half pair (dims d and d + 64 of head slot `slot` of the
-// stacked q | k | v projection) of row `row`: rotary on q and k at the row's
-// position, then q to its rows, k to the key cache and v to the Vt cache (at
-// the attention kernel's interleaved position), each with its fp16 remainder
-// where the remainder planes are given. head_dim 128.
 // Rotary position of row `row`.
 __device__ __forceinline__ int qkv_row_pos(const QKVOut<f16> &o, int row) {
   // One load through a selected pointer (two loads into one register in
@@ -203,19 +198,12 @@ __device__ __forceinline__ int qkv_row_pos(const QKVOut<f16> &o, int row) {
   return p ? *p : row;
 }
 
-// qkv_store with the rotary-table entry of (row's position, d) given as cs
-// (unused for value slots), so that a caller can load the entries of many
-// rows before it stores any of them.
-__device__ __forceinline__ void qkv_store_cs(const QKVOut<f16> &o, int n_heads, int n_kv,
-                                             int slot, int row, int d, float x1, float x2,
-                                             float2 cs) {
+// qkv_store without the rotary: x1, x2 are the pair as stored (queries and
+// keys already rotated).
+__device__ __forceinline__ void qkv_store_rotated(const QKVOut<f16> &o, int n_heads, int n_kv,
+                                                  int slot, int row, int d, float x1, float x2) {
   const bool second = row >= o.split;  // a candidate row of a fused pass
   const int row2 = row - o.split;
-  if (slot < n_heads + n_kv) {
-    const float y1 = x1 * cs.x - x2 * cs.y, y2 = x2 * cs.x + x1 * cs.y;
-    x1 = y1;
-    x2 = y2;
-  }
   const f16 h1 = static_cast<f16>(x1), h2 = static_cast<f16>(x2);
   const f16 l1 = static_cast<f16>(x1 - static_cast<float>(h1));
   const f16 l2 = static_cast<f16>(x2 - static_cast<float>(h2));
@@ -256,6 +244,29 @@ __device__ __forceinline__ void qkv_store_cs(const QKVOut<f16> &o, int n_heads, 
   }
 }
 
+// The rotate-half pair of query / key slots turned by the rotary-table entry
+// cs of (row's position, d).
+__device__ __forceinline__ void rope_pair(float &x1, float &x2, float2 cs) {
+  const float y1 = x1 * cs.x - x2 * cs.y, y2 = x2 * cs.x + x1 * cs.y;
+  x1 = y1;
+  x2 = y2;
+}
+
+// qkv_store with the rotary-table entry given as cs (unused for value slots),
+// so that a caller can load the entries of many rows before it stores any of
+// them.
+__device__ __forceinline__ void qkv_store_cs(const QKVOut<f16> &o, int n_heads, int n_kv,
+                                             int slot, int row, int d, float x1, float x2,
+                                             float2 cs) {
+  if (slot < n_heads + n_kv) rope_pair(x1, x2, cs);
+  qkv_store_rotated(o, n_heads, n_kv, slot, row, d, x1, x2);
+}
+
+// Stores one rotate-half pair (dims d and d + 64 of head slot `slot` of the
+// stacked q | k | v projection) of row `row`: rotary on q and k at the row's
+// position, then q to its rows, k to the key cache and v to the Vt cache (at
+// the attention kernel's interleaved position), each with its fp16 remainder
+// where the remainder planes are given. head_dim 128.
 __device__ __forceinline__ void qkv_store(const QKVOut<f16> &o, int n_heads, int n_kv, int slot,
                                           int row, int d, float x1, float x2) {
   const float2 cs = slot < n_heads + n_kv ? o.rope[(long)qkv_row_pos(o, row) * 64 + d]

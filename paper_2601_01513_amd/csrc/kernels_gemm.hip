@@ -533,6 +533,96 @@ __global__ __launch_bounds__(256) void k_reduce_swiglu(const float *__restrict__
 }
 
 // ------------------------------------------------- QKV + rotary + KV caches
+// Staged stores. A 64-row block of one head slot (a wave's outputs, or a
+// quarter of a summed tail tile) passes through 16 KB of LDS and leaves in
+// 16-byte stores, each store instruction covering whole 128-byte lines.
+// Stored straight from the accumulators, a lane wrote 2 bytes: a value tile,
+// transposed into the Vt cache, touched 64 lines per store instruction.
+//
+// Row form (queries, keys): [64 rows][128 dims], 256 B a row; chunk c of row
+// s sits at c ^ 4 ((s / 4) % 2), so the rows s and s + 4 written by the two
+// half-waves of one accumulator register fall in different banks.
+__device__ __forceinline__ int stg_row(int s, int d) {
+  return s * 128 + (((d >> 3) ^ (((s >> 2) & 1) << 2)) << 3) + (d & 7);
+}
+// Transposed form (values): [128 dims][64 cache positions], 128 B a dim;
+// chunk C of dim e sits at C ^ ((e / 2) % 8).
+__device__ __forceinline__ int stg_vt(int e, int p) {
+  return e * 64 + (((p >> 3) ^ ((e >> 1) & 7)) << 3) + (p & 7);
+}
+// Position (within its aligned group of 16) that the Vt interleave gives
+// position p: quarters 1 and 2 swap. Groups of 4 stay contiguous.
+__device__ __forceinline__ int vt_interleave(int p) {
+  return (p & ~12) | ((p & 4) << 1) | ((p & 8) >> 1);
+}
+
+__device__ __forceinline__ bool aligned16(const void *p) {
+  return (reinterpret_cast<uintptr_t>(p) & 15) == 0;
+}
+
+// Destination of a staged 64-row block of a value slot: Vt cache rows at
+// positions crow0 .. crow0 + 63. Only blocks whose rows are all valid, lie
+// in one cache and start at a multiple of 16 there (the interleave then maps
+// the block onto itself) are staged; the rest are stored element by element.
+struct VtBlock {
+  f16 *vt;
+  int npos, crow0;
+};
+__device__ __forceinline__ bool vt_block(const QKVOut<f16> &o, int n_heads, int n_kv, int slot,
+                                         int r0, int rows, VtBlock &b) {
+  if (o.cache_row || r0 + 64 > rows) return false;
+  const bool first = r0 + 64 <= o.split;
+  const bool second = r0 >= o.split && (o.split & 15) == 0;
+  if (!first && !second) return false;
+  b.npos = second ? o.kv_npos2 : o.kv_npos;
+  f16 *vt = second ? o.vt2 : o.vt;
+  b.vt = vt + (long)(slot - n_heads - n_kv) * 128 * b.npos;
+  b.crow0 = second ? r0 - o.split : r0;
+  return (b.npos & 7) == 0 && aligned16(vt);
+}
+
+// Query and key destinations 16-byte aligned (their rows are 256 B).
+__device__ __forceinline__ bool qk_staged_ok(const QKVOut<f16> &o) {
+  return aligned16(o.q) && aligned16(o.k) && aligned16(o.k2);
+}
+
+// Destination of row `row` of query / key slot `slot`; NULL past the rows.
+__device__ __forceinline__ f16 *qk_row_dst(const QKVOut<f16> &o, int n_heads, int slot, int row,
+                                           int rows) {
+  if (row >= rows) return nullptr;
+  if (slot < n_heads) return o.q + ((long)row * n_heads + slot) * 128;
+  const bool second = row >= o.split;
+  f16 *k = second ? o.k2 : o.k;
+  const int crow = second ? row - o.split : o.cache_row ? o.cache_row[row] : row;
+  const int npos = second ? o.kv_npos2 : o.kv_npos;
+  return k + ((long)(slot - n_heads) * npos + crow) * 128;
+}
+
+// Copy-out of a staged block by one wave: store rounds it0 .. it0 + NIT - 1
+// of 16 (a round: 64 lanes x 16 B, 4 rows or 8 dims).
+template <int NIT>
+__device__ __forceinline__ void qk_copy_out(const f16 *stg, const QKVOut<f16> &o, int n_heads,
+                                            int slot, int r0, int rows, int it0) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll 2
+  for (int it = it0; it < it0 + NIT; ++it) {
+    const int s = it * 4 + (lane >> 4), c = lane & 15;
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(stg + stg_row(s, c * 8));
+    f16 *p = qk_row_dst(o, n_heads, slot, r0 + s, rows);
+    if (p) *reinterpret_cast<u32x4 *>(p + c * 8) = v;
+  }
+}
+template <int NIT>
+__device__ __forceinline__ void vt_copy_out(const f16 *stg, f16 *dst, int npos, int crow0, int it0) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll 2
+  for (int it = it0; it < it0 + NIT; ++it) {
+    const int e = it * 8 + (lane >> 3), c = lane & 7;
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(stg + stg_vt(e, c * 8));
+    *reinterpret_cast<u32x4 *>(dst + (long)e * npos + crow0 + c * 8) = v;
+  }
+}
+
 // Column tile = two heads of the stacked q|k|v projection; wave column wn owns
 // head slot 2 tn + wn. MFMA blocks fn and fn+2 hold head dims d and d + 64,
 // the rotate-half pair.
@@ -543,6 +633,7 @@ __global__ __launch_bounds__(NT) void k_gemm_qkv(const f16 *__restrict__ A,
                                                  Launch ln,
                                                  QKVOut<f16> o, float *__restrict__ part) {
   static_assert(TL::WN == 2 && TL::TN == 128 && TL::BN == 256, "one head per wave column");
+  static_assert(TL::TM == 64 && TL::STAGE * 2 >= NWAVES * 1024, "a 16 KB staging block per wave");
   __shared__ u32x4 lds[2 * TL::STAGE];
   const Work wk = block_work(ln);
   const int nslots = n_heads + 2 * n_kv, nrows = nslots * 128;
@@ -558,11 +649,36 @@ __global__ __launch_bounds__(NT) void k_gemm_qkv(const f16 *__restrict__ A,
     store_partial<TL>(acc, part, ln, wk);
     return;
   }
+  // The main loop ends on a barrier after its last LDS reads, so each wave
+  // may now use its own 16 KB of the ring as a staging block. Precise layers
+  // (remainder planes too) store element by element.
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w / TL::WN, wn = w % TL::WN;
   const int slot = wk.tn * 2 + wn;
   if (slot >= nslots) return;
+  const int r0 = m0 + wm * TL::TM;
+  const bool precise = o.q_lo || o.k_lo || o.vt_lo;
+  f16 *stg = reinterpret_cast<f16 *>(lds + w * 1024);
   if (slot >= n_heads + n_kv) {  // values: no rotary
+    VtBlock vb;
+    if (!precise && vt_block(o, n_heads, n_kv, slot, r0, rows, vb)) {
+      // Lane rows 8 q + 4 (lane / 32) + j (j < 4) of MFMA row block fm go to
+      // interleaved positions 32 fm + 16 (q / 2) + 8 (lane / 32) + 4 (q % 2) + j.
+#pragma unroll
+      for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < TL::FN; ++fn)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            f16x4 h;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) h[j] = static_cast<f16>(acc[fm][fn][4 * q + j]);
+            const int p = 32 * fm + 16 * (q >> 1) + 8 * (lane >> 5) + 4 * (q & 1);
+            *reinterpret_cast<f16x4 *>(stg + stg_vt(fn * 32 + (lane & 31), p)) = h;
+          }
+      vt_copy_out<16>(stg, vb.vt, vb.npos, vb.crow0, 0);
+      return;
+    }
 #pragma unroll
     for (int fm = 0; fm < TL::FM; ++fm)
 #pragma unroll
@@ -571,15 +687,16 @@ __global__ __launch_bounds__(NT) void k_gemm_qkv(const f16 *__restrict__ A,
         if (row >= rows) continue;
 #pragma unroll
         for (int fn = 0; fn < 2; ++fn)
-          qkv_store_cs(o, n_heads, n_kv, slot, row, fn * 32 + (lane & 31), acc[fm][fn][r],
-                       acc[fm][fn + 2][r], make_float2(1.f, 0.f));
+          qkv_store_rotated(o, n_heads, n_kv, slot, row, fn * 32 + (lane & 31), acc[fm][fn][r],
+                            acc[fm][fn + 2][r]);
       }
     return;
   }
   // Queries and keys: the positions and rotary-table entries of a block's 16
-  // rows are all loaded before any of its stores. The compiler cannot move a
-  // load above a store that may alias it, so loading them row by row waited
-  // out two memory round trips per row.
+  // rows are all loaded before any of them is used. (Loaded row by row
+  // between stores, they waited out two memory round trips per row: the
+  // compiler cannot move a load above a store that may alias it.)
+  const bool staged = !precise && qk_staged_ok(o);
 #pragma unroll
   for (int fm = 0; fm < TL::FM; ++fm) {
     int pos[16];
@@ -594,30 +711,92 @@ __global__ __launch_bounds__(NT) void k_gemm_qkv(const f16 *__restrict__ A,
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = m0 + acc_row<TL>(wm, fm, r, lane);
-      if (row >= rows) continue;
 #pragma unroll
-      for (int fn = 0; fn < 2; ++fn)
-        qkv_store_cs(o, n_heads, n_kv, slot, row, fn * 32 + (lane & 31), acc[fm][fn][r],
-                     acc[fm][fn + 2][r], cs[r][fn]);
+      for (int fn = 0; fn < 2; ++fn) {
+        const int d = fn * 32 + (lane & 31);
+        if (staged) {
+          float x1 = acc[fm][fn][r], x2 = acc[fm][fn + 2][r];
+          rope_pair(x1, x2, cs[r][fn]);
+          const int sr = acc_row<TL>(0, fm, r, lane);
+          stg[stg_row(sr, d)] = static_cast<f16>(x1);
+          stg[stg_row(sr, d + 64)] = static_cast<f16>(x2);
+        } else if (row < rows) {
+          qkv_store_cs(o, n_heads, n_kv, slot, row, d, acc[fm][fn][r], acc[fm][fn + 2][r],
+                       cs[r][fn]);
+        }
+      }
     }
   }
+  if (staged) qk_copy_out<16>(stg, o, n_heads, slot, r0, rows, 0);
 }
 
-// Tail tiles: rotary + cache scatter from the summed partials. Block (tail
-// tile, half of its 256 rows); thread -> (row, head of the pair, d < 64).
+// Tail tiles: the partials summed in split order, then the rotary and the
+// staged stores as above. Block (tail tile, 64-row quarter), 4 waves: wave w
+// sums head h = w % 2 of the pair for the 4-row groups g = 2 it + w / 2
+// (it < 8), then stores its half of that head's staging block.
 __global__ __launch_bounds__(256) void k_reduce_qkv(const float *__restrict__ part, Launch ln,
                                                     int rows, int n_heads, int n_kv,
                                                     QKVOut<f16> o) {
-  const int i = blockIdx.x / 128, e = (blockIdx.x % 128) * 256 + threadIdx.x;
+  __shared__ u32x4 lds[2 * 1024];  // a 16 KB staging block per head
+  const int i = blockIdx.x >> 2, quarter = blockIdx.x & 3;
   int tm, tn;
   tile_coords(ln.ndp + i, ln.nm, ln.nn, ln.gm, tm, tn);
-  const int lr = e / 128, hh = (e % 128) / 64, d = e % 64;
-  const int row = tm * 256 + lr, slot = tn * 2 + hh;
-  if (row >= rows || slot >= n_heads + 2 * n_kv) return;
-  const int c = hh * 128 + d;
-  const float x1 = sum_partials(part, ln, i, lr * 256 + c);
-  const float x2 = sum_partials(part, ln, i, lr * 256 + c + 64);
-  qkv_store(o, n_heads, n_kv, slot, row, d, x1, x2);
+  const int w = threadIdx.x >> 6, h = w & 1, d = threadIdx.x & 63;
+  const int slot = tn * 2 + h, nslots = n_heads + 2 * n_kv;
+  const bool live = slot < nslots, value = slot >= n_heads + n_kv;
+  const int r0 = tm * 256 + quarter * 64;
+  f16 *stg = reinterpret_cast<f16 *>(lds + h * 1024);
+  const bool precise = o.q_lo || o.k_lo || o.vt_lo;
+  VtBlock vb;
+  const bool staged = live && !precise &&
+                      (value ? vt_block(o, n_heads, n_kv, slot, r0, rows, vb) : qk_staged_ok(o));
+#pragma unroll
+  for (int it = 0; it < 8; ++it) {
+    const int g = 2 * it + (w >> 1);
+    float x1[4], x2[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = (quarter * 64 + 4 * g + j) * 256 + h * 128 + d;
+      x1[j] = sum_partials(part, ln, i, e);
+      x2[j] = sum_partials(part, ln, i, e + 64);
+    }
+    if (!live) continue;
+    if (!value) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int row = min(r0 + 4 * g + j, rows - 1);
+        rope_pair(x1[j], x2[j], o.rope[(long)qkv_row_pos(o, row) * 64 + d]);
+      }
+    }
+    if (!staged) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (r0 + 4 * g + j < rows)
+          qkv_store_rotated(o, n_heads, n_kv, slot, r0 + 4 * g + j, d, x1[j], x2[j]);
+    } else if (value) {
+      f16x4 a, b;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        a[j] = static_cast<f16>(x1[j]);
+        b[j] = static_cast<f16>(x2[j]);
+      }
+      const int p = vt_interleave(4 * g);
+      *reinterpret_cast<f16x4 *>(stg + stg_vt(d, p)) = a;
+      *reinterpret_cast<f16x4 *>(stg + stg_vt(d + 64, p)) = b;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        stg[stg_row(4 * g + j, d)] = static_cast<f16>(x1[j]);
+        stg[stg_row(4 * g + j, d + 64)] = static_cast<f16>(x2[j]);
+      }
+    }
+  }
+  __syncthreads();
+  if (!staged) return;
+  if (value)
+    vt_copy_out<8>(stg, vb.vt, vb.npos, vb.crow0, 8 * (w >> 1));
+  else
+    qk_copy_out<8>(stg, o, n_heads, slot, r0, rows, 8 * (w >> 1));
 }
 
 // ------------------------------------------------------ LM head + chunk LSE
@@ -829,7 +1008,7 @@ hipError_t gemm_qkv_rope(const f16 *A, const void *W, bool w_f16, int rows, int 
                                 K / BK * asplit);
   VSR_WLAUNCH(k_gemm_qkv, ln.blocks(), A, W16, rows, K, asplit, n_heads, n_kv, ln, out, part);
   if (ln.ntail > 0)
-    k_reduce_qkv<<<ln.ntail * 128, 256, 0, s>>>(part, ln, rows, n_heads, n_kv, out);
+    k_reduce_qkv<<<ln.ntail * 4, 256, 0, s>>>(part, ln, rows, n_heads, n_kv, out);
   return hipGetLastError();
 }
 
