@@ -187,6 +187,9 @@ struct QKVOut {
   T *k2 = nullptr, *vt2 = nullptr, *k2_lo = nullptr, *vt2_lo = nullptr;
   int kv_npos2 = 0;
   const int32_t *row_pos2 = nullptr;
+  // Queries are stored multiplied by q_scale (after the rotary): the fast
+  // attention kernels take them pre-scaled by log2(e) / sqrt(hd).
+  float q_scale = 1.f;
 };
 
 // Rotary position of row `row`.
@@ -252,13 +255,23 @@ __device__ __forceinline__ void rope_pair(float &x1, float &x2, float2 cs) {
   x2 = y2;
 }
 
+// Rotary of a query / key pair (entry cs), then the query scale.
+__device__ __forceinline__ void qk_turn(const QKVOut<f16> &o, int n_heads, int n_kv, int slot,
+                                        float &x1, float &x2, float2 cs) {
+  if (slot < n_heads + n_kv) rope_pair(x1, x2, cs);
+  if (slot < n_heads) {
+    x1 *= o.q_scale;
+    x2 *= o.q_scale;
+  }
+}
+
 // qkv_store with the rotary-table entry given as cs (unused for value slots),
 // so that a caller can load the entries of many rows before it stores any of
 // them.
 __device__ __forceinline__ void qkv_store_cs(const QKVOut<f16> &o, int n_heads, int n_kv,
                                              int slot, int row, int d, float x1, float x2,
                                              float2 cs) {
-  if (slot < n_heads + n_kv) rope_pair(x1, x2, cs);
+  qk_turn(o, n_heads, n_kv, slot, x1, x2, cs);
   qkv_store_rotated(o, n_heads, n_kv, slot, row, d, x1, x2);
 }
 

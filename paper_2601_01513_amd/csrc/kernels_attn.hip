@@ -18,13 +18,16 @@
 // product is permuted to the key order the S^T accumulator leaves in each
 // lane, and the Vt cache stores positions in the matching order (within each
 // aligned group of 16 positions the middle two quarters are swapped), so a
-// lane's V^T operand is one 16-byte LDS read. Softmax runs online in fp32:
-// the reference maximum is kept on the raw scores and the scale folds into
-// the exponent, exp2(s * c - m * c) with c = log2(e) / sqrt(hd), one FMA per
-// score; the reference moves (and the output is rescaled) only when a tile's
-// maximum exceeds it by a factor 2^8 after scaling. A query's 64 keys of a
-// tile sit in two lanes (l, l ^ 32), combined by v_permlane32_swap; operands
-// (queries, keys, values, probabilities) are fp16.
+// lane's V^T operand is one 16-byte LDS read. Softmax runs online in fp32
+// with c = log2(e) / sqrt(hd): the fast kernels take queries already
+// multiplied by c (the QKV epilogue does it), start the S^T products from -m
+// so each probability is one exp2, and add the row sums with v_dot2 over the
+// fp16 probabilities; the precise kernels keep the reference on the raw
+// scores, exp2(s * c - m * c). Either way the reference moves (and the
+// output is rescaled) only when a tile's maximum exceeds it by a factor 2^8
+// after scaling. A query's 64 keys of a tile sit in two lanes (l, l ^ 32),
+// combined by v_permlane32_swap; operands (queries, keys, values,
+// probabilities) are fp16.
 //
 // The candidate and draft passes may split a block's keys (prefix tiles, then
 // branch tiles) into chunks (more blocks on the chip); each chunk writes (max,
@@ -98,6 +101,8 @@ struct Lane {
              // the keys (the halves are added once, after the walk)
   float thr; // 8 / c: probabilities stay below 2^8 between moves
   f32x16 o[HD / 32];
+  f32x16 negm;  // fast kernels: -m in every element (the S^T products start from it)
+  bool seen;    // fast kernels: a key of this query was visible (in either lane half)
   f16x8 qh[HD / 16], ql[HD / 16];  // chunks 2kk + h of the row (precise: hi / lo)
 };
 
@@ -237,6 +242,111 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *st
     }
 }
 
+// Largest of the 32 scores a lane holds for one tile, as a tree of 3-input
+// maxima (depth 4 instead of a chain of 16).
+__device__ __forceinline__ float tile_max(const f32x16 (&s)[2]) {
+  float a[11];
+#pragma unroll
+  for (int i = 0; i < 10; ++i) {
+    const int j = 3 * i;
+    a[i] = fmaxf(fmaxf(s[j >> 4][j & 15], s[(j + 1) >> 4][(j + 1) & 15]),
+                 s[(j + 2) >> 4][(j + 2) & 15]);
+  }
+  a[10] = fmaxf(s[1][14], s[1][15]);
+  const float b0 = fmaxf(fmaxf(a[0], a[1]), a[2]), b1 = fmaxf(fmaxf(a[3], a[4]), a[5]);
+  const float b2 = fmaxf(fmaxf(a[6], a[7]), a[8]), b3 = fmaxf(a[9], a[10]);
+  return fmaxf(fmaxf(fmaxf(b0, b1), b2), b3);
+}
+
+// Fast kernels: one 64-key tile against this wave's 32 query rows. The
+// queries arrive multiplied by log2(e) / sqrt(hd), so S^T is in log2 units,
+// and the products start from -m (L.negm), so the accumulators hold s - m
+// and each probability is one exp2. The reference m moves (the output is
+// rescaled) only when a tile's largest s - m exceeds 8, or at the first
+// visible key of a row. The row sum adds the fp16 probabilities that the PV
+// products use (v_dot2_f32_f16 against ones, fp32 accumulation).
+template <bool MASK>
+__device__ __forceinline__ void tile_step_fast(const Seg &sg, int kb, const u32x4 *st, Lane &L) {
+  const int lane = threadIdx.x & 63, h = lane >> 5;
+  const u32x4 *Ks = st, *Vs = st + KCH;
+  f32x16 s[2];
+#pragma unroll
+  for (int kk = 0; kk < HD / 16; ++kk) {
+    const f16x8 qf = L.qh[kk];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const f16x8 kf = as_f16x8(Ks[ks_idx(b * 32 + (lane & 31), 2 * kk + h)]);
+      s[b] = mfma(kf, qf, kk == 0 ? L.negm : s[b]);
+    }
+  }
+  if constexpr (MASK) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kb + b * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        bool vis = key < sg.kvalid;
+        if (sg.mode == SEG_CAUSAL) vis = vis && key <= L.tok;
+        if (sg.mode == SEG_BRANCH) vis = vis && key >= L.lo && key <= L.tok;
+        s[b][r] = vis ? s[b][r] : -INFINITY;
+      }
+  }
+  // t and seen are the same in both lane halves of a query, so the two halves
+  // move together and keep one reference.
+  const float t = max_halves(tile_max(s));
+  const bool move = t > 8.f || (!L.seen && t != -INFINITY);
+  if (__builtin_amdgcn_ballot_w64(move)) {
+    // Rare: new reference m + d for the lanes that move (alpha rescales what
+    // was summed against the old one; nothing was before the first visible key).
+    const float d = move ? t : 0.f;
+    const float alpha = L.seen ? __builtin_amdgcn_exp2f(-d) : 0.f;
+    L.seen = L.seen || move;
+    L.m += d;
+    L.l *= alpha;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      L.negm[r] = -L.m;
+      s[0][r] -= d;
+      s[1][r] -= d;
+    }
+#pragma unroll
+    for (int db = 0; db < HD / 32; ++db) L.o[db] *= alpha;
+  }
+  f16x8 p[4];
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      p[b * 2 + (r >> 3)][r & 7] = static_cast<f16>(__builtin_amdgcn_exp2f(s[b][r]));
+  const f16x2 one = {static_cast<f16>(1.f), static_cast<f16>(1.f)};
+  float ps[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    ps[c] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      ps[c] = __builtin_amdgcn_fdot2(f16x2{p[c][2 * e], p[c][2 * e + 1]}, one, ps[c], false);
+  }
+  L.l += (ps[0] + ps[1]) + (ps[2] + ps[3]);
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int db = 0; db < HD / 32; ++db) {
+      const f16x8 vf = as_f16x8(Vs[vs_idx(db * 32 + (lane & 31), 2 * c + h)]);
+      L.o[db] = mfma(vf, p[c], L.o[db]);
+    }
+}
+
+// One tile of either variant.
+template <bool MASK, bool PREC>
+__device__ __forceinline__ void tile_any(const Seg &sg, int kb, const u32x4 *st, Lane &L,
+                                         float scale_log2) {
+  if constexpr (PREC)
+    tile_step<MASK, true>(sg, kb, st, L, scale_log2);
+  else
+    tile_step_fast<MASK>(sg, kb, st, L);
+}
+
 // Whether tile kb can skip the per-key mask for every row of the block.
 __device__ __forceinline__ bool tile_clear(const Seg &sg, int kb) {
   if (kb + KT > sg.kvalid) return false;
@@ -260,7 +370,7 @@ __device__ __forceinline__ void walk_segment(const Seg &sg, u32x4 *lds, Lane &L,
   for (; kb < sg.kend && tile_clear(sg, kb); kb += KT) {
     u32x4 *cur = lds + stage * STAGE;
     if (kb + KT < sg.kend) load_tile<PREC, DEC>(sg, kb + KT, lds + (stage ^ 1) * STAGE);
-    tile_step<false, PREC>(sg, kb, cur, L, scale_log2);
+    tile_any<false, PREC>(sg, kb, cur, L, scale_log2);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     stage ^= 1;
@@ -268,7 +378,7 @@ __device__ __forceinline__ void walk_segment(const Seg &sg, u32x4 *lds, Lane &L,
   for (; kb < sg.kend; kb += KT) {
     u32x4 *cur = lds + stage * STAGE;
     if (kb + KT < sg.kend) load_tile<PREC, DEC>(sg, kb + KT, lds + (stage ^ 1) * STAGE);
-    tile_step<true, PREC>(sg, kb, cur, L, scale_log2);
+    tile_any<true, PREC>(sg, kb, cur, L, scale_log2);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     stage ^= 1;
@@ -296,7 +406,7 @@ __device__ __forceinline__ void walk_concat(const Seg &sp, const Seg &sb, int pr
   for (; v < v1 && tile_clear(src(v), key0(v)); ++v) {
     u32x4 *cur = lds + stage * STAGE;
     if (v + 1 < v1) load_tile<PREC, DEC>(src(v + 1), key0(v + 1), lds + (stage ^ 1) * STAGE);
-    tile_step<false, PREC>(src(v), key0(v), cur, L, scale_log2);
+    tile_any<false, PREC>(src(v), key0(v), cur, L, scale_log2);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     stage ^= 1;
@@ -304,7 +414,7 @@ __device__ __forceinline__ void walk_concat(const Seg &sp, const Seg &sb, int pr
   for (; v < v1; ++v) {
     u32x4 *cur = lds + stage * STAGE;
     if (v + 1 < v1) load_tile<PREC, DEC>(src(v + 1), key0(v + 1), lds + (stage ^ 1) * STAGE);
-    tile_step<true, PREC>(src(v), key0(v), cur, L, scale_log2);
+    tile_any<true, PREC>(src(v), key0(v), cur, L, scale_log2);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     stage ^= 1;
@@ -336,8 +446,11 @@ __global__ __launch_bounds__((Shape<PREC, DEC>::NT)) void k_attn(AttnArgs a) {
   const int head = kvh * G + rowc % G;
   L.lo = MODE >= 1 ? a.row_lo[tok] : 0;
   L.tok = MODE == 2 ? a.q_pos[tok] : tok;
-  L.m = -INFINITY;
+  // Precise kernels: raw reference, none yet; fast kernels: log2 units, 0.
+  L.m = PREC ? -INFINITY : 0.f;
   L.l = 0.f;
+  L.negm = f32x16{};
+  L.seen = false;
 #pragma unroll
   for (int db = 0; db < HD / 32; ++db) L.o[db] = f32x16{};
   {
@@ -437,7 +550,11 @@ __global__ __launch_bounds__((Shape<PREC, DEC>::NT)) void k_attn(AttnArgs a) {
         *reinterpret_cast<f32x4 *>(pa + db * 32 + 8 * g4 + 4 * h) = v;
       }
     // The merge works in the scaled log2 domain.
-    if (h == 0) a.part_ml[prow] = make_float2(L.m * scale_log2, L.l);
+    if (h == 0) {
+      // A chunk with no visible key of this row reports m = -inf (no weight).
+      const float m = PREC ? L.m * scale_log2 : L.l == 0.f ? -INFINITY : L.m;
+      a.part_ml[prow] = make_float2(m, L.l);
+    }
   }
 }
 

@@ -716,7 +716,7 @@ __global__ __launch_bounds__(NT) void k_gemm_qkv(const f16 *__restrict__ A,
         const int d = fn * 32 + (lane & 31);
         if (staged) {
           float x1 = acc[fm][fn][r], x2 = acc[fm][fn + 2][r];
-          rope_pair(x1, x2, cs[r][fn]);
+          qk_turn(o, n_heads, n_kv, slot, x1, x2, cs[r][fn]);
           const int sr = acc_row<TL>(0, fm, r, lane);
           stg[stg_row(sr, d)] = static_cast<f16>(x1);
           stg[stg_row(sr, d + 64)] = static_cast<f16>(x2);
@@ -765,7 +765,8 @@ __global__ __launch_bounds__(256) void k_reduce_qkv(const float *__restrict__ pa
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int row = min(r0 + 4 * g + j, rows - 1);
-        rope_pair(x1[j], x2[j], o.rope[(long)qkv_row_pos(o, row) * 64 + d]);
+        qk_turn(o, n_heads, n_kv, slot, x1[j], x2[j],
+                o.rope[(long)qkv_row_pos(o, row) * 64 + d]);
       }
     }
     if (!staged) {

@@ -421,6 +421,8 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
     xn_ready = false;
     QKVOut<TA> qo;
     qo.q = q;
+    // The fast attention kernels take the queries pre-scaled (log2 units).
+    if (kMfma && !precise) qo.q_scale = 1.4426950408889634f / std::sqrt((float)cf.head_dim);
     qo.rope = c->at<float2>(p.rope);
     if (mode == 0 || fused) {
       qo.k = kc;
