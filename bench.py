@@ -98,8 +98,9 @@ def stage_bytes(cfg, P, lens):
          "verify.cand_attention": L * (P * kv + T * kv + T * qd * 4),
          # LM head once, inputs, per-chunk partials and target logits
          "verify.lm_head_lse": V * d * 2 + T * d * 2 + (V // 256 + 1) * T * 8 + T * 4,
-         # two norms per layer: fp32 rows in, fp16 rows out
-         "verify.rmsnorm": (rows * max(L - 1, 0) + rows + (T + 1 if L else 0)) * d * 6,
+         # two norms per layer (attention: every row; FFN: the rows past
+         # attention): fp32 rows in, fp16 rows out
+         "verify.rmsnorm": (rows * L + body) * d * 6,
          "verify.embed": rows * d * 6}
     return b
 

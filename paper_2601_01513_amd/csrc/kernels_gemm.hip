@@ -333,20 +333,34 @@ __device__ __forceinline__ void store_partial(const f32x16 (&acc)[TL::FM][TL::FN
 }
 
 // Sum of the partials of local element e (row * 256 + col) of tail tile i,
-// in split order. All kMaxSplit loads are issued before the first add (split
-// indices past nsplit re-read the last partial and are not added), so the
-// latencies overlap instead of adding up.
-__device__ __forceinline__ float sum_partials(const float *part, const Launch &ln, int i, int e) {
-  const float *p = part + (long)i * ln.nsplit * kTileElems + e;
-  float v[kMaxSplit];
+// in split order. The reduce kernels are instantiated per split count NS
+// (= ln.nsplit), so exactly NS loads are issued, all before the first add
+// (the latencies overlap instead of adding up).
+template <int NS>
+__device__ __forceinline__ float sum_partials(const float *part, int i, int e) {
+  const float *p = part + (long)i * NS * kTileElems + e;
+  float v[NS];
 #pragma unroll
-  for (int s = 0; s < kMaxSplit; ++s) v[s] = p[(long)min(s, ln.nsplit - 1) * kTileElems];
+  for (int s = 0; s < NS; ++s) v[s] = p[(long)s * kTileElems];
   float sum = 0.f;
 #pragma unroll
-  for (int s = 0; s < kMaxSplit; ++s)
-    if (s < ln.nsplit) sum += v[s];
+  for (int s = 0; s < NS; ++s) sum += v[s];
   return sum;
 }
+
+// Launch of reduce kernel `kern<NS>` for the launch's split count (2 .. 8).
+#define VSR_REDUCE_LAUNCH(ns, kern, grid, block, ...)                              \
+  do {                                                                            \
+    switch (ns) {                                                                 \
+      case 2: kern<2><<<grid, block, 0, s>>>(__VA_ARGS__); break;                 \
+      case 3: kern<3><<<grid, block, 0, s>>>(__VA_ARGS__); break;                 \
+      case 4: kern<4><<<grid, block, 0, s>>>(__VA_ARGS__); break;                 \
+      case 5: kern<5><<<grid, block, 0, s>>>(__VA_ARGS__); break;                 \
+      case 6: kern<6><<<grid, block, 0, s>>>(__VA_ARGS__); break;                 \
+      case 7: kern<7><<<grid, block, 0, s>>>(__VA_ARGS__); break;                 \
+      default: kern<kMaxSplit><<<grid, block, 0, s>>>(__VA_ARGS__); break;        \
+    }                                                                             \
+  } while (0)
 
 // silu(g) * u with the hardware reciprocal (about 1 ulp; the result is
 // rounded to fp16 next): an IEEE division here cost ten instructions per
@@ -426,6 +440,7 @@ __global__ __launch_bounds__(NT) void k_gemm_residual(const f16 *__restrict__ A,
 }
 
 // Tail tiles: x += sum of the partials. Block (tail tile, 256-element slab).
+template <int NS>
 __global__ __launch_bounds__(256) void k_reduce_residual(const float *__restrict__ part,
                                                          Launch ln, int rows, int N,
                                                          float *__restrict__ x) {
@@ -434,7 +449,7 @@ __global__ __launch_bounds__(256) void k_reduce_residual(const float *__restrict
   tile_coords(ln.ndp + i, ln.nm, ln.nn, ln.gm, tm, tn);
   const int row = tm * 256 + e / 256, col = tn * 256 + e % 256;
   if (row >= rows || col >= N) return;
-  x[(long)row * N + col] += sum_partials(part, ln, i, e);
+  x[(long)row * N + col] += sum_partials<NS>(part, i, e);
 }
 
 // ------------------------------------------------------------------- SwiGLU
@@ -517,6 +532,7 @@ __global__ __launch_bounds__(NT) void k_gemm_swiglu(const f16 *__restrict__ A,
 
 // Tail tiles: h = silu(gate) * up from the summed partials. Block (tail tile,
 // half of its 256 rows); thread -> (row, output column oc < 128).
+template <int NS>
 __global__ __launch_bounds__(256) void k_reduce_swiglu(const float *__restrict__ part,
                                                        Launch ln, int rows, int F, int hsplit,
                                                        f16 *__restrict__ h) {
@@ -527,8 +543,8 @@ __global__ __launch_bounds__(256) void k_reduce_swiglu(const float *__restrict__
   const int row = tm * 256 + lr, o = tn * 128 + oc;
   if (row >= rows || o >= F) return;
   const int cg = (oc / 64) * 128 + oc % 64;
-  const float g = sum_partials(part, ln, i, lr * 256 + cg);
-  const float u = sum_partials(part, ln, i, lr * 256 + cg + 64);
+  const float g = sum_partials<NS>(part, i, lr * 256 + cg);
+  const float u = sum_partials<NS>(part, i, lr * 256 + cg + 64);
   store_act(h, (long)row * F * hsplit, o, F, hsplit, silu_mul(g, u));
 }
 
@@ -734,6 +750,7 @@ __global__ __launch_bounds__(NT) void k_gemm_qkv(const f16 *__restrict__ A,
 // staged stores as above. Block (tail tile, 64-row quarter), 4 waves: wave w
 // sums head h = w % 2 of the pair for the 4-row groups g = 2 it + w / 2
 // (it < 8), then stores its half of that head's staging block.
+template <int NS>
 __global__ __launch_bounds__(256) void k_reduce_qkv(const float *__restrict__ part, Launch ln,
                                                     int rows, int n_heads, int n_kv,
                                                     QKVOut<f16> o) {
@@ -750,6 +767,22 @@ __global__ __launch_bounds__(256) void k_reduce_qkv(const float *__restrict__ pa
   VtBlock vb;
   const bool staged = live && !precise &&
                       (value ? vt_block(o, n_heads, n_kv, slot, r0, rows, vb) : qk_staged_ok(o));
+  // The rotary entries of the thread's 32 rows, loaded before the loop (in
+  // it they waited out two memory round trips per row group: the position,
+  // then the entry).
+  float2 cs[8][4];
+  if (live && !value) {
+    int pos[8][4];
+#pragma unroll
+    for (int it = 0; it < 8; ++it)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        pos[it][j] = qkv_row_pos(o, min(r0 + 4 * (2 * it + (w >> 1)) + j, rows - 1));
+#pragma unroll
+    for (int it = 0; it < 8; ++it)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) cs[it][j] = o.rope[(long)pos[it][j] * 64 + d];
+  }
 #pragma unroll
   for (int it = 0; it < 8; ++it) {
     const int g = 2 * it + (w >> 1);
@@ -757,17 +790,13 @@ __global__ __launch_bounds__(256) void k_reduce_qkv(const float *__restrict__ pa
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int e = (quarter * 64 + 4 * g + j) * 256 + h * 128 + d;
-      x1[j] = sum_partials(part, ln, i, e);
-      x2[j] = sum_partials(part, ln, i, e + 64);
+      x1[j] = sum_partials<NS>(part, i, e);
+      x2[j] = sum_partials<NS>(part, i, e + 64);
     }
     if (!live) continue;
     if (!value) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int row = min(r0 + 4 * g + j, rows - 1);
-        qk_turn(o, n_heads, n_kv, slot, x1[j], x2[j],
-                o.rope[(long)qkv_row_pos(o, row) * 64 + d]);
-      }
+      for (int j = 0; j < 4; ++j) qk_turn(o, n_heads, n_kv, slot, x1[j], x2[j], cs[it][j]);
     }
     if (!staged) {
 #pragma unroll
@@ -979,7 +1008,7 @@ hipError_t gemm_residual(const f16 *A, const void *W, bool w_f16, int rows, int 
                                 K / BK * asplit);
   VSR_WLAUNCH(k_gemm_residual, ln.blocks(), A, W16, rows, N, K, asplit, ln, x, part);
   if (ln.ntail > 0)
-    k_reduce_residual<<<ln.ntail * 256, 256, 0, s>>>(part, ln, rows, N, x);
+    VSR_REDUCE_LAUNCH(ln.nsplit, k_reduce_residual, ln.ntail * 256, 256, part, ln, rows, N, x);
   return hipGetLastError();
 }
 
@@ -995,7 +1024,8 @@ hipError_t gemm_swiglu(const f16 *A, const void *W, bool w_f16, int rows, int F,
   const Launch ln = plan_launch(nm, (F + 127) / 128, (nm + ng - 1) / ng, K / BK * asplit);
   VSR_WLAUNCH(k_gemm_swiglu, ln.blocks(), A, W16, rows, F, K, asplit, ln, h, part);
   if (ln.ntail > 0)
-    k_reduce_swiglu<<<ln.ntail * 128, 256, 0, s>>>(part, ln, rows, F, asplit, h);
+    VSR_REDUCE_LAUNCH(ln.nsplit, k_reduce_swiglu, ln.ntail * 128, 256, part, ln, rows, F, asplit,
+                      h);
   return hipGetLastError();
 }
 
@@ -1009,7 +1039,8 @@ hipError_t gemm_qkv_rope(const f16 *A, const void *W, bool w_f16, int rows, int 
                                 K / BK * asplit);
   VSR_WLAUNCH(k_gemm_qkv, ln.blocks(), A, W16, rows, K, asplit, n_heads, n_kv, ln, out, part);
   if (ln.ntail > 0)
-    k_reduce_qkv<<<ln.ntail * 4, 256, 0, s>>>(part, ln, rows, n_heads, n_kv, out);
+    VSR_REDUCE_LAUNCH(ln.nsplit, k_reduce_qkv, ln.ntail * 4, 256, part, ln, rows, n_heads, n_kv,
+                      out);
   return hipGetLastError();
 }
 
@@ -1039,6 +1070,7 @@ hipError_t gemm_lmargmax(const f16 *A, const void *W, bool w_f16, int rows, int 
 }
 
 #undef VSR_WLAUNCH
+#undef VSR_REDUCE_LAUNCH
 
 namespace {
 // Eight values per thread (16-byte loads and stores); the tail one by one.
