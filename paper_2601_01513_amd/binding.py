@@ -49,7 +49,8 @@ class VsrConfig(ctypes.Structure):
                 ("rope_base", ctypes.c_float), ("dtype", ctypes.c_int32),
                 ("max_prefix", ctypes.c_int32), ("max_cands", ctypes.c_int32),
                 ("max_cand_len", ctypes.c_int32), ("split_layers", ctypes.c_int32),
-                ("gemm_weights", ctypes.c_int32), ("max_new", ctypes.c_int32)]
+                ("gemm_weights", ctypes.c_int32), ("max_new", ctypes.c_int32),
+                ("split_mlp_layers", ctypes.c_int32)]
 
 
 _PP = ctypes.POINTER(ctypes.c_void_p)
@@ -159,18 +160,29 @@ def default_split_layers(n_layers: int) -> int:
     return min(n_layers, max(1, n_layers // 32))
 
 
+def default_split_mlp_layers(n_layers: int, split_layers: int) -> int:
+    """Precise layers whose feed-forward block is split too: all of them past
+    32 layers, none up to 32 (measured against the oracle: 28 layers stay
+    well inside the per-token bound with a plain FFN; 64 layers do not)."""
+    return split_layers if n_layers > 32 else 0
+
+
 def make_config(cfg, max_prefix: Optional[int] = None, max_cands: Optional[int] = None,
                 max_cand_len: Optional[int] = None, split_layers: Optional[int] = None,
-                gemm_weights: int = 0, max_new: int = 0) -> VsrConfig:
+                gemm_weights: int = 0, max_new: int = 0,
+                split_mlp_layers: Optional[int] = None) -> VsrConfig:
     """vsr_config from a workload.VerifierConfig (maxima default to its sizes;
-    split_layers defaults to default_split_layers(n_layers); max_new = 0
-    reserves no draft cache)."""
+    split_layers defaults to default_split_layers(n_layers), split_mlp_layers
+    to default_split_mlp_layers; max_new = 0 reserves no draft cache)."""
     if split_layers is None:
         split_layers = default_split_layers(cfg.n_layers)
+    if split_mlp_layers is None:
+        split_mlp_layers = default_split_mlp_layers(cfg.n_layers, split_layers)
     return VsrConfig(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim,
                      cfg.d_ff, cfg.vocab, cfg.rms_eps, cfg.rope_base, cfg.dtype,
                      max_prefix or cfg.n_prefix, max_cands or cfg.n_cands,
-                     max_cand_len or cfg.cand_len, split_layers, gemm_weights, max_new)
+                     max_cand_len or cfg.cand_len, split_layers, gemm_weights, max_new,
+                     split_mlp_layers)
 
 
 def workspace_size(c: VsrConfig) -> int:
@@ -192,7 +204,7 @@ class Verifier:
 
     def __init__(self, cfg, weights: Dict, device="cuda", stream=None,
                  max_prefix=None, max_cands=None, max_cand_len=None, split_layers=None,
-                 gemm_weights: str = "f16", max_new: int = 0):
+                 gemm_weights: str = "f16", max_new: int = 0, split_mlp_layers=None):
         import torch
         self._torch = torch
         self.lib = load_library()
@@ -201,7 +213,7 @@ class Verifier:
             raise ValueError("gemm_weights must be 'f16' or 'bf16'")
         self.gemm_f16 = cfg.dtype == VSR_BF16 and gemm_weights == "f16"
         self.c = make_config(cfg, max_prefix, max_cands, max_cand_len, split_layers,
-                             VSR_F16 if self.gemm_f16 else 0, max_new)
+                             VSR_F16 if self.gemm_f16 else 0, max_new, split_mlp_layers)
         size = self.lib.vsr_workspace_size(ctypes.byref(self.c))
         if size == 0:
             raise VsrError(VSR_EINVAL, "unsupported config")

@@ -66,6 +66,8 @@ std::string check_config(const vsr_config *c) {
   if (c->max_prefix > (1 << 24)) return "max_prefix too large";
   if (c->split_layers < 0 || c->split_layers > c->n_layers)
     return "split_layers must be in [0, n_layers]";
+  if (c->split_mlp_layers < 0 || c->split_mlp_layers > c->split_layers)
+    return "split_mlp_layers must be in [0, split_layers]";
   if (c->max_new < 0 || c->max_new > 4096) return "max_new must be in [0, 4096]";
   if (c->dtype == VSR_BF16 ? (c->gemm_weights != 0 && c->gemm_weights != VSR_BF16 &&
                               c->gemm_weights != VSR_F16)
@@ -414,6 +416,9 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
     // remainder.
     const bool precise = kMfma && l < cf.split_layers;
     const int sp = precise ? 2 : 1;
+    // The feed-forward block of a precise layer is split too only in the
+    // first split_mlp_layers layers.
+    const int spm = kMfma && l < cf.split_mlp_layers ? 2 : 1;
     if (!xn_ready)
       STAGE(c, K_NORM, "attention norm",
             launch_rmsnorm<TW, TA>(x, static_cast<const TW *>(c->attn_norm[l]), rows, d,
@@ -566,13 +571,13 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
         // prefix pass's last-row layer is timed as a kind of its own.
         STAGE(c, tail ? K_TAIL : K_OPROJ, "output projection",
               skinny_residual(attn_r, nr, sp, wo, wf16, d, Hq * hd, x_r, ffn_g, cf.rms_eps, xn,
-                              sp, gpart, s));
+                              spm, gpart, s));
         STAGE(c, tail ? K_TAIL : K_GATEUP, "gate/up projection",
-              skinny_swiglu(xn, nr, sp, wgu, wf16, F, d, h, gpart, s));
+              skinny_swiglu(xn, nr, spm, wgu, wf16, F, d, h, gpart, s));
         const bool next = l + 1 < cf.n_layers;
         const int sp_next = kMfma && l + 1 < cf.split_layers ? 2 : 1;
         STAGE(c, tail ? K_TAIL : K_DOWN, "down projection",
-              skinny_residual(h, nr, sp, wdown, wf16, d, F, x_r,
+              skinny_residual(h, nr, spm, wdown, wf16, d, F, x_r,
                               next ? static_cast<const TW *>(c->attn_norm[l + 1]) : nullptr,
                               cf.rms_eps, xn, sp_next, gpart, s));
         xn_ready = next;
@@ -585,12 +590,12 @@ int run_layers(vsr_ctx *c, int rows, int mode, const Split &split) {
             simple_residual<TA>(attn_r, wo, nr, d, Hq * hd, x_r, s));
     }
     STAGE(c, K_NORM, "ffn norm",
-          launch_rmsnorm<TW, TA>(x_r, ffn_g, nr, d, cf.rms_eps, xn, sp, s));
+          launch_rmsnorm<TW, TA>(x_r, ffn_g, nr, d, cf.rms_eps, xn, spm, s));
     if constexpr (kMfma) {
       STAGE(c, K_GATEUP, "gate/up projection",
-            gemm_swiglu(xn, wgu, wf16, nr, F, d, sp, h, gpart, s));
+            gemm_swiglu(xn, wgu, wf16, nr, F, d, spm, h, gpart, s));
       STAGE(c, K_DOWN, "down projection",
-            gemm_residual(h, wdown, wf16, nr, d, F, sp, x_r, gpart, s));
+            gemm_residual(h, wdown, wf16, nr, d, F, spm, x_r, gpart, s));
     } else {
       STAGE(c, K_GATEUP, "gate/up projection", simple_swiglu<TA>(xn, wgu, nr, F, d, h, s));
       STAGE(c, K_DOWN, "down projection", simple_residual<TA>(h, wdown, nr, d, F, x_r, s));

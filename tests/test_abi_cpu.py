@@ -42,7 +42,8 @@ def test_workspace_size_of_each_workload(cfg):
     ("n_heads", 5), ("head_dim", 64), ("d_model", 100), ("dtype", 7), ("max_cands", 0),
     ("max_cands", B.VSR_MAX_CANDS + 1), ("vocab", 0), ("max_prefix", 0), ("d_ff", 96),
     ("split_layers", -1), ("split_layers", W.B1_5.n_layers + 1), ("gemm_weights", 3),
-    ("gemm_weights", -1), ("max_new", -1), ("max_new", 4097)])
+    ("gemm_weights", -1), ("max_new", -1), ("max_new", 4097), ("split_mlp_layers", -1),
+    ("split_mlp_layers", 2)])
 def test_invalid_configs_have_no_workspace(field, value):
     _lib()
     c = B.make_config(W.B1_5)
@@ -115,6 +116,11 @@ def test_default_precise_layers_follow_depth():
     assert B.default_split_layers(1) == 1
     assert B.default_split_layers(28) == 1
     assert B.default_split_layers(64) == 2
+    # The feed-forward block is split in the precise layers of deep models only.
+    assert B.default_split_mlp_layers(28, 1) == 0
+    assert B.default_split_mlp_layers(64, 2) == 2
+    assert B.make_config(W.B7).split_mlp_layers == 0
+    assert B.make_config(W.B32).split_mlp_layers == 2
 
 
 def test_align_select_rejects_bad_arguments():
