@@ -530,6 +530,171 @@ __global__ __launch_bounds__(NT) void k_gemm_swiglu(const f16 *__restrict__ A,
   }
 }
 
+// ------------------------------------ four-wave tile with an ordered K loop
+// 256 threads = 4 waves, one per SIMD, on a 256 x 256 tile: wave w owns
+// rows 128 (w / 2) .. + 127 and columns 128 (w % 2) .. + 127 as 4 x 4 MFMA
+// blocks (256 accumulation registers). With one wave per SIMD every stall of
+// the wave idles the matrix core, so the K loop is one inline-assembly block
+// (gemm_loop_4w.inc, written and checked by gen_gemm_loop.py) that places
+// each LDS read, LDS-direct load, wait and barrier between the MFMAs; a
+// compiler-scheduled form of the same tile lost 5-14% to the 8-wave kernel,
+// waiting on whole groups of reads mid-stream. Same LDS panel layout and
+// swizzle as the 8-wave tile, with the operands apart: A rows of stage s at
+// 32 KB s, B rows at 64 KB + 32 KB s. fp16 operands only, K a multiple of
+// 64, and every byte offset into A and B below 4 GiB (the loads take 32-bit
+// offsets from 64-bit bases).
+template <class ARow, class BRow>
+__device__ __forceinline__ void mainloop_4w(const void *A, ARow arow, const void *B, BRow brow,
+                                            int K, int kt0, int kt1, u32x4 *lds,
+                                            f32x16 (&acc)[4][4]) {
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int wm = w >> 1, wn = w & 1;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+  const int n = kt1 - kt0;
+  if (n <= 0) return;
+  // The LDS byte address is the low half of the array's generic address.
+  const uint32_t lb = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
+  // LDS-direct load i of wave w fills tile rows (4 i + w) * 8 .. + 7; lane l
+  // lands in physical chunk l % 8 of row l / 8 (so the four waves' load i
+  // fill rows 32 i .. + 31, the rows of fragment i).
+  uint32_t dA[8], dB[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int row = (i * 4 + w) * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ ((row >> 1) & 7);
+    dA[i] = static_cast<uint32_t>(((size_t)arow(row) * K + c * 8) * 2 + (size_t)kt0 * 128);
+    dB[i] = static_cast<uint32_t>(((size_t)brow(row) * K + c * 8) * 2 + (size_t)kt0 * 128);
+  }
+  // Fragment reads of k-step s: row (lane % 32) of the wave's first 32-row
+  // block, chunk 2 s + lane / 32, swizzled; blocks 1..3 and stage 1 are
+  // immediate offsets (4 KB per block, 32 KB per stage).
+  const int x = ((lane & 31) >> 1) & 7, hc = lane >> 5;
+  uint32_t rdA[4], rdB[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const uint32_t cp = (((2 * s + hc) ^ x) * 16);
+    rdA[s] = lb + (wm * 128 + (lane & 31)) * 128 + cp;
+    rdB[s] = lb + 65536 + (wn * 128 + (lane & 31)) * 128 + cp;
+  }
+  const uint32_t mw = __builtin_amdgcn_readfirstlane(lb + w * 1024);
+  int np = __builtin_amdgcn_readfirstlane(n);
+  u32x4 fa00, fa01, fa02, fa03, fb00, fb01, fb02, fb03;
+  u32x4 fa10, fa11, fa12, fa13, fb10, fb11, fb12, fb13;
+  // M0 is a reserved register, so its clobber draws a note that the
+  // compiler may not preserve it: nothing in these kernels keeps a value in
+  // M0 across the block (the loads set it before each use).
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+  asm volatile(
+#include "gemm_loop_4w.inc"
+      : [c00] "+a"(acc[0][0]), [c01] "+a"(acc[0][1]), [c02] "+a"(acc[0][2]), [c03] "+a"(acc[0][3]),
+        [c10] "+a"(acc[1][0]), [c11] "+a"(acc[1][1]), [c12] "+a"(acc[1][2]), [c13] "+a"(acc[1][3]),
+        [c20] "+a"(acc[2][0]), [c21] "+a"(acc[2][1]), [c22] "+a"(acc[2][2]), [c23] "+a"(acc[2][3]),
+        [c30] "+a"(acc[3][0]), [c31] "+a"(acc[3][1]), [c32] "+a"(acc[3][2]), [c33] "+a"(acc[3][3]),
+        [fa00] "=&v"(fa00), [fa01] "=&v"(fa01), [fa02] "=&v"(fa02), [fa03] "=&v"(fa03),
+        [fb00] "=&v"(fb00), [fb01] "=&v"(fb01), [fb02] "=&v"(fb02), [fb03] "=&v"(fb03),
+        [fa10] "=&v"(fa10), [fa11] "=&v"(fa11), [fa12] "=&v"(fa12), [fa13] "=&v"(fa13),
+        [fb10] "=&v"(fb10), [fb11] "=&v"(fb11), [fb12] "=&v"(fb12), [fb13] "=&v"(fb13),
+        [dA0] "+v"(dA[0]), [dA1] "+v"(dA[1]), [dA2] "+v"(dA[2]), [dA3] "+v"(dA[3]),
+        [dA4] "+v"(dA[4]), [dA5] "+v"(dA[5]), [dA6] "+v"(dA[6]), [dA7] "+v"(dA[7]),
+        [dB0] "+v"(dB[0]), [dB1] "+v"(dB[1]), [dB2] "+v"(dB[2]), [dB3] "+v"(dB[3]),
+        [dB4] "+v"(dB[4]), [dB5] "+v"(dB[5]), [dB6] "+v"(dB[6]), [dB7] "+v"(dB[7]),
+        [n] "+s"(np)
+      : [rdA0] "v"(rdA[0]), [rdA1] "v"(rdA[1]), [rdA2] "v"(rdA[2]), [rdA3] "v"(rdA[3]),
+        [rdB0] "v"(rdB[0]), [rdB1] "v"(rdB[1]), [rdB2] "v"(rdB[2]), [rdB3] "v"(rdB[3]),
+        [pa] "s"(A), [pb] "s"(B), [mw] "s"(mw)
+      : "memory", "m0", "scc");
+#pragma clang diagnostic pop
+}
+
+// Tile row of accumulator register r of block row i (four-wave tile).
+__device__ __forceinline__ int row_4w(int wm, int i, int r, int lane) {
+  return wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+}
+
+// Raw fp32 partial tile of a split block, the 8-wave tile's layout.
+__device__ __forceinline__ void store_partial_4w(const f32x16 (&acc)[4][4], float *part,
+                                                 const Launch &ln, const Work &wk) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w >> 1, wn = w & 1;
+  float *p = part + ((long)wk.tail * ln.nsplit + wk.split) * kTileElems;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int col = wn * 128 + j * 32 + (lane & 31);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) p[row_4w(wm, i, r, lane) * 256 + col] = acc[i][j][r];
+  }
+}
+
+// Gate/up projection + SwiGLU on the four-wave tile (fp16 weights, unsplit
+// activations). A wave's 128 B rows are 64 gate + 64 up rows, as in the
+// 8-wave kernel, so block columns j and j + 2 pair up in one lane.
+__global__ __launch_bounds__(256) void k_gemm_swiglu_4w(const f16 *__restrict__ A,
+                                                        const uint16_t *__restrict__ W, int rows,
+                                                        int F, int K, Launch ln,
+                                                        f16 *__restrict__ h,
+                                                        float *__restrict__ part) {
+  __shared__ u32x4 lds[8192];  // two stages of 64 KB
+  const Work wk = block_work(ln);
+  const int m0 = wk.tm * 256, o0 = wk.tn * 128;
+  const bool split = wk.tail >= 0;
+  int k0 = 0, k1 = K / BK;
+  if (split) split_range(k1, ln.nsplit, wk.split, k0, k1);
+  f32x16 acc[4][4];
+  mainloop_4w(
+      A, [=](int r) { return min(m0 + r, rows - 1); }, W,
+      [=](int r) {
+        const int q = r & 127;
+        const int oc = min(o0 + (r >> 7) * 64 + (q & 63), F - 1);
+        return q < 64 ? oc : F + oc;
+      },
+      K, k0, k1, lds, acc);
+  if (split) {
+    store_partial_4w(acc, part, ln, wk);
+    return;
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w >> 1, wn = w & 1;
+  if (m0 + 256 <= rows && o0 + 128 <= F && (F & 1) == 0) {
+    // Adjacent lanes trade values so each writes two adjacent columns of one
+    // row with one 4-byte store (as in the 8-wave kernel).
+    const bool odd = lane & 1;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int c0 = o0 + wn * 64 + j * 32 + (lane & 30);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const float a = silu_mul(acc[i][j][2 * k], acc[i][j + 2][2 * k]);
+          const float b = silu_mul(acc[i][j][2 * k + 1], acc[i][j + 2][2 * k + 1]);
+          const float got = __int_as_float(
+              __builtin_amdgcn_update_dpp(0, __float_as_int(odd ? a : b), 0xB1, 0xF, 0xF, false));
+          const float v0 = odd ? got : a, v1 = odd ? b : got;
+          const int row = m0 + row_4w(wm, i, 2 * k + (odd ? 1 : 0), lane);
+          *reinterpret_cast<f16x2 *>(h + (long)row * F + c0) =
+              f16x2{static_cast<f16>(v0), static_cast<f16>(v1)};
+        }
+    }
+    return;
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int col = o0 + wn * 64 + j * 32 + (lane & 31);
+    if (col >= F) continue;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + row_4w(wm, i, r, lane);
+        if (row < rows) h[(long)row * F + col] = static_cast<f16>(silu_mul(acc[i][j][r], acc[i][j + 2][r]));
+      }
+  }
+}
+
 // Tail tiles: h = silu(gate) * up from the summed partials. Block (tail tile,
 // half of its 256 rows); thread -> (row, output column oc < 128).
 template <int NS>
@@ -990,6 +1155,14 @@ size_t gemm_split_floats(int rows, int N, int K) {
   return (size_t)ln.ntail * ln.nsplit * kTileElems;
 }
 
+// The four-wave gate/up kernel; building with VSR_NO_FOUR_WAVE keeps the
+// 8-wave kernel everywhere (for comparisons).
+#ifdef VSR_NO_FOUR_WAVE
+constexpr bool kFourWave = false;
+#else
+constexpr bool kFourWave = true;
+#endif
+
 // Weight-format dispatch of a GEMM kernel launch.
 #define VSR_WLAUNCH(kern, grid, ...)                                              \
   do {                                                                           \
@@ -1022,7 +1195,16 @@ hipError_t gemm_swiglu(const f16 *A, const void *W, bool w_f16, int rows, int F,
   const int nm = (rows + TL::BM - 1) / TL::BM;
   const int ng = (nm + 8) / 9;
   const Launch ln = plan_launch(nm, (F + 127) / 128, (nm + ng - 1) / ng, K / BK * asplit);
-  VSR_WLAUNCH(k_gemm_swiglu, ln.blocks(), A, W16, rows, F, K, asplit, ln, h, part);
+  // fp16 weights and unsplit activations: the four-wave tile with the
+  // ordered K loop (same tiles, same partial layout), if its 32-bit operand
+  // offsets reach every row.
+  const bool four_wave = kFourWave && w_f16 && asplit == 1 && K % BK == 0 &&
+                         (size_t)rows * K * 2 <= UINT32_MAX && (size_t)2 * F * K * 2 <= UINT32_MAX;
+  if (four_wave)
+    k_gemm_swiglu_4w<<<ln.blocks(), 256, 0, s>>>(A, static_cast<const uint16_t *>(W), rows, F, K,
+                                                   ln, h, part);
+  else
+    VSR_WLAUNCH(k_gemm_swiglu, ln.blocks(), A, W16, rows, F, K, asplit, ln, h, part);
   if (ln.ntail > 0)
     VSR_REDUCE_LAUNCH(ln.nsplit, k_reduce_swiglu, ln.ntail * 128, 256, part, ln, rows, F, asplit,
                       h);
