@@ -630,6 +630,74 @@ __device__ __forceinline__ void store_partial_4w(const f32x16 (&acc)[4][4], floa
   }
 }
 
+// x += A . W^T on the four-wave tile (fp16 weights, unsplit activations).
+// The residual values of two block rows (32 per lane) are loaded before any
+// of them is stored back: the compiler cannot move a load of x above a
+// store to x, and 64 at a time spilled registers.
+__global__ __launch_bounds__(256) void k_gemm_residual_4w(const f16 *__restrict__ A,
+                                                          const uint16_t *__restrict__ W,
+                                                          int rows, int N, int K, Launch ln,
+                                                          float *__restrict__ x,
+                                                          float *__restrict__ part) {
+  __shared__ u32x4 lds[8192];  // two stages of 64 KB
+  const Work wk = block_work(ln);
+  const int m0 = wk.tm * 256, n0 = wk.tn * 256;
+  const bool split = wk.tail >= 0;
+  int k0 = 0, k1 = K / BK;
+  if (split) split_range(k1, ln.nsplit, wk.split, k0, k1);
+  f32x16 acc[4][4];
+  mainloop_4w(
+      A, [=](int r) { return min(m0 + r, rows - 1); }, W,
+      [=](int r) { return min(n0 + r, N - 1); }, K, k0, k1, lds, acc);
+  if (split) {
+    store_partial_4w(acc, part, ln, wk);
+    return;
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w >> 1, wn = w & 1;
+  // Buffer loads and stores over x (rows * N * 4 bytes < 2 GiB, checked at
+  // launch): element (block row i, register r, block column j) of this lane
+  // is at byte [(i * 32 + 8 (r / 4) + r % 4) N + 32 j] * 4, the same for the
+  // whole wave (scalar offset), plus 4 lo (one lane offset). Rows past the
+  // matrix and columns past N are masked explicitly: the buffer's range
+  // check covers the lane offset only, not the scalar one. Per-element
+  // 64-bit addresses spilled registers, and so did a separate edge-tile path
+  // (the compiler copied all 256 accumulators out of the accumulation
+  // registers up front).
+  const __amdgpu_buffer_rsrc_t xr =
+      __builtin_amdgcn_make_buffer_rsrc(x, (short)0, (int)((size_t)rows * N * 4), 0x00020000);
+  const int r0 = m0 + wm * 128 + 4 * (lane >> 5);
+  const int c0 = n0 + wn * 128 + (lane & 31);
+  const uint32_t lo4 = (uint32_t)(r0 * N + c0) * 4u;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const bool col_ok = c0 + 32 * j < N;
+#pragma unroll
+    for (int ip = 0; ip < 2; ++ip) {
+      float xv[2][16];
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int dr = (2 * ip + h) * 32 + 8 * (r >> 2) + (r & 3);
+          // (the b32 buffer builtins move raw bits: bit-cast, not convert)
+          xv[h][r] = col_ok && r0 + dr < rows
+                         ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                               xr, lo4, (dr * N + 32 * j) * 4, 0))
+                         : 0.f;
+        }
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int dr = (2 * ip + h) * 32 + 8 * (r >> 2) + (r & 3);
+          if (col_ok && r0 + dr < rows)
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(xv[h][r] + acc[2 * ip + h][j][r]),
+                                                  xr, lo4, (dr * N + 32 * j) * 4, 0);
+        }
+    }
+  }
+}
+
 // Gate/up projection + SwiGLU on the four-wave tile (fp16 weights, unsplit
 // activations). A wave's 128 B rows are 64 gate + 64 up rows, as in the
 // 8-wave kernel, so block columns j and j + 2 pair up in one lane.
@@ -1155,13 +1223,22 @@ size_t gemm_split_floats(int rows, int N, int K) {
   return (size_t)ln.ntail * ln.nsplit * kTileElems;
 }
 
-// The four-wave gate/up kernel; building with VSR_NO_FOUR_WAVE keeps the
-// 8-wave kernel everywhere (for comparisons).
-#ifdef VSR_NO_FOUR_WAVE
-constexpr bool kFourWave = false;
+// Where the four-wave kernels run: bit 0 the gate/up projection, bit 1 the
+// residual projections with K >= kFourWaveMinK, bit 2 those with smaller K.
+// Building with VSR_FOUR_WAVE=<mask> changes it (for comparisons).
+#ifdef VSR_FOUR_WAVE
+constexpr int kFourWave = VSR_FOUR_WAVE;
 #else
-constexpr bool kFourWave = true;
+constexpr int kFourWave = 3;
 #endif
+constexpr int kFourWaveMinK = 8192;
+
+// The four-wave kernels' conditions: fp16 weights, unsplit activations, and
+// 32-bit byte offsets reaching every operand row.
+inline bool four_wave_ok(bool w_f16, int asplit, int rows, int nrows_w, int K) {
+  return w_f16 && asplit == 1 && K % BK == 0 && (size_t)rows * K * 2 <= UINT32_MAX &&
+         (size_t)nrows_w * K * 2 <= UINT32_MAX;
+}
 
 // Weight-format dispatch of a GEMM kernel launch.
 #define VSR_WLAUNCH(kern, grid, ...)                                              \
@@ -1179,7 +1256,13 @@ hipError_t gemm_residual(const f16 *A, const void *W, bool w_f16, int rows, int 
   typedef TileStd TL;
   const Launch ln = plan_launch((rows + TL::BM - 1) / TL::BM, (N + TL::BN - 1) / TL::BN, 8,
                                 K / BK * asplit);
-  VSR_WLAUNCH(k_gemm_residual, ln.blocks(), A, W16, rows, N, K, asplit, ln, x, part);
+  const int fw = K >= kFourWaveMinK ? 2 : 4;
+  if ((kFourWave & fw) && four_wave_ok(w_f16, asplit, rows, N, K) &&
+      (size_t)rows * N * 4 <= INT32_MAX)
+    k_gemm_residual_4w<<<ln.blocks(), 256, 0, s>>>(A, static_cast<const uint16_t *>(W), rows, N, K,
+                                                     ln, x, part);
+  else
+    VSR_WLAUNCH(k_gemm_residual, ln.blocks(), A, W16, rows, N, K, asplit, ln, x, part);
   if (ln.ntail > 0)
     VSR_REDUCE_LAUNCH(ln.nsplit, k_reduce_residual, ln.ntail * 256, 256, part, ln, rows, N, x);
   return hipGetLastError();
@@ -1195,12 +1278,9 @@ hipError_t gemm_swiglu(const f16 *A, const void *W, bool w_f16, int rows, int F,
   const int nm = (rows + TL::BM - 1) / TL::BM;
   const int ng = (nm + 8) / 9;
   const Launch ln = plan_launch(nm, (F + 127) / 128, (nm + ng - 1) / ng, K / BK * asplit);
-  // fp16 weights and unsplit activations: the four-wave tile with the
-  // ordered K loop (same tiles, same partial layout), if its 32-bit operand
-  // offsets reach every row.
-  const bool four_wave = kFourWave && w_f16 && asplit == 1 && K % BK == 0 &&
-                         (size_t)rows * K * 2 <= UINT32_MAX && (size_t)2 * F * K * 2 <= UINT32_MAX;
-  if (four_wave)
+  // The four-wave tile with the ordered K loop where it applies (same
+  // tiles, same partial layout).
+  if ((kFourWave & 1) && four_wave_ok(w_f16, asplit, rows, 2 * F, K))
     k_gemm_swiglu_4w<<<ln.blocks(), 256, 0, s>>>(A, static_cast<const uint16_t *>(W), rows, F, K,
                                                    ln, h, part);
   else
