@@ -33,10 +33,12 @@ METRIC = ("candidate tokens scored/sec and ms per verify pass "
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 
-# Kernels as the profiler sees them, and the stages each one serves.
+# Kernels as the profiler sees them (fp16 GEMM weights, the default), and
+# the stages each one serves.
 KERNELS = {
-    "k_gemm_swiglu": ["verify.gate_up_swiglu"],
-    "k_gemm_residual": ["verify.o_proj", "verify.down_proj"],
+    "k_gemm_swiglu_4w": ["verify.gate_up_swiglu"],
+    "k_gemm_residual_4w": ["verify.down_proj"],
+    "k_gemm_residual": ["verify.o_proj"],
     "k_gemm_qkv": ["verify.qkv_rope"],
     "k_attn<0> (prefill)": ["verify.attention"],
     "k_attn<1> (cascade)": ["verify.cand_attention"],

@@ -654,45 +654,42 @@ __global__ __launch_bounds__(256) void k_gemm_residual_4w(const f16 *__restrict_
     return;
   }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w >> 1, wn = w & 1;
-  // Buffer loads and stores over x (rows * N * 4 bytes < 2 GiB, checked at
-  // launch): element (block row i, register r, block column j) of this lane
-  // is at byte [(i * 32 + 8 (r / 4) + r % 4) N + 32 j] * 4, the same for the
-  // whole wave (scalar offset), plus 4 lo (one lane offset). Rows past the
-  // matrix and columns past N are masked explicitly: the buffer's range
-  // check covers the lane offset only, not the scalar one. Per-element
-  // 64-bit addresses spilled registers, and so did a separate edge-tile path
-  // (the compiler copied all 256 accumulators out of the accumulation
-  // registers up front).
+  // Buffer loads and stores over x, rows * N * 4 bytes (< 2 GiB, checked at
+  // launch). Element (block row i, register r, block column j) of this lane
+  // is at byte 4 [(r0 + dr) N + c0] + 128 j with dr = i * 32 + 8 (r / 4) +
+  // r % 4: the lane offset carries the row, so rows past the matrix fail
+  // the buffer's range check (which covers the lane offset, not the scalar
+  // one) -- their loads read 0 and their stores are dropped -- and a lane
+  // whose column is past N starts beyond the buffer. Branch-free: masking
+  // each element made the compiler branch per element. Per-element 64-bit
+  // addresses spilled registers, and so did a separate edge-tile path (the
+  // compiler copied all 256 accumulators out of the accumulation registers).
   const __amdgpu_buffer_rsrc_t xr =
       __builtin_amdgcn_make_buffer_rsrc(x, (short)0, (int)((size_t)rows * N * 4), 0x00020000);
   const int r0 = m0 + wm * 128 + 4 * (lane >> 5);
   const int c0 = n0 + wn * 128 + (lane & 31);
-  const uint32_t lo4 = (uint32_t)(r0 * N + c0) * 4u;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const bool col_ok = c0 + 32 * j < N;
+    const uint32_t base = c0 + 32 * j < N ? (uint32_t)(r0 * N + c0 + 32 * j) * 4u : 0x80000000u;
 #pragma unroll
     for (int ip = 0; ip < 2; ++ip) {
       float xv[2][16];
+      // (the b32 buffer builtins move raw bits: bit-cast, not convert)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int dr = (2 * ip + h) * 32 + 8 * (r >> 2) + (r & 3);
-          // (the b32 buffer builtins move raw bits: bit-cast, not convert)
-          xv[h][r] = col_ok && r0 + dr < rows
-                         ? __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-                               xr, lo4, (dr * N + 32 * j) * 4, 0))
-                         : 0.f;
+          const uint32_t dr = (2 * ip + h) * 32 + 8 * (r >> 2) + (r & 3);
+          xv[h][r] = __uint_as_float(
+              __builtin_amdgcn_raw_buffer_load_b32(xr, base + dr * (uint32_t)N * 4u, 0, 0));
         }
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int dr = (2 * ip + h) * 32 + 8 * (r >> 2) + (r & 3);
-          if (col_ok && r0 + dr < rows)
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(xv[h][r] + acc[2 * ip + h][j][r]),
-                                                  xr, lo4, (dr * N + 32 * j) * 4, 0);
+          const uint32_t dr = (2 * ip + h) * 32 + 8 * (r >> 2) + (r & 3);
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(xv[h][r] + acc[2 * ip + h][j][r]),
+                                                xr, base + dr * (uint32_t)N * 4u, 0, 0);
         }
     }
   }
