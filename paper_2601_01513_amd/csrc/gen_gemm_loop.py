@@ -15,24 +15,33 @@ Shape of the work (per wave, one of four; wave w owns output rows
   - a K panel is 64 wide = four 16-wide k-steps; k-step s uses fragments
     fa{set}{i} (rows of A) and fb{set}{j} (rows of B), 16 bytes per lane,
     read from LDS; two fragment sets alternate between k-steps;
-  - LDS holds two panels (stages): A rows at stage * 32 KB, B rows at
-    64 KB + stage * 32 KB, 128-byte rows, chunk c of row r at c ^ ((r/2) % 8);
-  - the next panel streams into the other stage with LDS-direct global loads
-    (`global_load_lds_dwordx4`, 1 KB per instruction and wave; M0 holds the
-    wave's LDS destination), 8 for A and 8 for B per lane and panel.
+  - LDS (160 KB) holds the A panels in two stages (32 KB each, at 0) and the
+    B panels in three (at 64 KB): B is the weight matrix, streamed from HBM,
+    so its loads are issued two panels ahead; A (activations, mostly cache
+    hits) one panel ahead. Rows are 128 bytes, chunk c of row r at
+    c ^ ((r/2) % 8). The stage of panel k is k % 2 for A and k % 3 for B, so
+    the loop is unrolled over the 6-panel cycle (each body names its stages
+    as immediate offsets: rdA / rdB with stage * 32 KB, rdC = rdB + 64 KB
+    for the third B stage);
+  - LDS-direct global loads (`global_load_lds_dwordx4`, 1 KB per instruction
+    and wave; M0 holds the wave's LDS destination), 8 per operand, lane and
+    panel.
 
-Schedule of one panel (16 MFMAs per k-step, each about 32 cycles of the
+Schedule of panel k (16 MFMAs per k-step, each about 32 cycles of the
 SIMD's matrix core; other instructions are issued between them):
-  - k-steps 0 and 1: the next panel's 16 loads, one after each MFMA; the
-    fragments of the following k-step are read from MFMA 1 on;
+  - k-step 0: A(k + 1)'s 8 loads, k-step 1: B(k + 2)'s 8 loads, one after
+    each MFMA (each M0 written one MFMA ahead); the fragments of the
+    following k-step are read from MFMA 1 on;
   - k-step 2: the global offsets advance by one panel (128 bytes);
-  - k-step 3: after 12 MFMAs, wait for this lane's loads (vmcnt(0)) and for
-    its fragment reads, then barrier (every wave's loads of the next panel
-    are in LDS, and no wave still reads the current stage, which the next
-    panel's loads will overwrite); the last 4 MFMAs cover the reads of the
-    next panel's first k-step.
+  - k-step 3: after 12 MFMAs, wait for this lane's loads of panel k + 1
+    (vmcnt(8): A(k+1) and the older B(k+1) done, B(k+2) may still fly) and
+    for its fragment reads, then barrier (every wave's loads of panel k + 1
+    are in LDS, and no wave still reads the stages that panel k + 2's loads
+    overwrite); the last 4 MFMAs cover the reads of panel k + 1's first
+    k-step.
 Before each MFMA, lgkmcnt(N) waits exactly for its two fragments (LDS reads
-complete in issue order). A last panel issues no loads and has no barrier.
+complete in issue order). The second-to-last panel loads only A, the last
+panel nothing and has no barrier.
 """
 from __future__ import annotations
 
@@ -40,31 +49,33 @@ import os
 import re
 import sys
 
-NSTEP = 4            # 16-wide k-steps per 64-wide panel
-A_STAGE = 32768      # bytes of one stage's A (or B) rows
-B_BASE = 65536       # byte offset of the B rows
-FRAG = 4096          # bytes between 32-row fragments
-HANDOFF = 12         # MFMAs of the last k-step issued before the barrier
-LOADS_PER_PANEL = 16
+OUT = os.path.join(os.path.dirname(os.path.abspath(__file__)), "gemm_loop_4w.inc")
+
+NSTEP = 4        # 16-wide k-steps per 64-wide panel
+STG = 32768      # bytes of one stage of one operand (256 rows x 128 bytes)
+B_BASE = 65536   # byte offset of the B stages
+FRAG = 4096      # bytes between 32-row fragments
+HANDOFF = 12   # MFMAs of the last k-step issued before the barrier
 # Read order of a fragment set: the first MFMA needs A0 and B0, the next
 # three B1..B3, then A1..A3 one per row of four MFMAs.
 READ_ORDER = [('a', 0), ('b', 0), ('b', 1), ('b', 2), ('b', 3), ('a', 1), ('a', 2), ('a', 3)]
 MFMA_ORDER = [(i, j) for i in range(4) for j in range(4)]
 
-OUT = os.path.join(os.path.dirname(os.path.abspath(__file__)), "gemm_loop_4w.inc")
-
 
 class Stream:
     def __init__(self):
-        self.lines = []
-        self.lgkm = []  # outstanding fragment reads, issue order
+        self.lines, self.lgkm = [], []
 
     def op(self, s):
         self.lines.append(s)
 
-    def read(self, fset, kind, idx, step, stage):
-        self.op(f'ds_read_b128 %[f{kind}{fset}{idx}], %[rd{kind.upper()}{step}] '
-                f'offset:{idx * FRAG + stage * A_STAGE}')
+    def read(self, fset, kind, idx, step, ast, bst):
+        if kind == 'a':
+            self.op(f'ds_read_b128 %[fa{fset}{idx}], %[rdA{step}] offset:{ast * STG + idx * FRAG}')
+        elif bst < 2:
+            self.op(f'ds_read_b128 %[fb{fset}{idx}], %[rdB{step}] offset:{bst * STG + idx * FRAG}')
+        else:
+            self.op(f'ds_read_b128 %[fb{fset}{idx}], %[rdC{step}] offset:{idx * FRAG}')
         self.lgkm.append((fset, kind, idx))
 
     def need(self, fset, kind, idx):
@@ -84,45 +95,54 @@ class Stream:
         self.op(f'v_mfma_f32_32x32x16_f16 %[c{i}{j}], %[fa{fset}{i}], %[fb{fset}{j}], %[c{i}{j}]')
 
 
-def loads(stage):
-    """(M0 write, load) pairs that fill LDS stage `stage` with a panel."""
-    out = []
-    for kind, base in (('A', 0), ('B', B_BASE)):
-        for i in range(8):
-            out.append((f's_add_u32 m0, %[mw], {base + stage * A_STAGE + i * FRAG}',
-                        f'global_load_lds_dwordx4 %[d{kind}{i}], %[p{kind.lower()}]'))
-    return out
+def loads(kind, stage):
+    base = 0 if kind == 'A' else B_BASE
+    return [(f's_add_u32 m0, %[mw], {base + stage * STG + i * FRAG}',
+             f'global_load_lds_dwordx4 %[d{kind}{i}], %[p{kind.lower()}]') for i in range(8)]
 
 
-ADVANCE = [f'v_add_u32 %[d{k}{i}], 128, %[d{k}{i}]' for k in 'AB' for i in range(8)]
+ADV_A = [f'v_add_u32 %[dA{i}], 128, %[dA{i}]' for i in range(8)]
+ADV_B = [f'v_add_u32 %[dB{i}], 128, %[dB{i}]' for i in range(8)]
 
 
-def panel(e, cur, last):
-    """One panel from stage `cur`; fragment set 0 holds (or is reading) k-step 0."""
-    nxt = 1 - cur
-    todo = [] if last else loads(nxt)
+def publish(e, vm):
+    """Panel hand-off: this lane's loads down to vm in flight, then barrier."""
+    e.op(f's_waitcnt vmcnt({vm})')
+    e.op('s_barrier')
+
+
+def panel(e, p, kind):
+    """Panel of phase p (A stage p % 2, B stage p % 3). kind: 'full' (loads
+    A(k+1), B(k+2)), 'pre' (loads A(k+1) only), 'last' (no loads)."""
+    a, b = p % 2, p % 3
+    an, bn = (p + 1) % 2, (p + 1) % 3
+    todo = []
+    if kind in ('full', 'pre'):
+        todo += loads('A', an)
+    if kind == 'full':
+        todo += loads('B', (p + 2) % 3)
     for s in range(NSTEP):
         fs, other = s & 1, (s & 1) ^ 1
-        reads = [(other, k, idx, s + 1, cur) for k, idx in READ_ORDER] if s + 1 < NSTEP else []
-        handoff = s == NSTEP - 1 and not last
+        reads = [(other, k, idx, s + 1, a, b) for k, idx in READ_ORDER] if s + 1 < NSTEP else []
+        handoff = s == NSTEP - 1 and kind != 'last'
         mine = todo[:8] if s < 2 else []
         todo = todo[8:] if s < 2 else todo
         m0_set = False
         for n, (i, j) in enumerate(MFMA_ORDER):
             if handoff and n == HANDOFF:
                 e.drain()
-                e.op('s_waitcnt vmcnt(0)')
-                e.op('s_barrier')
+                publish(e, 8 if kind == 'full' else 0)
             e.mfma(fs, i, j)
             if 1 <= n <= len(reads):
                 e.read(*reads[n - 1])
-            if s == 2 and not last:
-                e.op(ADVANCE[n])
+            if s == 2 and kind == 'full':
+                e.op((ADV_A + ADV_B)[n])
+            if s == 2 and kind == 'pre' and n < 8:
+                e.op(ADV_A[n])
             if handoff and n >= HANDOFF:
                 per = -(-len(READ_ORDER) // (16 - HANDOFF))
                 for k, idx in READ_ORDER[(n - HANDOFF) * per:(n - HANDOFF + 1) * per]:
-                    e.read(0, k, idx, 0, nxt)
-            # each load one MFMA after the write of its M0
+                    e.read(0, k, idx, 0, an, bn)
             if mine and m0_set and n >= 1:
                 e.op(mine.pop(0)[1])
                 m0_set = False
@@ -134,80 +154,93 @@ def panel(e, cur, last):
 
 def generate():
     e = Stream()
-    for m0, ld in loads(0):
-        e.op(m0)
-        e.op('s_nop 0')
-        e.op(ld)
+    for m0, ld in loads('A', 0) + loads('B', 0):
+        e.op(m0); e.op('s_nop 0'); e.op(ld)
+    e.op('s_cmp_eq_u32 %[n], 1')
+    e.op('s_cbranch_scc1 L_one_%=')
+    for a in ADV_B:
+        e.op(a)
+    for m0, ld in loads('B', 1):
+        e.op(m0); e.op('s_nop 0'); e.op(ld)
+    e.op('s_waitcnt vmcnt(8)')
+    e.op('s_barrier')
+    for x in ADV_A + ADV_B:
+        e.op(x)
+    for k, idx in READ_ORDER:
+        e.read(0, k, idx, 0, 0, 0)
+    entry = list(e.lgkm)
+    e.op('s_cmp_eq_u32 %[n], 2')
+    e.op('s_cbranch_scc1 L_pre0_%=')
+    e.op('L_loop_%=:')
+    for p in range(6):
+        e.lgkm = list(entry)
+        panel(e, p, 'full')
+        e.op('s_sub_u32 %[n], %[n], 1')
+        e.op('s_cmp_eq_u32 %[n], 2')
+        e.op(f's_cbranch_scc1 L_pre{(p + 1) % 6}_%=')
+    e.op('s_branch L_loop_%=')
+    e.op('L_one_%=:')
     e.op('s_waitcnt vmcnt(0)')
     e.op('s_barrier')
-    for a in ADVANCE:
-        e.op(a)
     for k, idx in READ_ORDER:
-        e.read(0, k, idx, 0, 0)
-    entry = list(e.lgkm)
-    e.op('s_cmp_eq_u32 %[n], 1')
-    e.op('s_cbranch_scc1 L_last0_%=')
-    e.op('L_loop_%=:')
-    panel(e, 0, False)
-    e.op('s_sub_u32 %[n], %[n], 1')
-    e.op('s_cmp_eq_u32 %[n], 1')
-    e.op('s_cbranch_scc1 L_last1_%=')
-    panel(e, 1, False)
-    e.op('s_sub_u32 %[n], %[n], 1')
-    e.op('s_cmp_eq_u32 %[n], 1')
-    e.op('s_cbranch_scc1 L_last0_%=')
-    e.op('s_branch L_loop_%=')
-    e.op('L_last0_%=:')
-    e.lgkm = list(entry)
-    panel(e, 0, True)
-    e.op('s_branch L_end_%=')
-    e.op('L_last1_%=:')
-    e.lgkm = list(entry)
-    panel(e, 1, True)
+        e.read(0, k, idx, 0, 0, 0)
+    e.op('s_branch L_last0_%=')
+    for p in range(6):
+        e.op(f'L_pre{p}_%=:')
+        e.lgkm = list(entry)
+        panel(e, p, 'pre')
+        e.op(f's_branch L_last{(p + 1) % 6}_%=')
+    for p in range(6):
+        e.op(f'L_last{p}_%=:')
+        e.lgkm = list(entry)
+        panel(e, p, 'last')
+        e.op('s_branch L_end_%=')
     e.op('L_end_%=:')
-    # the accumulators are read right after the block: let the last MFMAs
-    # retire first
     for _ in range(3):
         e.op('s_nop 7')
     return e.lines
 
 
-def check(lines, nmax=7):
+def check(lines, nmax=14):
     """Interprets the stream for 1..nmax panels. Every MFMA must read
     fragments of its own (panel, k-step), with their reads complete; every
-    fragment read must come from a stage whose loads completed (vmcnt(0)) and
-    were published by a barrier; a load may not overwrite a stage that this
-    wave has read since the last barrier; each load's M0 must be the slot of
-    its own row block, and the 32 rows a fragment reads must hold the panel
-    its k-step belongs to (each load slot advances on its own); the MFMAs must walk panels 0..n-1, k-steps 0..3."""
+    fragment read must come from a stage whose loads completed (vmcnt) and
+    were published by a barrier, and the 32 rows it reads must hold the panel
+    its k-step belongs to (load slot q of the four waves fills rows
+    32 q .. + 31: fragment i is slot i for waves in the first row (A) or
+    column (B) half and slot 4 + i for the others; each slot's offset
+    advances on its own); a load may not overwrite a stage that this wave
+    has read since the last barrier, or whose reads were still in flight at
+    it; each load's M0 must be the slot of its own row block; the MFMAs must
+    walk panels 0..n-1, k-steps 0..3."""
     labels = {l[:-1]: i for i, l in enumerate(lines) if re.match(r'L_\w+_%=:$', l)}
     for n0 in range(1, nmax + 1):
         n, pc, scc = n0, 0, False
         koff = {(k, i): 0 for k in 'AB' for i in range(8)}
         stage, inflight = {}, []
         tag, pending, done, src = {}, [], set(), {}
-        seen, read_since_bar, m0 = [], set(), None
+        seen, busy, m0 = [], set(), None
         steps = 0
         while pc < len(lines):
             steps += 1
-            assert steps < 100000, 'no exit'
-            l = lines[pc]
-            pc += 1
+            assert steps < 400000
+            l = lines[pc]; pc += 1
             if l.endswith(':') or l.startswith('s_nop'):
                 continue
             m = re.match(r's_add_u32 m0, %\[mw\], (\d+)$', l)
             if m:
                 off = int(m.group(1))
-                assert off % FRAG == 0
-                m0 = ('B' if off >= B_BASE else 'A', (off % B_BASE) // A_STAGE, (off % A_STAGE) // FRAG)
+                kind = 'B' if off >= B_BASE else 'A'
+                rel = off - (B_BASE if kind == 'B' else 0)
+                m0 = (kind, rel // STG, (rel % STG) // FRAG)
+                assert (kind == 'A' and m0[1] < 2) or (kind == 'B' and m0[1] < 3)
                 continue
             m = re.match(r'global_load_lds_dwordx4 %\[d([AB])(\d)\], %\[p([ab])\]$', l)
             if m:
                 kind = m.group(1)
-                assert m0 is not None and m0[0] == kind and m0[2] == int(m.group(2)), (l, m0)
-                assert m.group(3) == kind.lower(), l
+                assert m0 and m0[0] == kind and m0[2] == int(m.group(2)) and m.group(3) == kind.lower(), (l, m0)
                 st, slot = m0[1], m0[2]
-                assert (kind, st) not in read_since_bar, ('load over a stage still being read', l)
+                assert (kind, st) not in busy, ('load over a stage in use', l)
                 inflight.append((kind, st, slot, koff[(kind, slot)]))
                 stage[(kind, st, slot)] = (koff[(kind, slot)], 'pending')
                 m0 = None
@@ -216,37 +249,34 @@ def check(lines, nmax=7):
             if m:
                 koff[(m.group(1), int(m.group(2)))] += 1
                 continue
-            if l == 's_waitcnt vmcnt(0)':
-                for kind, st, slot, p in inflight:
-                    stage[(kind, st, slot)] = (p, 'landed')
-                inflight = []
+            m = re.match(r's_waitcnt vmcnt\((\d+)\)$', l)
+            if m:
+                keep = int(m.group(1))
+                while len(inflight) > keep:
+                    kind, st, slot, p = inflight.pop(0)
+                    if stage[(kind, st, slot)] == (p, 'pending'):
+                        stage[(kind, st, slot)] = (p, 'landed')
                 continue
             if l == 's_barrier':
                 for k, v in list(stage.items()):
                     if v[1] == 'landed':
                         stage[k] = (v[0], 'visible')
-                # a read still in flight at the barrier keeps its stage busy
-                read_since_bar = {src[r] for r in pending}
+                busy = {src[r] for r in pending}
                 continue
-            m = re.match(r'ds_read_b128 %\[(f([ab])\d(\d))\], %\[rd([AB])(\d)\] offset:(\d+)$', l)
+            m = re.match(r'ds_read_b128 %\[(f([ab])\d(\d))\], %\[rd([ABC])(\d)\] offset:(\d+)$', l)
             if m:
-                reg, kind, idx = m.group(1), m.group(4), int(m.group(3))
+                reg, idx, base, step, off = m.group(1), int(m.group(3)), m.group(4), int(m.group(5)), int(m.group(6))
+                kind = 'A' if base == 'A' else 'B'
                 assert m.group(2) == kind.lower()
-                step, off = int(m.group(5)), int(m.group(6))
-                st = off // A_STAGE
-                assert off % A_STAGE == idx * FRAG, l
-                # load slot q of the four waves fills tile rows 32 q .. + 31:
-                # fragment idx is slot idx for waves in the first row (A) or
-                # column (B) half and slot 4 + idx for the others
+                st = 2 if base == 'C' else off // STG
+                assert off % STG == idx * FRAG
                 p, state = stage[(kind, st, idx)]
                 p2, state2 = stage[(kind, st, 4 + idx)]
                 assert state == state2 == 'visible', ('read of an unpublished stage', l, state, state2)
-                assert p == p2, ('halves of a stage hold different panels', l)
-                tag[reg] = (p, step)
-                src[reg] = (kind, st)
-                pending.append(reg)
-                done.discard(reg)
-                read_since_bar.add((kind, st))
+                assert p == p2
+                tag[reg] = (p, step); src[reg] = (kind, st)
+                pending.append(reg); done.discard(reg)
+                busy.add((kind, st))
                 continue
             m = re.match(r's_waitcnt lgkmcnt\((\d+)\)$', l)
             if m:
@@ -255,30 +285,27 @@ def check(lines, nmax=7):
                 continue
             m = re.match(r'v_mfma_f32_32x32x16_f16 %\[c(\d)(\d)\], %\[(fa\d(\d))\], %\[(fb\d(\d))\], %\[c\1\2\]$', l)
             if m:
-                a, b = m.group(3), m.group(5)
-                assert m.group(4) == m.group(1) and m.group(6) == m.group(2), l
-                assert a in done and b in done, ('fragment read not complete', l)
-                assert tag[a] == tag[b], (tag[a], tag[b], l)
-                seen.append(tag[a])
+                a_, b_ = m.group(3), m.group(5)
+                assert m.group(4) == m.group(1) and m.group(6) == m.group(2)
+                assert a_ in done and b_ in done, ('fragment read not complete', l)
+                assert tag[a_] == tag[b_], (tag[a_], tag[b_], l)
+                seen.append(tag[a_])
                 continue
-            if l == 's_cmp_eq_u32 %[n], 1':
-                scc = n == 1
-                continue
+            m = re.match(r's_cmp_eq_u32 %\[n\], (\d)$', l)
+            if m:
+                scc = n == int(m.group(1)); continue
             if l == 's_sub_u32 %[n], %[n], 1':
-                n -= 1
-                continue
+                n -= 1; continue
             m = re.match(r's_cbranch_scc1 (L_\w+_%=)$', l)
             if m:
-                pc = labels[m.group(1)] if scc else pc
-                continue
+                pc = labels[m.group(1)] if scc else pc; continue
             m = re.match(r's_branch (L_\w+_%=)$', l)
             if m:
-                pc = labels[m.group(1)]
-                continue
-            raise AssertionError(f'unknown instruction: {l}')
+                pc = labels[m.group(1)]; continue
+            raise AssertionError(f'unknown: {l}')
         want = [(p, s) for p in range(n0) for s in range(NSTEP) for _ in range(16)]
-        assert seen == want, (n0, 'panel / k-step order')
-        assert not inflight, 'loads left in flight'
+        assert seen == want, (n0, seen[:5], len(seen))
+        assert not inflight
     return True
 
 

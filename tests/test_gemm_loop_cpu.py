@@ -24,11 +24,11 @@ def _gen():
 def test_committed_loop_matches_generator_and_checks():
     g = _gen()
     lines = g.generate()
-    assert g.check(lines, nmax=9)
+    assert g.check(lines, nmax=14)
     with open(g.OUT) as f:
         body = f.read()
     assert body.endswith(g.render(lines)), "gemm_loop_4w.inc is stale: rerun the generator"
-    assert sum("v_mfma" in l for l in lines) == 256  # 4 bodies x 64
+    assert sum("v_mfma" in l for l in lines) == 18 * 64  # 6 full, 6 second-to-last, 6 last panels
 
 
 def _mutations(lines):
@@ -47,6 +47,7 @@ def _mutations(lines):
         "M0 of a load slot swapped": [l.replace("%[mw], 4096", "%[mw], 8192") if late(k) else l
                                       for k, l in enumerate(lines)],
         "one load slot not advanced": [l for l in lines if not l.startswith("v_add_u32 %[dB5]")],
+        "hand-off waits for one load too few": [l.replace("vmcnt(8)", "vmcnt(9)") for l in lines],
         "k-steps swapped": [l.replace("%[rdA1]", "%[rdAx]").replace("%[rdA2]", "%[rdA1]")
                             .replace("%[rdAx]", "%[rdA2]") for l in lines],
     }
