@@ -378,6 +378,53 @@ __device__ __forceinline__ void store_act(f16 *p, long base, int col, int n, int
 }
 
 // ------------------------------------------------------- residual (O, down)
+// x += acc for one wave's NI x 4 MFMA blocks: this lane holds rows r0 + dr
+// (dr = 32 i + 8 (r / 4) + r % 4 for block row i, register r) of columns
+// c0 + 32 j (block column j). Buffer loads and stores over x (rows * N * 4
+// bytes < 2 GiB, checked at launch): the lane offset carries the row, so
+// rows past the matrix fail the buffer's range check (which covers the lane
+// offset, not the scalar one) -- their loads read 0 and their stores are
+// dropped -- and a lane whose column is past N starts beyond the buffer.
+// Branch-free: masking each element made the compiler branch per element;
+// per-element 64-bit addresses spilled registers. Batches of 8 rows x 4
+// column blocks (32 values) are loaded before any of them is stored (the
+// compiler cannot move a load of x above a store to x).
+template <int NI>
+__device__ __forceinline__ void residual_epilogue(const f32x16 (&acc)[NI][4], int r0, int c0,
+                                                  int rows, int N, float *x) {
+  const __amdgpu_buffer_rsrc_t xr =
+      __builtin_amdgcn_make_buffer_rsrc(x, (short)0, (int)((size_t)rows * N * 4), 0x00020000);
+  uint32_t bx[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int col = c0 + 32 * j;
+    bx[j] = col < N ? (uint32_t)(r0 * N + col) * 4u : 0x80000000u;
+  }
+#pragma unroll
+  for (int i = 0; i < NI; ++i)
+#pragma unroll
+    for (int rh = 0; rh < 2; ++rh) {
+      float xv[8][4];
+      // (the b32 buffer builtins move raw bits: bit-cast, not convert)
+#pragma unroll
+      for (int rr = 0; rr < 8; ++rr)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t dr = 32 * i + 16 * rh + 8 * (rr >> 2) + (rr & 3);
+          xv[rr][j] = __uint_as_float(
+              __builtin_amdgcn_raw_buffer_load_b32(xr, bx[j] + dr * (uint32_t)N * 4u, 0, 0));
+        }
+#pragma unroll
+      for (int rr = 0; rr < 8; ++rr) {
+        const uint32_t dr = 32 * i + 16 * rh + 8 * (rr >> 2) + (rr & 3);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(xv[rr][j] + acc[i][j][8 * rh + rr]),
+                                                xr, bx[j] + dr * (uint32_t)N * 4u, 0, 0);
+      }
+    }
+}
+
 template <class TL, bool WCVT>
 __global__ __launch_bounds__(NT) void k_gemm_residual(const f16 *__restrict__ A,
                                                       const uint16_t *__restrict__ W, int rows,
@@ -398,45 +445,11 @@ __global__ __launch_bounds__(NT) void k_gemm_residual(const f16 *__restrict__ A,
     store_partial<TL>(acc, part, ln, wk);
     return;
   }
+  static_assert(TL::FN == 4 && TL::TN == 128, "four 32-column blocks per wave");
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wm = w / TL::WN, wn = w % TL::WN;
-  if (m0 + TL::BM <= rows && n0 + TL::BN <= N) {
-    // Whole tile: the residual values of one MFMA column block (32 per
-    // lane) are all loaded before any of them is stored back. The compiler
-    // cannot move a load of x above a store to x, so an element-by-element
-    // x += acc waits out one memory round trip per element (measured: 24 us
-    // of the O projection's 140 us, 40 us of the down projection's 645 us);
-    // two column blocks at a time (64 values beside the 128 accumulators)
-    // spilled registers.
-#pragma unroll
-    for (int fn = 0; fn < TL::FN; ++fn) {
-      float xv[TL::FM][16];
-      const int col = n0 + acc_col<TL>(wn, fn, lane);
-#pragma unroll
-      for (int fm = 0; fm < TL::FM; ++fm)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          xv[fm][r] = x[(long)(m0 + acc_row<TL>(wm, fm, r, lane)) * N + col];
-#pragma unroll
-      for (int fm = 0; fm < TL::FM; ++fm)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          x[(long)(m0 + acc_row<TL>(wm, fm, r, lane)) * N + col] = xv[fm][r] + acc[fm][fn][r];
-    }
-    return;
-  }
-#pragma unroll
-  for (int fn = 0; fn < TL::FN; ++fn) {
-    const int col = n0 + acc_col<TL>(wn, fn, lane);
-    if (col >= N) continue;
-#pragma unroll
-    for (int fm = 0; fm < TL::FM; ++fm)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + acc_row<TL>(wm, fm, r, lane);
-        if (row < rows) x[(long)row * N + col] += acc[fm][fn][r];
-      }
-  }
+  residual_epilogue<TL::FM>(acc, m0 + wm * TL::TM + 4 * (lane >> 5), n0 + wn * TL::TN + (lane & 31),
+                            rows, N, x);
 }
 
 // Tail tiles: x += sum of the partials. Block (tail tile, 256-element slab).
@@ -660,45 +673,8 @@ __global__ __launch_bounds__(256) void k_gemm_residual_4w(const f16 *__restrict_
     return;
   }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w >> 1, wn = w & 1;
-  // Buffer loads and stores over x, rows * N * 4 bytes (< 2 GiB, checked at
-  // launch). Element (block row i, register r, block column j) of this lane
-  // is at byte 4 [(r0 + dr) N + c0] + 128 j with dr = i * 32 + 8 (r / 4) +
-  // r % 4: the lane offset carries the row, so rows past the matrix fail
-  // the buffer's range check (which covers the lane offset, not the scalar
-  // one) -- their loads read 0 and their stores are dropped -- and a lane
-  // whose column is past N starts beyond the buffer. Branch-free: masking
-  // each element made the compiler branch per element. Per-element 64-bit
-  // addresses spilled registers, and so did a separate edge-tile path (the
-  // compiler copied all 256 accumulators out of the accumulation registers).
-  const __amdgpu_buffer_rsrc_t xr =
-      __builtin_amdgcn_make_buffer_rsrc(x, (short)0, (int)((size_t)rows * N * 4), 0x00020000);
-  const int r0 = m0 + wm * 128 + 4 * (lane >> 5);
-  const int c0 = n0 + wn * 128 + (lane & 31);
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const uint32_t base = c0 + 32 * j < N ? (uint32_t)(r0 * N + c0 + 32 * j) * 4u : 0x80000000u;
-#pragma unroll
-    for (int ip = 0; ip < 2; ++ip) {
-      float xv[2][16];
-      // (the b32 buffer builtins move raw bits: bit-cast, not convert)
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const uint32_t dr = (2 * ip + h) * 32 + 8 * (r >> 2) + (r & 3);
-          xv[h][r] = __uint_as_float(
-              __builtin_amdgcn_raw_buffer_load_b32(xr, base + dr * (uint32_t)N * 4u, 0, 0));
-        }
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const uint32_t dr = (2 * ip + h) * 32 + 8 * (r >> 2) + (r & 3);
-          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(xv[h][r] + acc[2 * ip + h][j][r]),
-                                                xr, base + dr * (uint32_t)N * 4u, 0, 0);
-        }
-    }
-  }
+  residual_epilogue<4>(acc, m0 + wm * 128 + 4 * (lane >> 5), n0 + wn * 128 + (lane & 31), rows, N,
+                       x);
 }
 
 // Gate/up projection + SwiGLU on the four-wave tile (fp16 weights, unsplit
@@ -1257,11 +1233,13 @@ hipError_t gemm_residual(const f16 *A, const void *W, bool w_f16, int rows, int 
                          int asplit, float *x, float *part, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
+  // Both residual epilogues address x through buffer descriptors of 32-bit
+  // byte ranges.
+  if ((size_t)rows * N * 4 > INT32_MAX) return hipErrorInvalidValue;
   const Launch ln = plan_launch((rows + TL::BM - 1) / TL::BM, (N + TL::BN - 1) / TL::BN, 8,
                                 K / BK * asplit);
   const int fw = K >= kFourWaveMinK ? 2 : 4;
-  if ((kFourWave & fw) && four_wave_ok(w_f16, asplit, rows, N, K) &&
-      (size_t)rows * N * 4 <= INT32_MAX)
+  if ((kFourWave & fw) && four_wave_ok(w_f16, asplit, rows, N, K))
     k_gemm_residual_4w<<<ln.blocks(), 256, 0, s>>>(A, static_cast<const uint16_t *>(W), rows, N, K,
                                                      ln, x, part);
   else
