@@ -1128,6 +1128,91 @@ __global__ __launch_bounds__(NT) void k_gemm_lmhead(const f16 *__restrict__ Hn,
   }
 }
 
+// The LM head on the four-wave tile (fp16 weights): the same transposed
+// product and partials, 128 vocabulary rows x 128 tokens per wave, so a
+// token's reduction runs down a lane's registers, across the lane halves and
+// across the two waves of a token column. The main loop fills all of LDS;
+// after a barrier its first 4 KB hold the cross-wave values.
+__global__ __launch_bounds__(256) void k_gemm_lmhead_4w(const f16 *__restrict__ Hn,
+                                                        const uint16_t *__restrict__ Wlm, int T,
+                                                        int vocab, int K, Launch ln,
+                                                        const int32_t *__restrict__ lm_tgt,
+                                                        float2 *__restrict__ part,
+                                                        float *__restrict__ tgt_logit) {
+  __shared__ u32x4 lds[10240];  // A: 2 stages, B: 3 stages of 32 KB
+  const Work wk = block_work(ln);
+  const int m0 = wk.tm * 256, n0 = wk.tn * 256;
+  f32x16 acc[4][4];
+  mainloop_4w(
+      Wlm, [=](int r) { return min(m0 + r, vocab - 1); }, Hn,
+      [=](int r) { return min(n0 + r, T - 1); }, K, 0, K / BK, lds, acc);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, wm = w >> 1, wn = w & 1;
+  float (*red)[256] = reinterpret_cast<float (*)[256]>(lds);  // [4][256]
+  __syncthreads();  // every wave is past its last LDS fragment reads
+  float mx[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float v = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (m0 + row_4w(wm, i, r, lane) < vocab) v = fmaxf(v, acc[i][j][r]);
+    v = fmaxf(v, __shfl_xor(v, 32, 64));
+    if (lane < 32) red[wm][wn * 128 + j * 32 + lane] = v;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int c = wn * 128 + j * 32 + (lane & 31);
+    mx[j] = fmaxf(red[0][c], red[1][c]);
+  }
+  __syncthreads();
+  // Sums of exp(l - max) per 64-row half of the wave, added in row order
+  // across the halves: the order of the 8-wave kernel (four waves of 64
+  // rows), so that fp16 and bf16 weight storage give bitwise equal scores.
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      float sum = 0.f;
+#pragma unroll
+      for (int i = 2 * hh; i < 2 * hh + 2; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (m0 + row_4w(wm, i, r, lane) < vocab) sum += __expf(acc[i][j][r] - mx[j]);
+      sum += __shfl_xor(sum, 32, 64);
+      if (lane < 32) red[2 * wm + hh][wn * 128 + j * 32 + lane] = sum;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int c = wn * 128 + j * 32 + (lane & 31);
+    const int t = n0 + c;
+    if (t >= T) continue;
+    if (wm == 0 && lane < 32) {
+      float sum = red[0][c];
+#pragma unroll
+      for (int q = 1; q < 4; ++q) sum += red[q][c];
+      part[(long)wk.tm * T + t] = make_float2(mx[j], sum);
+    }
+    // Target logit: row tr of this wave's 128 rows, held by lane half
+    // (tr / 4) % 2 in register 4 (tr % 32 / 8) + tr % 4 of block row tr / 32.
+    const int tr = lm_tgt[t] - m0 - wm * 128;
+    if (tr >= 0 && tr < 128 && ((tr >> 2) & 1) == (lane >> 5)) {
+      const int it = tr >> 5, w32 = tr & 31, rr = (w32 >> 3) * 4 + (w32 & 3);
+      float v = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (i == it && r == rr) v = acc[i][j][r];
+      tgt_logit[t] = v;
+    }
+  }
+}
+
 // Greedy variant of the LM head: per (vocab tile, token) the largest logit and
 // its vocabulary index (the lowest on ties), part[c][t] = (max, index bits).
 template <class TL, bool WCVT>
@@ -1203,12 +1288,13 @@ size_t gemm_split_floats(int rows, int N, int K) {
 }
 
 // Where the four-wave kernels run: bit 0 the gate/up projection, bit 1 the
-// residual projections with K >= kFourWaveMinK, bit 2 those with smaller K.
-// Building with VSR_FOUR_WAVE=<mask> changes it (for comparisons).
+// residual projections with K >= kFourWaveMinK, bit 2 those with smaller K,
+// bit 3 the LM head. Building with VSR_FOUR_WAVE=<mask> changes it (for
+// comparisons).
 #ifdef VSR_FOUR_WAVE
 constexpr int kFourWave = VSR_FOUR_WAVE;
 #else
-constexpr int kFourWave = 3;
+constexpr int kFourWave = 3 | 8;
 #endif
 constexpr int kFourWaveMinK = 8192;
 
@@ -1298,7 +1384,11 @@ hipError_t gemm_lmhead(const f16 *A, const void *W, bool w_f16, int rows, int vo
   // partials).
   const int nm = lmhead_chunks(vocab), nn = (rows + TL::BN - 1) / TL::BN;
   const Launch ln{nm, nn, 1, nm * nn, 0, 1};
-  VSR_WLAUNCH(k_gemm_lmhead, ln.blocks(), A, W16, rows, vocab, K, ln, lm_tgt, part, tgt_logit);
+  if ((kFourWave & 8) && four_wave_ok(w_f16, 1, vocab, rows, K))
+    k_gemm_lmhead_4w<<<ln.blocks(), 256, 0, s>>>(A, static_cast<const uint16_t *>(W), rows, vocab,
+                                                   K, ln, lm_tgt, part, tgt_logit);
+  else
+    VSR_WLAUNCH(k_gemm_lmhead, ln.blocks(), A, W16, rows, vocab, K, ln, lm_tgt, part, tgt_logit);
   return hipGetLastError();
 }
 
