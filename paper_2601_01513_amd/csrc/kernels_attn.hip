@@ -258,18 +258,16 @@ __device__ __forceinline__ float tile_max(const f32x16 (&s)[2]) {
   return fmaxf(fmaxf(fmaxf(b0, b1), b2), b3);
 }
 
-// Fast kernels: one 64-key tile against this wave's 32 query rows. The
-// queries arrive multiplied by log2(e) / sqrt(hd), so S^T is in log2 units,
-// and the products start from -m (L.negm), so the accumulators hold s - m
-// and each probability is one exp2. The reference m moves (the output is
-// rescaled) only when a tile's largest s - m exceeds 8, or at the first
-// visible key of a row. The row sum adds the fp16 probabilities that the PV
-// products use (v_dot2_f32_f16 against ones, fp32 accumulation).
-template <bool MASK>
-__device__ __forceinline__ void tile_step_fast(const Seg &sg, int kb, const u32x4 *st, Lane &L) {
+// Fast kernels: one 64-key tile against this wave's 32 query rows: the
+// scores, the probabilities and the PV products. The queries
+// arrive multiplied by log2(e) / sqrt(hd), so S^T is in log2 units, and the
+// products start from -m (L.negm), so the accumulators hold s - m and each
+// probability is one exp2. The reference m moves (the output is rescaled)
+// only when a tile's largest s - m exceeds 8, or at the first visible key of
+// a row. The row sum adds the fp16 probabilities that the PV products use
+// (v_dot2_f32_f16 against ones, fp32 accumulation).
+__device__ __forceinline__ void scores_fast(const u32x4 *Ks, const Lane &L, f32x16 (&s)[2]) {
   const int lane = threadIdx.x & 63, h = lane >> 5;
-  const u32x4 *Ks = st, *Vs = st + KCH;
-  f32x16 s[2];
 #pragma unroll
   for (int kk = 0; kk < HD / 16; ++kk) {
     const f16x8 qf = L.qh[kk];
@@ -279,18 +277,9 @@ __device__ __forceinline__ void tile_step_fast(const Seg &sg, int kb, const u32x
       s[b] = mfma(kf, qf, kk == 0 ? L.negm : s[b]);
     }
   }
-  if constexpr (MASK) {
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kb + b * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-        bool vis = key < sg.kvalid;
-        if (sg.mode == SEG_CAUSAL) vis = vis && key <= L.tok;
-        if (sg.mode == SEG_BRANCH) vis = vis && key >= L.lo && key <= L.tok;
-        s[b][r] = vis ? s[b][r] : -INFINITY;
-      }
-  }
+}
+
+__device__ __forceinline__ void probs_fast(f32x16 (&s)[2], Lane &L, f16x8 (&p)[4]) {
   // t and seen are the same in both lane halves of a query, so the two halves
   // move together and keep one reference.
   const float t = max_halves(tile_max(s));
@@ -312,7 +301,6 @@ __device__ __forceinline__ void tile_step_fast(const Seg &sg, int kb, const u32x
 #pragma unroll
     for (int db = 0; db < HD / 32; ++db) L.o[db] *= alpha;
   }
-  f16x8 p[4];
 #pragma unroll
   for (int b = 0; b < 2; ++b)
 #pragma unroll
@@ -328,6 +316,10 @@ __device__ __forceinline__ void tile_step_fast(const Seg &sg, int kb, const u32x
       ps[c] = __builtin_amdgcn_fdot2(f16x2{p[c][2 * e], p[c][2 * e + 1]}, one, ps[c], false);
   }
   L.l += (ps[0] + ps[1]) + (ps[2] + ps[3]);
+}
+
+__device__ __forceinline__ void pv_fast(const u32x4 *Vs, const f16x8 (&p)[4], Lane &L) {
+  const int lane = threadIdx.x & 63, h = lane >> 5;
 #pragma unroll
   for (int c = 0; c < 4; ++c)
 #pragma unroll
@@ -335,6 +327,46 @@ __device__ __forceinline__ void tile_step_fast(const Seg &sg, int kb, const u32x
       const f16x8 vf = as_f16x8(Vs[vs_idx(db * 32 + (lane & 31), 2 * c + h)]);
       L.o[db] = mfma(vf, p[c], L.o[db]);
     }
+}
+
+// Scheduling order of a run of NSTEP steps of two LDS fragment reads and the
+// two matrix products that use them: each step's reads are issued before the
+// previous step's products, so a wave's LDS latency overlaps its own
+// products (left to itself, the scheduler issues each pair of reads right
+// before its products and waits for them).
+template <int NSTEP>
+__device__ __forceinline__ void order_reads_ahead() {
+  __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // LDS reads
+#pragma unroll
+  for (int i = 1; i < NSTEP; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // matrix products
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+}
+
+template <bool MASK>
+__device__ __forceinline__ void tile_step_fast(const Seg &sg, int kb, const u32x4 *st, Lane &L) {
+  const int h = (threadIdx.x & 63) >> 5;
+  f32x16 s[2];
+  scores_fast(st, L, s);
+  order_reads_ahead<8>();
+  if constexpr (MASK) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kb + b * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        bool vis = key < sg.kvalid;
+        if (sg.mode == SEG_CAUSAL) vis = vis && key <= L.tok;
+        if (sg.mode == SEG_BRANCH) vis = vis && key >= L.lo && key <= L.tok;
+        s[b][r] = vis ? s[b][r] : -INFINITY;
+      }
+  }
+  f16x8 p[4];
+  probs_fast(s, L, p);
+  pv_fast(st + KCH, p, L);
+  order_reads_ahead<8>();
 }
 
 // One tile of either variant.
