@@ -602,6 +602,18 @@ __global__ __launch_bounds__(64 * NW) void k_attn_merge(AttnArgs a) {
   const int G = a.n_heads / a.n_kv, TG = a.T * G;
   const int kvh = head / G, row = t * G + head % G;
   const long r0 = (long)kvh * TG + row, cstride = (long)a.n_kv * TG;
+  // The first eight chunks' outputs are loaded together with the (max, sum)
+  // pairs: they do not depend on the weights.
+  float v0[8], v1[8];
+  const auto load8 = [&](int i0) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const long prow = min(w + NW * (i0 + j), a.nchunks - 1) * cstride + r0;
+      v0[j] = a.part_acc[prow * HD + lane];
+      v1[j] = a.part_acc[prow * HD + 64 + lane];
+    }
+  };
+  load8(0);
   const float2 ml = lane < a.nchunks ? a.part_ml[lane * cstride + r0]
                                      : make_float2(-INFINITY, 0.f);
   const float M = wave_max(ml.x);
@@ -609,13 +621,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_merge(AttnArgs a) {
   const float Lsum = wave_sum(ml.y * wl);
   float o0 = 0.f, o1 = 0.f;
   for (int i0 = 0; w + NW * i0 < a.nchunks; i0 += 8) {
-    float v0[8], v1[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const long prow = min(w + NW * (i0 + j), a.nchunks - 1) * cstride + r0;
-      v0[j] = a.part_acc[prow * HD + lane];
-      v1[j] = a.part_acc[prow * HD + 64 + lane];
-    }
+    if (i0 > 0) load8(i0);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int c = w + NW * (i0 + j);
