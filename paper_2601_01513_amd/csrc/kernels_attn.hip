@@ -243,18 +243,20 @@ __device__ __forceinline__ void tile_step(const Seg &sg, int kb, const u32x4 *st
 }
 
 // Largest of the 32 scores a lane holds for one tile, as a tree of 3-input
-// maxima (depth 4 instead of a chain of 16).
+// maxima (depth 4 instead of a chain of 16). All but one step take three
+// inputs: the compiler turns those into v_max3 as they are, but precedes a
+// two-input maximum with canonicalizing moves of both inputs (the two left
+// over from 32 inputs join a[9]).
 __device__ __forceinline__ float tile_max(const f32x16 (&s)[2]) {
-  float a[11];
+  float a[10];
 #pragma unroll
   for (int i = 0; i < 10; ++i) {
     const int j = 3 * i;
     a[i] = fmaxf(fmaxf(s[j >> 4][j & 15], s[(j + 1) >> 4][(j + 1) & 15]),
                  s[(j + 2) >> 4][(j + 2) & 15]);
   }
-  a[10] = fmaxf(s[1][14], s[1][15]);
   const float b0 = fmaxf(fmaxf(a[0], a[1]), a[2]), b1 = fmaxf(fmaxf(a[3], a[4]), a[5]);
-  const float b2 = fmaxf(fmaxf(a[6], a[7]), a[8]), b3 = fmaxf(a[9], a[10]);
+  const float b2 = fmaxf(fmaxf(a[6], a[7]), a[8]), b3 = fmaxf(fmaxf(a[9], s[1][14]), s[1][15]);
   return fmaxf(fmaxf(fmaxf(b0, b1), b2), b3);
 }
 
@@ -397,15 +399,26 @@ __device__ __forceinline__ void walk_segment(const Seg &sg, u32x4 *lds, Lane &L,
   // The mask-free tiles come first (tile_clear holds for a prefix of the
   // walk), so the two variants run in two loops: with one loop around both,
   // the fast kernels spilled about 20 registers inside it.
+  // The mask-free loop is unrolled by two, one copy per stage, so that the
+  // stage offset is an immediate of the LDS reads and their per-lane
+  // addresses stay in registers across tiles.
   int stage = 0;
   int kb = sg.kbeg;
-  for (; kb < sg.kend && tile_clear(sg, kb); kb += KT) {
-    u32x4 *cur = lds + stage * STAGE;
-    if (kb + KT < sg.kend) load_tile<PREC, DEC>(sg, kb + KT, lds + (stage ^ 1) * STAGE);
-    tile_any<false, PREC>(sg, kb, cur, L, scale_log2);
+  while (kb < sg.kend && tile_clear(sg, kb)) {
+    if (kb + KT < sg.kend) load_tile<PREC, DEC>(sg, kb + KT, lds + STAGE);
+    tile_any<false, PREC>(sg, kb, lds, L, scale_log2);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    stage ^= 1;
+    kb += KT;
+    if (!(kb < sg.kend && tile_clear(sg, kb))) {
+      stage = 1;
+      break;
+    }
+    if (kb + KT < sg.kend) load_tile<PREC, DEC>(sg, kb + KT, lds);
+    tile_any<false, PREC>(sg, kb, lds + STAGE, L, scale_log2);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    kb += KT;
   }
   for (; kb < sg.kend; kb += KT) {
     u32x4 *cur = lds + stage * STAGE;
