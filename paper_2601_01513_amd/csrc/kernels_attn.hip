@@ -467,8 +467,8 @@ __device__ __forceinline__ void walk_concat(const Seg &sp, const Seg &sb, int pr
 }
 
 // mode 0: prefill (causal over the prefix cache, one chunk, direct output);
-// mode 1: candidate pass (chunk blockIdx.z of the prefix; the last chunk also
-//         walks the candidates' own keys);
+// mode 1: candidate pass (chunk blockIdx.z of [prefix tiles | the
+//         candidates' own tiles]);
 // mode 2: draft pass (chunk blockIdx.z of the prefix + branch-cache tiles).
 template <int MODE, bool PREC, bool DEC = false>
 __global__ __launch_bounds__((Shape<PREC, DEC>::NT)) void k_attn(AttnArgs a) {
@@ -525,20 +525,26 @@ __global__ __launch_bounds__((Shape<PREC, DEC>::NT)) void k_attn(AttnArgs a) {
            PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.T, kb, ke, SEG_CAUSAL, tok_first};
     walk_segment<PREC, DEC>(sg, lds, L, scale_log2);
   } else if (MODE == 1) {
-    // Candidate pass: chunks of whole prefix tiles (the last one short); the
-    // last chunk also walks the branch keys from the block's first query's
-    // segment start to its last query (both non-decreasing in token order).
+    // Candidate pass: chunk `chunk` walks an even share of the block's tiles
+    // [prefix tiles | branch tiles], the branch tiles running from the
+    // block's first query's segment start to its last query (both
+    // non-decreasing in token order). (With the branch tiles all on the last
+    // chunk on top of an even share of the prefix, that chunk bounded the
+    // launch.)
     const int pre_t = (a.P + KT - 1) / KT;
-    const int ct = (pre_t + a.nchunks - 1) / a.nchunks;
-    const int kb = min(a.P, chunk * ct * KT), ke = min(a.P, (chunk + 1) * ct * KT);
+    const int lo = a.row_lo[tok_first] & ~(KT - 1);
+    const int tot = pre_t + (tok_last + 1 - lo + KT - 1) / KT;
+    const int c0 = (int)((long)tot * chunk / a.nchunks);
+    const int c1 = (int)((long)tot * (chunk + 1) / a.nchunks);
     Seg sp{a.k + koff, a.vt + koff, PREC ? a.k_lo + koff : nullptr,
-           PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.P, kb, ke, SEG_ALL, tok_first};
+           PREC ? a.vt_lo + koff : nullptr, a.kv_npos, a.P, min(a.P, c0 * KT),
+           min(a.P, min(c1, pre_t) * KT), SEG_ALL, tok_first};
     walk_segment<PREC, DEC>(sp, lds, L, scale_log2);
-    if (chunk == a.nchunks - 1) {
-      const int lo = a.row_lo[tok_first] & ~(KT - 1);
+    if (c1 > pre_t) {
+      const int b0 = max(c0, pre_t) - pre_t;
       Seg sb{a.bk + boff, a.bvt + boff, PREC ? a.bk_lo + boff : nullptr,
-             PREC ? a.bvt_lo + boff : nullptr, a.bk_npos, a.T, lo, tok_last + 1, SEG_BRANCH,
-             tok_first};
+             PREC ? a.bvt_lo + boff : nullptr, a.bk_npos, a.T, lo + b0 * KT,
+             min(tok_last + 1, lo + (c1 - pre_t) * KT), SEG_BRANCH, tok_first};
       walk_segment<PREC, DEC>(sb, lds, L, scale_log2);
     }
   } else {
