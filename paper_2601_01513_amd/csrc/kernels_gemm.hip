@@ -1339,13 +1339,11 @@ hipError_t gemm_swiglu(const f16 *A, const void *W, bool w_f16, int rows, int F,
                        int asplit, f16 *h, float *part, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   typedef TileStd TL;
-  // Row-tile groups of at most 6, evenly sized (18 row tiles: 3 x 6). Each
-  // XCD re-fetches the activation panels of a group's row tiles once per
-  // round and the weight panels once per group: on 4608 rows groups of 6
-  // miss L2 11% less than groups of 9 at the same speed (groups of 9 were
-  // 1.6% faster than groups of 8, which left a last group of 2).
+  // Row-tile groups of at most 9, evenly sized (16 row tiles: 2 x 8; 18: 2 x
+  // 9): measured 1.6% faster than groups of 8 on 4608 rows, where the last
+  // group of 2 row tiles shares its operand panels poorly.
   const int nm = (rows + TL::BM - 1) / TL::BM;
-  const int ng = (nm + 5) / 6;
+  const int ng = (nm + 8) / 9;
   const Launch ln = plan_launch(nm, (F + 127) / 128, (nm + ng - 1) / ng, K / BK * asplit);
   // The four-wave tile with the ordered K loop where it applies (same
   // tiles, same partial layout).
