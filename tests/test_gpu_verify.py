@@ -9,7 +9,8 @@ all layers precise; seven query heads per KV head; a pass small enough
 (prefix + candidate rows <= 32) for the few-row kernels; a one-row prefix
 with one one-token candidate, and with candidates inside one row tile; the fp32 and
 no-candidate-token fallbacks; the prefix state it leaves for later calls;
-argument errors. The full-size 7B-class pass (the benchmark's) is checked in
+argument errors; candidate tokens at the end of the vocabulary (the LM head's
+partial last tile). The full-size 7B-class pass (the benchmark's) is checked in
 test_gpu_parity.py next to the two-call pass.
 """
 import sys
@@ -39,6 +40,19 @@ def test_verify_small_bf16_ragged(seed, split):
 def test_verify_gqa7(seed, split):
     wl = _case(GQA7_BF16, seed, split=split)
     check(wl.cfg, run_gpu_verify(wl, split_layers=split), run_oracle(wl), wl.cand_len)
+
+
+def test_verify_targets_at_the_vocabulary_end():
+    """Candidate tokens among the last 300 vocabulary entries (vocab 1000: the
+    LM head's last 256-entry tile is partial), so the target logits come
+    from the partial tile and the full one before it, at every row offset."""
+    wl = _case(SMALL_BF16, 4, lens=[40, 17, 33, 40, 9])
+    vocab = wl.cfg.vocab
+    k = np.arange(wl.cand_ids.size).reshape(wl.cand_ids.shape)
+    wl.cand_ids = (vocab - 1 - (k * 7) % 300).astype(wl.cand_ids.dtype)
+    for m, n in enumerate(wl.cand_len):
+        wl.cand_ids[m, n:] = 0
+    check(wl.cfg, run_gpu_verify(wl), run_oracle(wl), wl.cand_len)
 
 
 def test_verify_agrees_with_prefill_and_score():
